@@ -1,0 +1,1266 @@
+// Host side of the FP-Sketch verifier library: the C ABI of include/fpsketch.h.
+//
+// Owns the hash rounds and bucket-sorted tables (Sec. III-B), the bucket-count rules and the
+// localization plan (Eq. 3-5, Sec. III-G), device workspaces, and the localization driver
+// (Algorithm 2 with Algorithm 1 per round).  Every arithmetic step over A, B and C runs in the
+// kernels of fpsk_kernels.hip; the host handles O(m^2) selection on the dirty path only.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <unordered_map>
+#include <unordered_set>
+#include <vector>
+
+#include "../../include/fpsketch.h"
+#include "fpsk_internal.h"
+
+using fpsk::kColTile;
+using fpsk::kThreads;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+fpsketch_status fail(fpsketch_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+#define FPSK_HIP(call)                                                                    \
+  do {                                                                                    \
+    hipError_t e_ = (call);                                                               \
+    if (e_ != hipSuccess) {                                                               \
+      return fail(e_ == hipErrorOutOfMemory ? FPSK_ENOMEM : FPSK_EHIP,                    \
+                  std::string(#call) + " failed: " + hipGetErrorString(e_));              \
+    }                                                                                     \
+  } while (0)
+
+#define FPSK_TRY(expr)                      \
+  do {                                      \
+    fpsketch_status s_ = (expr);            \
+    if (s_ != FPSK_OK) return s_;           \
+  } while (0)
+
+// ------------------------------------------------------------------------------------------
+// splitmix64 (Steele, Lea and Flood 2014; Vigna's reference mixer).  Output idx of the stream
+// whose state starts at `seed` is mix(seed + (idx + 1) * golden_gamma).
+
+constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+
+inline uint64_t sm_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+inline uint64_t sm_output(uint64_t seed, uint64_t idx) { return sm_mix(seed + (idx + 1) * kGamma); }
+
+// Hash of one side of one round: key = output (2 round + side) of the stream at `seed`;
+// index idx uses output idx of the stream at key; bucket = (x >> 32) * m >> 32; sign = bit 0.
+void hash_side(uint64_t seed, int round, int side, int64_t n, int m, int32_t* bucket,
+               int8_t* sign) {
+  const uint64_t key = sm_output(seed, 2ull * static_cast<uint64_t>(round) + side);
+  for (int64_t idx = 0; idx < n; ++idx) {
+    const uint64_t x = sm_output(key, static_cast<uint64_t>(idx));
+    bucket[idx] = static_cast<int32_t>(((x >> 32) * static_cast<uint64_t>(m)) >> 32);
+    sign[idx] = (x & 1ull) ? -1 : 1;
+  }
+}
+
+int64_t pow2_ceil(int64_t n) {
+  int64_t p = 1;
+  while (p < n) p *= 2;
+  return p;
+}
+
+// ------------------------------------------------------------------------------------------
+// Bucket-count rules (Sec. III-F, Eq. 3-5) and plan (Sec. III-G).
+
+double law_cf(fpsketch_dtype dt) { return dt == FPSK_F16 ? 0.19 * 1.76 : 0.19; }
+
+int32_t m_comb(const fpsketch_params& p) {
+  const double a = 3.0 * p.c_coll * p.delta_rc;
+  const double b = std::sqrt(3.0 * p.c_coll * p.s_budget);
+  return static_cast<int32_t>(std::ceil(std::max(a, b)));
+}
+
+int64_t m_max(int64_t n1, int64_t n3) {
+  const int64_t q = (n1 * n3) / 16;
+  int64_t r = static_cast<int64_t>(std::sqrt(static_cast<double>(q)));
+  while (r * r > q) --r;
+  while ((r + 1) * (r + 1) <= q) ++r;
+  return std::max<int64_t>(16, r);
+}
+
+// Eq. 3 noise over rms(C): c_f 2^-24 sqrt(n1 n3 n2) (n2/8192)^0.07 / m.
+double law_sigma_over_rms(int64_t n1, int64_t n2, int64_t n3, int64_t m, fpsketch_dtype dt) {
+  return law_cf(dt) * std::ldexp(1.0, -24) *
+         std::sqrt(static_cast<double>(n1) * static_cast<double>(n3) * static_cast<double>(n2)) *
+         std::pow(static_cast<double>(n2) / 8192.0, 0.07) / static_cast<double>(m);
+}
+
+int64_t m_start(int64_t n1, int64_t n2, int64_t n3, fpsketch_dtype dt, const fpsketch_params& p) {
+  // Eq. 4 at delta = rms(C) with target B* (rms(C) cancels), then Eq. 5.
+  const double v = static_cast<double>(std::max(n1, n3)) / p.b_star * law_cf(dt) *
+                   std::ldexp(1.0, -24) *
+                   std::sqrt(static_cast<double>(n1) * static_cast<double>(n3) *
+                             static_cast<double>(n2)) *
+                   std::pow(static_cast<double>(n2) / 8192.0, 0.07);
+  const int64_t mnum = static_cast<int64_t>(std::ceil(v));
+  const int64_t mc = m_comb(p);
+  return std::min(std::max<int64_t>({mc, mnum, 16}), std::max<int64_t>(mc, m_max(n1, n3)));
+}
+
+// Largest m with 4 (3 m^2 + 6 m n2) bytes within 2 GiB.
+int64_t m_mem(int64_t n2) {
+  auto fits = [n2](int64_t m) { return 4 * (3 * m * m + 6 * m * n2) <= (int64_t{1} << 31); };
+  int64_t lo = 0, hi = 1;
+  while (fits(hi)) hi *= 2;
+  while (hi - lo > 1) {
+    const int64_t mid = (lo + hi) / 2;
+    (fits(mid) ? lo : hi) = mid;
+  }
+  return lo;
+}
+
+bool positive_finite(double x) { return std::isfinite(x) && x > 0.0; }
+
+int32_t radius_rule(double B) {
+  if (B <= 0.05) return 0;
+  return std::max(2, static_cast<int32_t>(std::ceil(2.5 * B)));
+}
+
+struct PlanOut {
+  int32_t m_loc, r, fallback;
+  double B;
+};
+
+PlanOut plan_localize(int64_t n1, int64_t n2, int64_t n3, fpsketch_dtype dt, int32_t m,
+                      double sigma, double rms, const fpsketch_params& p) {
+  const double mx = static_cast<double>(std::max(n1, n3));
+  PlanOut o{};
+  o.fallback = !(positive_finite(sigma) && positive_finite(rms));
+  o.B = o.fallback ? mx * law_sigma_over_rms(n1, n2, n3, m, dt) / p.rho_min
+                   : mx * sigma / (p.rho_min * rms);
+  const int32_t rb = radius_rule(o.B);
+  if (rb <= p.r_star) {
+    o.m_loc = m;
+    o.r = rb;
+    return o;
+  }
+  const int64_t need = static_cast<int64_t>(
+      std::ceil(static_cast<double>(m) * static_cast<double>(rb) / static_cast<double>(p.r_star)));
+  const int64_t grown = 16 * ((need + 15) / 16);
+  const int64_t mloc = std::max<int64_t>(m, std::min({grown, m_max(n1, n3), m_mem(n2)}));
+  o.m_loc = static_cast<int32_t>(mloc);
+  const double b2 = o.B * static_cast<double>(m) / static_cast<double>(mloc);
+  o.r = b2 <= 0.05 ? 0
+                   : std::min(p.r_max, std::max(2, static_cast<int32_t>(std::ceil(2.5 * b2))));
+  return o;
+}
+
+void recalibrate(int64_t n1, int64_t n3, int32_t m, double sigma_bar, double rms,
+                 const fpsketch_params& p, int32_t* m_new, int32_t* rebuild) {
+  *m_new = m;
+  *rebuild = 0;
+  if (!(positive_finite(sigma_bar) && positive_finite(rms))) return;
+  const double b1 = static_cast<double>(std::max(n1, n3)) * sigma_bar / rms;
+  const int64_t want = static_cast<int64_t>(std::ceil(static_cast<double>(m) * b1 / p.b_star));
+  const int64_t mp = std::max<int64_t>({m_comb(p), 16, std::min(want, m_max(n1, n3))});
+  if (static_cast<double>(mp) < m / 1.25 || static_cast<double>(mp) > 1.25 * m) {
+    *m_new = static_cast<int32_t>(mp);
+    *rebuild = 1;
+  }
+}
+
+// Median with the even-count convention (mean of the two middle order statistics).
+double median_of(std::vector<double> v) {
+  const size_t n = v.size();
+  if (n == 0) return std::nan("");
+  const size_t h = n / 2;
+  std::nth_element(v.begin(), v.begin() + h, v.end());
+  const double hi = v[h];
+  if (n % 2) return hi;
+  const double lo = *std::max_element(v.begin(), v.begin() + h);
+  return 0.5 * (lo + hi);
+}
+
+double rms_hat_from_samples(const float* s, int64_t count) {
+  std::vector<double> a;
+  a.reserve(static_cast<size_t>(count));
+  for (int64_t t = 0; t < count; ++t) {
+    const double x = s[t];
+    if (std::isfinite(x)) a.push_back(std::fabs(x));
+  }
+  if (a.empty()) return std::nan("");
+  const double clip = 64.0 * median_of(a);
+  double acc = 0.0;
+  for (double x : a) {
+    const double c = std::min(x, clip);
+    acc += c * c;
+  }
+  return std::sqrt(acc / static_cast<double>(a.size()));
+}
+
+// ------------------------------------------------------------------------------------------
+// Tables of one hash round at one m.
+
+struct HostRound {
+  int m = 0;
+  std::vector<int32_t> h1, h2;
+  std::vector<int8_t> v1, v2;
+  std::vector<int32_t> perm1, off1, coff, boff;
+  std::vector<uint16_t> ctab, btab;
+};
+
+// Column tiles of width W sorted by bucket (stable in column order).
+void build_col_tables(const std::vector<int32_t>& h2, const std::vector<int8_t>& v2, int m,
+                      int64_t W, std::vector<uint16_t>& tab, std::vector<int32_t>& off) {
+  const int64_t n3 = static_cast<int64_t>(h2.size());
+  const int64_t T = (n3 + W - 1) / W;
+  tab.assign(static_cast<size_t>(T * W), 0);
+  off.assign(static_cast<size_t>(T * (m + 1)), 0);
+  std::vector<int32_t> cnt(static_cast<size_t>(m) + 1);
+  for (int64_t t = 0; t < T; ++t) {
+    const int64_t j0 = t * W, j1 = std::min(n3, j0 + W);
+    std::fill(cnt.begin(), cnt.end(), 0);
+    for (int64_t j = j0; j < j1; ++j) cnt[static_cast<size_t>(h2[j]) + 1]++;
+    for (int b = 0; b < m; ++b) cnt[b + 1] += cnt[b];
+    int32_t* o = off.data() + t * (m + 1);
+    for (int b = 0; b <= m; ++b) o[b] = cnt[b];
+    for (int64_t j = j0; j < j1; ++j) {
+      const int32_t pos = cnt[h2[j]]++;
+      tab[static_cast<size_t>(t * W + pos)] =
+          static_cast<uint16_t>((j - j0) | (v2[j] < 0 ? 0x8000 : 0));
+    }
+  }
+}
+
+void build_round(uint64_t seed, int round, int64_t n1, int64_t n3, int m, int64_t cwb,
+                 HostRound& R) {
+  R.m = m;
+  R.h1.resize(n1);
+  R.v1.resize(n1);
+  R.h2.resize(n3);
+  R.v2.resize(n3);
+  hash_side(seed, round, 0, n1, m, R.h1.data(), R.v1.data());
+  hash_side(seed, round, 1, n3, m, R.h2.data(), R.v2.data());
+  R.off1.assign(static_cast<size_t>(m) + 1, 0);
+  for (int64_t i = 0; i < n1; ++i) R.off1[static_cast<size_t>(R.h1[i]) + 1]++;
+  for (int b = 0; b < m; ++b) R.off1[b + 1] += R.off1[b];
+  std::vector<int32_t> pos(R.off1.begin(), R.off1.end() - 1);
+  R.perm1.resize(n1);
+  for (int64_t i = 0; i < n1; ++i) {
+    R.perm1[pos[R.h1[i]]++] =
+        static_cast<int32_t>(static_cast<uint32_t>(i) | (R.v1[i] < 0 ? 0x80000000u : 0u));
+  }
+  build_col_tables(R.h2, R.v2, m, kColTile, R.ctab, R.coff);
+  build_col_tables(R.h2, R.v2, m, cwb, R.btab, R.boff);
+}
+
+// ------------------------------------------------------------------------------------------
+// Device memory helpers.
+
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+};
+
+fpsketch_status dev_alloc(DevBuf& b, size_t bytes) {
+  if (b.p != nullptr && b.bytes >= bytes) return FPSK_OK;
+  if (b.p != nullptr) {
+    (void)hipFree(b.p);
+    b.p = nullptr;
+    b.bytes = 0;
+  }
+  if (bytes == 0) return FPSK_OK;
+  FPSK_HIP(hipMalloc(&b.p, bytes));
+  b.bytes = bytes;
+  return FPSK_OK;
+}
+
+void dev_free(DevBuf& b) {
+  if (b.p != nullptr) (void)hipFree(b.p);
+  b.p = nullptr;
+  b.bytes = 0;
+}
+
+template <typename T>
+T* as(DevBuf& b) {
+  return static_cast<T*>(b.p);
+}
+
+// Work decomposition of one sketch pass at bucket count m.
+struct Decomp {
+  int m = 0;
+  int TA = 0, nA = 0;
+  int rb = 8, g = 1, cwb = 2048, TB = 0, nB = 0;
+  int TC = 0, npc = 1, tg = 1, nC = 0;
+  int ts = 16, nt = 1, NS = 1, ksl = 0;
+  size_t lds_stream = 0;
+};
+
+Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
+  (void)n1;
+  Decomp d;
+  d.m = m;
+  d.TA = static_cast<int>((n2 + kColTile - 1) / kColTile);
+  d.nA = m * d.TA;
+  if (m <= 256) {
+    d.rb = 8, d.g = 1;
+  } else if (m <= 512) {
+    d.rb = 8, d.g = 2;
+  } else if (m <= 1024) {
+    d.rb = 4, d.g = 4;
+  } else if (m <= 2048) {
+    d.rb = 2, d.g = 8;
+  } else {
+    d.rb = 1, d.g = 16;
+  }
+  d.cwb = fpsk::kBChunkHalfs / d.rb;
+  d.TB = static_cast<int>((n3 + d.cwb - 1) / d.cwb);
+  d.nB = static_cast<int>((n2 + d.rb - 1) / d.rb);
+  d.TC = static_cast<int>((n3 + kColTile - 1) / kColTile);
+  int npc = static_cast<int>((1024 + m - 1) / m);
+  npc = std::max(1, std::min(npc, d.TC));
+  d.tg = (d.TC + npc - 1) / npc;
+  d.npc = (d.TC + d.tg - 1) / d.tg;
+  d.nC = m * d.npc;
+  d.ts = m <= 128 ? 16 : (m <= 512 ? 32 : 64);
+  d.nt = (m + d.ts - 1) / d.ts;
+  const int tiles = d.nt * d.nt;
+  int ns = (512 + tiles - 1) / tiles;
+  ns = std::max(1, std::min<int>(ns, static_cast<int>(std::max<int64_t>(1, n2 / 128))));
+  int ksl = static_cast<int>((n2 + ns - 1) / ns);
+  ksl = (ksl + 15) / 16 * 16;
+  d.ksl = ksl;
+  d.NS = static_cast<int>((n2 + ksl - 1) / ksl);
+  const size_t a_lds = (mom ? 4096 : 2048) * sizeof(double);
+  const size_t b_lds = static_cast<size_t>(fpsk::kBChunkHalfs) * sizeof(uint16_t);
+  const size_t c_lds = (mom ? 5120 : 2560) * sizeof(double);
+  d.lds_stream = std::max({a_lds, b_lds, c_lds});
+  return d;
+}
+
+struct DevRound {
+  int m = 0;
+  int64_t cwb = 0;
+  DevBuf perm1, off1, ctab, coff, btab, boff;
+};
+
+fpsketch_status upload_round(const HostRound& R, int64_t cwb, DevRound& D, hipStream_t st) {
+  D.m = R.m;
+  D.cwb = cwb;
+  auto up = [st](DevBuf& b, const void* src, size_t bytes) -> fpsketch_status {
+    FPSK_TRY(dev_alloc(b, bytes));
+    if (bytes) FPSK_HIP(hipMemcpyAsync(b.p, src, bytes, hipMemcpyHostToDevice, st));
+    return FPSK_OK;
+  };
+  FPSK_TRY(up(D.perm1, R.perm1.data(), R.perm1.size() * 4));
+  FPSK_TRY(up(D.off1, R.off1.data(), R.off1.size() * 4));
+  FPSK_TRY(up(D.ctab, R.ctab.data(), R.ctab.size() * 2));
+  FPSK_TRY(up(D.coff, R.coff.data(), R.coff.size() * 4));
+  FPSK_TRY(up(D.btab, R.btab.data(), R.btab.size() * 2));
+  FPSK_TRY(up(D.boff, R.boff.data(), R.boff.size() * 4));
+  // host vectors must outlive the asynchronous copies
+  FPSK_HIP(hipStreamSynchronize(st));
+  return FPSK_OK;
+}
+
+void free_round(DevRound& D) {
+  dev_free(D.perm1);
+  dev_free(D.off1);
+  dev_free(D.ctab);
+  dev_free(D.coff);
+  dev_free(D.btab);
+  dev_free(D.boff);
+}
+
+struct Workspace {
+  Decomp d;
+  bool mom = false;
+  DevBuf P, Pw, Q, Qw, partS, partR, partT, scratch, S, R, T, maxpart, tile_cnt, glob_cnt,
+      tilestat;
+};
+
+fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n3, int m,
+                                 bool mom) {
+  const Decomp d = decompose(n1, n2, n3, m, mom);
+  W.d = d;
+  W.mom = mom;
+  const size_t fm = static_cast<size_t>(m) * static_cast<size_t>(n2) * sizeof(float);
+  const size_t mm = static_cast<size_t>(m) * static_cast<size_t>(m) * sizeof(double);
+  FPSK_TRY(dev_alloc(W.P, fm));
+  FPSK_TRY(dev_alloc(W.Q, fm));
+  FPSK_TRY(dev_alloc(W.partS, mm * d.npc));
+  FPSK_TRY(dev_alloc(W.S, mm));
+  if (mom) {
+    FPSK_TRY(dev_alloc(W.Pw, fm));
+    FPSK_TRY(dev_alloc(W.Qw, fm));
+    FPSK_TRY(dev_alloc(W.partR, mm * d.npc));
+    FPSK_TRY(dev_alloc(W.partT, mm * d.npc));
+    FPSK_TRY(dev_alloc(W.R, mm));
+    FPSK_TRY(dev_alloc(W.T, mm));
+  }
+  const int tiles = d.nt * d.nt;
+  const size_t sc = d.NS > 1 ? static_cast<size_t>(d.NS) * tiles * d.ts * d.ts * (mom ? 3 : 1) *
+                                   sizeof(double)
+                             : 0;
+  FPSK_TRY(dev_alloc(W.scratch, sc));
+  FPSK_TRY(dev_alloc(W.maxpart, static_cast<size_t>(d.nA + d.nB) * sizeof(float)));
+  // counters: allocated zeroed once; the kernels leave them at zero after every launch
+  const size_t cnt_bytes = static_cast<size_t>(tiles) * sizeof(uint32_t);
+  if (W.tile_cnt.bytes < cnt_bytes) {
+    FPSK_TRY(dev_alloc(W.tile_cnt, cnt_bytes));
+    FPSK_HIP(hipMemset(W.tile_cnt.p, 0, cnt_bytes));
+  }
+  if (W.glob_cnt.p == nullptr) {
+    FPSK_TRY(dev_alloc(W.glob_cnt, sizeof(uint32_t)));
+    FPSK_HIP(hipMemset(W.glob_cnt.p, 0, sizeof(uint32_t)));
+  }
+  FPSK_TRY(dev_alloc(W.tilestat, static_cast<size_t>(tiles) * 4 * sizeof(double)));
+  return FPSK_OK;
+}
+
+void free_workspace(Workspace& W) {
+  for (DevBuf* b : {&W.P, &W.Pw, &W.Q, &W.Qw, &W.partS, &W.partR, &W.partT, &W.scratch, &W.S,
+                    &W.R, &W.T, &W.maxpart, &W.tile_cnt, &W.glob_cnt, &W.tilestat}) {
+    dev_free(*b);
+  }
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------------
+// Context.
+
+struct fpsketch_ctx {
+  int64_t n1 = 0, n2 = 0, n3 = 0;
+  fpsketch_dtype dt = FPSK_BF16;
+  fpsketch_params p{};
+  int device = 0;
+  int m = 0;
+  double inv_l1 = 1.0, inv_l3 = 1.0;
+  int64_t L1 = 1, L3 = 1;
+  // probe: hash round 0 of the context seed at m
+  DevRound probe_round;
+  Workspace probe_ws;
+  DevBuf stats;       // 8 doubles
+  DevBuf sigma_acc;   // 2 doubles
+  // localize / diagnostic workspaces
+  DevRound aux_round;
+  Workspace aux_ws;
+  DevBuf scan_counts, scan_rows, scan_base, scan_out, samples, patch_rowptr, patch_col,
+      patch_val, rc_coords, rc_gamma, rc_abs, rc_c;
+  fpsketch_plan_info last_plan{};
+  // optional per-probe event triples around the stream and product kernels
+  bool timing = false;
+  std::vector<hipEvent_t> events;
+  size_t events_used = 0;
+};
+
+namespace {
+
+bool valid_half(fpsketch_dtype d) { return d == FPSK_F16 || d == FPSK_BF16; }
+
+fpsketch_status check_params(const fpsketch_params& p) {
+  if (p.m < 0 || p.rounds < 1 || p.r_star < 0 || p.r_max < 0 || p.s_budget < 1 ||
+      p.delta_rc < 1 || p.k_cap < 0 || !(p.rho_min > 0) || !(p.mu > 0) || !(p.c_valid > 0) ||
+      !(p.b_star > 0) || !(p.c_coll > 0)) {
+    return fail(FPSK_EINVAL, "parameter out of range");
+  }
+  return FPSK_OK;
+}
+
+int32_t cap_K(const fpsketch_params& p) {
+  return p.k_cap > 0 ? p.k_cap : std::max(64, 8 * p.s_budget);
+}
+
+fpsketch_status set_device(const fpsketch_ctx* c) {
+  FPSK_HIP(hipSetDevice(c->device));
+  return FPSK_OK;
+}
+
+// One sketch pass (stream + product) on `st`.
+fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const void* A,
+                         const void* B, const float* Cm, bool mom, int mode, int32_t* d_dirty,
+                         const int32_t* prow, const int32_t* pcol, const float* pval,
+                         hipStream_t st, hipEvent_t* ev = nullptr) {
+  const Decomp& d = W.d;
+  fpsk::StreamArgs s{};
+  s.A = static_cast<const uint16_t*>(A);
+  s.B = static_cast<const uint16_t*>(B);
+  s.C = Cm;
+  s.n1 = c->n1;
+  s.n2 = c->n2;
+  s.n3 = c->n3;
+  s.m = d.m;
+  s.perm1 = static_cast<const int32_t*>(R.perm1.p);
+  s.off1 = static_cast<const int32_t*>(R.off1.p);
+  s.ctab = static_cast<const uint16_t*>(R.ctab.p);
+  s.coff = static_cast<const int32_t*>(R.coff.p);
+  s.btab = static_cast<const uint16_t*>(R.btab.p);
+  s.boff = static_cast<const int32_t*>(R.boff.p);
+  s.cwb = d.cwb;
+  s.P = as<float>(W.P);
+  s.Pw = mom ? as<float>(W.Pw) : nullptr;
+  s.Q = as<float>(W.Q);
+  s.Qw = mom ? as<float>(W.Qw) : nullptr;
+  s.partS = as<double>(W.partS);
+  s.partR = mom ? as<double>(W.partR) : nullptr;
+  s.partT = mom ? as<double>(W.partT) : nullptr;
+  s.maxpart = as<float>(W.maxpart);
+  s.patch_rowptr = prow;
+  s.patch_col = pcol;
+  s.patch_val = pval;
+  s.nA = d.nA;
+  s.nB = d.nB;
+  s.nC = d.nC;
+  s.TA = d.TA;
+  s.TC = d.TC;
+  s.TB = d.TB;
+  s.npc = d.npc;
+  s.tg = d.tg;
+  s.inv_l1 = c->inv_l1;
+  s.inv_l3 = c->inv_l3;
+  auto aligned16 = [](const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; };
+  s.vec_a = (c->n2 % 8 == 0) && aligned16(A);
+  s.vec_b = (c->n3 % 8 == 0) && aligned16(B);
+  s.vec_c = (c->n3 % 4 == 0) && aligned16(Cm);
+  if (R.cwb != d.cwb || R.m != d.m) return fail(FPSK_EINVAL, "internal: tables do not match");
+  if (ev) FPSK_HIP(hipEventRecord(ev[0], st));
+  FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.lds_stream, st));
+  if (ev) FPSK_HIP(hipEventRecord(ev[1], st));
+
+  fpsk::ProductArgs a{};
+  a.P = s.P;
+  a.Pw = s.Pw;
+  a.Q = s.Q;
+  a.Qw = s.Qw;
+  a.partS = s.partS;
+  a.partR = s.partR;
+  a.partT = s.partT;
+  a.S = as<double>(W.S);
+  a.R = mom ? as<double>(W.R) : nullptr;
+  a.T = mom ? as<double>(W.T) : nullptr;
+  a.scratch = as<double>(W.scratch);
+  a.tile_cnt = as<uint32_t>(W.tile_cnt);
+  a.glob_cnt = as<uint32_t>(W.glob_cnt);
+  a.tilestat = as<double>(W.tilestat);
+  a.m = d.m;
+  a.n2 = static_cast<int>(c->n2);
+  a.nt = d.nt;
+  a.NS = d.NS;
+  a.ksl = d.ksl;
+  a.npc = d.npc;
+  a.mode = mode;
+  a.maxpart = s.maxpart;
+  a.nA = d.nA;
+  a.nB = d.nB;
+  a.stats = as<double>(c->stats);
+  a.d_dirty = d_dirty;
+  a.sigma_acc = as<double>(c->sigma_acc);
+  a.mu = c->p.mu;
+  a.c_valid = c->p.c_valid;
+  FPSK_HIP(fpsk::launch_product(a, d.ts, mom, st));
+  if (ev) FPSK_HIP(hipEventRecord(ev[2], st));
+  return FPSK_OK;
+}
+
+fpsketch_status build_probe(fpsketch_ctx* c, int m, hipStream_t st) {
+  HostRound R;
+  const Decomp d = decompose(c->n1, c->n2, c->n3, m, false);
+  build_round(c->p.seed, 0, c->n1, c->n3, m, d.cwb, R);
+  FPSK_TRY(upload_round(R, d.cwb, c->probe_round, st));
+  FPSK_TRY(ensure_workspace(c->probe_ws, c->n1, c->n2, c->n3, m, false));
+  c->m = m;
+  return FPSK_OK;
+}
+
+fpsketch_status check_matrices(const fpsketch_ctx* c, const void* A, const void* B,
+                               const void* C, fpsketch_dtype c_dtype) {
+  if (c == nullptr) return fail(FPSK_EINVAL, "null context");
+  if (c_dtype != FPSK_F32) {
+    return fail(FPSK_EDTYPE, "C must be delivered in FP32 (a narrowed product is rejected)");
+  }
+  if (A == nullptr || B == nullptr || C == nullptr) return fail(FPSK_EINVAL, "null matrix");
+  return FPSK_OK;
+}
+
+// rms-hat(C): strided samples on the device, statistics on the host (Sec. III-G).
+fpsketch_status rms_hat_device(fpsketch_ctx* c, const float* C, hipStream_t st, double* out) {
+  const int64_t total = c->n1 * c->n3;
+  const int64_t stride = std::max<int64_t>(1, total / 65536);
+  const int64_t count = (total + stride - 1) / stride;
+  FPSK_TRY(dev_alloc(c->samples, static_cast<size_t>(count) * sizeof(float)));
+  FPSK_HIP(fpsk::launch_sample(C, stride, count, as<float>(c->samples), st));
+  std::vector<float> h(static_cast<size_t>(count));
+  FPSK_HIP(hipMemcpyAsync(h.data(), c->samples.p, h.size() * sizeof(float),
+                          hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  *out = rms_hat_from_samples(h.data(), count);
+  return FPSK_OK;
+}
+
+// Recheck a list of coordinates: gamma, sum |A||B| and C_ij.
+fpsketch_status recheck_coords(fpsketch_ctx* c, const void* A, const void* B, const float* C,
+                               const std::vector<int64_t>& coords, std::vector<double>& gamma,
+                               std::vector<double>& abssum, std::vector<float>& cval,
+                               hipStream_t st) {
+  const int n = static_cast<int>(coords.size() / 2);
+  gamma.assign(n, 0.0);
+  abssum.assign(n, 0.0);
+  cval.assign(n, 0.0f);
+  if (n == 0) return FPSK_OK;
+  FPSK_TRY(dev_alloc(c->rc_coords, coords.size() * sizeof(int64_t)));
+  FPSK_TRY(dev_alloc(c->rc_gamma, n * sizeof(double)));
+  FPSK_TRY(dev_alloc(c->rc_abs, n * sizeof(double)));
+  FPSK_TRY(dev_alloc(c->rc_c, n * sizeof(float)));
+  FPSK_HIP(hipMemcpyAsync(c->rc_coords.p, coords.data(), coords.size() * sizeof(int64_t),
+                          hipMemcpyHostToDevice, st));
+  FPSK_HIP(fpsk::launch_recheck(static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B),
+                                C, c->n2, c->n3, c->dt == FPSK_BF16 ? 1 : 0,
+                                as<int64_t>(c->rc_coords), n, as<double>(c->rc_gamma),
+                                as<double>(c->rc_abs), as<float>(c->rc_c), st));
+  FPSK_HIP(hipMemcpyAsync(gamma.data(), c->rc_gamma.p, n * sizeof(double), hipMemcpyDeviceToHost,
+                          st));
+  FPSK_HIP(hipMemcpyAsync(abssum.data(), c->rc_abs.p, n * sizeof(double), hipMemcpyDeviceToHost,
+                          st));
+  FPSK_HIP(hipMemcpyAsync(cval.data(), c->rc_c.p, n * sizeof(float), hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  return FPSK_OK;
+}
+
+// Exact scan (Sec. III-I): first K entries in row-major order that are non-finite or above
+// fp32max/16 in magnitude.
+fpsketch_status exact_scan(fpsketch_ctx* c, const float* C, int32_t K, hipStream_t st,
+                           std::vector<int64_t>& coords) {
+  coords.clear();
+  FPSK_TRY(dev_alloc(c->scan_counts, static_cast<size_t>(c->n1) * sizeof(int32_t)));
+  FPSK_HIP(fpsk::launch_scan_count(C, c->n1, c->n3, as<int32_t>(c->scan_counts), st));
+  std::vector<int32_t> counts(static_cast<size_t>(c->n1));
+  FPSK_HIP(hipMemcpyAsync(counts.data(), c->scan_counts.p, counts.size() * sizeof(int32_t),
+                          hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  std::vector<int32_t> rows, base;
+  int64_t total = 0;
+  for (int64_t i = 0; i < c->n1 && total < K; ++i) {
+    if (counts[i] > 0) {
+      rows.push_back(static_cast<int32_t>(i));
+      base.push_back(static_cast<int32_t>(total));
+      total += counts[i];
+    }
+  }
+  if (rows.empty()) return FPSK_OK;
+  const int32_t keep = static_cast<int32_t>(std::min<int64_t>(total, K));
+  FPSK_TRY(dev_alloc(c->scan_rows, rows.size() * sizeof(int32_t)));
+  FPSK_TRY(dev_alloc(c->scan_base, base.size() * sizeof(int32_t)));
+  FPSK_TRY(dev_alloc(c->scan_out, static_cast<size_t>(keep) * 2 * sizeof(int64_t)));
+  FPSK_HIP(hipMemcpyAsync(c->scan_rows.p, rows.data(), rows.size() * sizeof(int32_t),
+                          hipMemcpyHostToDevice, st));
+  FPSK_HIP(hipMemcpyAsync(c->scan_base.p, base.data(), base.size() * sizeof(int32_t),
+                          hipMemcpyHostToDevice, st));
+  FPSK_HIP(fpsk::launch_scan_extract(C, c->n3, as<int32_t>(c->scan_rows),
+                                     as<int32_t>(c->scan_base), static_cast<int>(rows.size()),
+                                     keep, as<int64_t>(c->scan_out), st));
+  coords.resize(static_cast<size_t>(keep) * 2);
+  FPSK_HIP(hipMemcpyAsync(coords.data(), c->scan_out.p, coords.size() * sizeof(int64_t),
+                          hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  return FPSK_OK;
+}
+
+// Sketches of one round into host arrays (S always; R, T with moments).
+fpsketch_status sketch_round(fpsketch_ctx* c, uint64_t seed, int round, int m, bool mom,
+                             const void* A, const void* B, const float* C, const int32_t* prow,
+                             const int32_t* pcol, const float* pval, hipStream_t st,
+                             HostRound& HR, std::vector<double>& S, std::vector<double>& Rm,
+                             std::vector<double>& T, double* maxA, double* maxB) {
+  const Decomp d = decompose(c->n1, c->n2, c->n3, m, mom);
+  build_round(seed, round, c->n1, c->n3, m, d.cwb, HR);
+  FPSK_TRY(upload_round(HR, d.cwb, c->aux_round, st));
+  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, mom));
+  FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, C, mom, 0, nullptr, prow, pcol, pval, st));
+  const size_t mm = static_cast<size_t>(m) * static_cast<size_t>(m);
+  S.resize(mm);
+  FPSK_HIP(hipMemcpyAsync(S.data(), c->aux_ws.S.p, mm * sizeof(double), hipMemcpyDeviceToHost,
+                          st));
+  if (mom) {
+    Rm.resize(mm);
+    T.resize(mm);
+    FPSK_HIP(hipMemcpyAsync(Rm.data(), c->aux_ws.R.p, mm * sizeof(double),
+                            hipMemcpyDeviceToHost, st));
+    FPSK_HIP(hipMemcpyAsync(T.data(), c->aux_ws.T.p, mm * sizeof(double),
+                            hipMemcpyDeviceToHost, st));
+  }
+  std::vector<float> mp(static_cast<size_t>(d.nA + d.nB));
+  FPSK_HIP(hipMemcpyAsync(mp.data(), c->aux_ws.maxpart.p, mp.size() * sizeof(float),
+                          hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  float ma = 0.0f, mb = 0.0f;
+  for (int i = 0; i < d.nA; ++i) ma = std::fmax(ma, mp[i]);
+  for (int i = 0; i < d.nB; ++i) mb = std::fmax(mb, mp[d.nA + i]);
+  if (maxA) *maxA = ma;
+  if (maxB) *maxB = mb;
+  return FPSK_OK;
+}
+
+double mad_sigma(const std::vector<double>& S) {
+  const double med = median_of(S);
+  std::vector<double> dev(S.size());
+  for (size_t i = 0; i < S.size(); ++i) dev[i] = std::fabs(S[i] - med);
+  return 1.4826 * median_of(dev);
+}
+
+struct Found {
+  int64_t i, j;
+  double delta;
+  int absolute;
+  int round;
+};
+
+}  // namespace
+
+// ==========================================================================================
+// C ABI.
+
+extern "C" {
+
+void fpsketch_default_params(fpsketch_params* p) {
+  if (p == nullptr) return;
+  std::memset(p, 0, sizeof(*p));
+  p->m = 0;
+  p->rounds = 3;
+  p->r_star = 4;
+  p->r_max = 16;
+  p->s_budget = 16;
+  p->delta_rc = 8;
+  p->k_cap = 0;
+  p->rho_min = 0.02;
+  p->mu = 4.0;
+  p->c_valid = 100.0;
+  p->b_star = 0.3;
+  p->c_coll = 2.0;
+  p->seed = 0x5EED5EEDull;
+}
+
+const char* fpsketch_status_str(fpsketch_status s) {
+  switch (s) {
+    case FPSK_OK: return "ok";
+    case FPSK_EINVAL: return "invalid argument";
+    case FPSK_EDTYPE: return "unsupported dtype (C must be FP32; A, B FP16 or BF16)";
+    case FPSK_ESHAPE: return "unsupported shape or bucket count";
+    case FPSK_ENOMEM: return "device out of memory";
+    case FPSK_EHIP: return "HIP runtime error";
+    case FPSK_ECAPACITY: return "more fault records than capacity";
+    case FPSK_ENODEV: return "no gfx950 device";
+  }
+  return "unknown status";
+}
+
+const char* fpsketch_last_error(void) { return g_last_error.c_str(); }
+
+fpsketch_status fpsketch_hash_table(uint64_t seed, int32_t round, int32_t side, int64_t n,
+                                    int32_t m, int32_t* bucket, int8_t* sign) {
+  if (bucket == nullptr || sign == nullptr || n < 0 || m < 1 || round < 0 || side < 0 ||
+      side > 1) {
+    return fail(FPSK_EINVAL, "fpsketch_hash_table: bad argument");
+  }
+  hash_side(seed, round, side, n, m, bucket, sign);
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_m_start(int64_t n1, int64_t n2, int64_t n3, fpsketch_dtype ab_dtype,
+                                 const fpsketch_params* params, int32_t* m_out) {
+  fpsketch_params p;
+  fpsketch_default_params(&p);
+  if (params) p = *params;
+  if (m_out == nullptr || n1 < 1 || n2 < 1 || n3 < 1) return fail(FPSK_EINVAL, "bad argument");
+  if (!valid_half(ab_dtype)) return fail(FPSK_EDTYPE, "A, B must be FP16 or BF16");
+  FPSK_TRY(check_params(p));
+  *m_out = static_cast<int32_t>(m_start(n1, n2, n3, ab_dtype, p));
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_plan_host(int64_t n1, int64_t n2, int64_t n3, fpsketch_dtype ab_dtype,
+                                   int32_t m, double sigma_hat, double rms,
+                                   const fpsketch_params* params, int32_t* m_loc, int32_t* r,
+                                   double* B, int32_t* fallback) {
+  fpsketch_params p;
+  fpsketch_default_params(&p);
+  if (params) p = *params;
+  if (m_loc == nullptr || r == nullptr || n1 < 1 || n2 < 1 || n3 < 1 || m < 1) {
+    return fail(FPSK_EINVAL, "bad argument");
+  }
+  if (!valid_half(ab_dtype)) return fail(FPSK_EDTYPE, "A, B must be FP16 or BF16");
+  FPSK_TRY(check_params(p));
+  const PlanOut o = plan_localize(n1, n2, n3, ab_dtype, m, sigma_hat, rms, p);
+  *m_loc = o.m_loc;
+  *r = o.r;
+  if (B) *B = o.B;
+  if (fallback) *fallback = o.fallback;
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_recalibrate_host(int64_t n1, int64_t n3, int32_t m, double sigma_bar,
+                                          double rms, const fpsketch_params* params,
+                                          int32_t* m_new, int32_t* rebuild) {
+  fpsketch_params p;
+  fpsketch_default_params(&p);
+  if (params) p = *params;
+  if (m_new == nullptr || rebuild == nullptr || n1 < 1 || n3 < 1 || m < 1) {
+    return fail(FPSK_EINVAL, "bad argument");
+  }
+  FPSK_TRY(check_params(p));
+  recalibrate(n1, n3, m, sigma_bar, rms, p, m_new, rebuild);
+  return FPSK_OK;
+}
+
+double fpsketch_rms_hat_samples(const float* samples, int64_t count) {
+  if (samples == nullptr || count <= 0) return std::nan("");
+  return rms_hat_from_samples(samples, count);
+}
+
+fpsketch_status fpsketch_create(int64_t n1, int64_t n2, int64_t n3, fpsketch_dtype ab_dtype,
+                                const fpsketch_params* params, fpsketch_ctx** out) {
+  if (out == nullptr) return fail(FPSK_EINVAL, "null output pointer");
+  *out = nullptr;
+  if (!valid_half(ab_dtype)) return fail(FPSK_EDTYPE, "A, B must be FP16 or BF16");
+  const int64_t lim = int64_t{1} << 31;
+  if (n1 < 1 || n2 < 1 || n3 < 1 || n1 >= lim || n2 >= lim || n3 >= lim) {
+    return fail(FPSK_ESHAPE, "dimensions must be in [1, 2^31)");
+  }
+  fpsketch_params p;
+  fpsketch_default_params(&p);
+  if (params) p = *params;
+  FPSK_TRY(check_params(p));
+  int dev = 0;
+  FPSK_HIP(hipGetDevice(&dev));
+  hipDeviceProp_t prop;
+  FPSK_HIP(hipGetDeviceProperties(&prop, dev));
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) {
+    return fail(FPSK_ENODEV, std::string("device is ") + prop.gcnArchName + ", not gfx950");
+  }
+  const int64_t m = p.m > 0 ? p.m : m_start(n1, n2, n3, ab_dtype, p);
+  if (m < 1 || m > fpsk::kMaxM) return fail(FPSK_ESHAPE, "bucket count outside [1, 4096]");
+  auto* c = new fpsketch_ctx();
+  c->n1 = n1;
+  c->n2 = n2;
+  c->n3 = n3;
+  c->dt = ab_dtype;
+  c->p = p;
+  c->device = dev;
+  c->L1 = pow2_ceil(n1);
+  c->L3 = pow2_ceil(n3);
+  c->inv_l1 = 1.0 / static_cast<double>(c->L1);
+  c->inv_l3 = 1.0 / static_cast<double>(c->L3);
+  fpsketch_status s = dev_alloc(c->stats, 8 * sizeof(double));
+  if (s == FPSK_OK) s = dev_alloc(c->sigma_acc, 2 * sizeof(double));
+  if (s == FPSK_OK) {
+    hipError_t e = hipMemset(c->stats.p, 0, 8 * sizeof(double));
+    if (e == hipSuccess) e = hipMemset(c->sigma_acc.p, 0, 2 * sizeof(double));
+    if (e != hipSuccess) s = fail(FPSK_EHIP, std::string("hipMemset: ") + hipGetErrorString(e));
+  }
+  if (s == FPSK_OK) s = build_probe(c, static_cast<int>(m), nullptr);
+  if (s != FPSK_OK) {
+    fpsketch_destroy(c);
+    return s;
+  }
+  *out = c;
+  return FPSK_OK;
+}
+
+void fpsketch_destroy(fpsketch_ctx* c) {
+  if (c == nullptr) return;
+  (void)hipSetDevice(c->device);
+  (void)hipDeviceSynchronize();
+  for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
+  free_round(c->probe_round);
+  free_workspace(c->probe_ws);
+  free_round(c->aux_round);
+  free_workspace(c->aux_ws);
+  for (DevBuf* b : {&c->stats, &c->sigma_acc, &c->scan_counts, &c->scan_rows, &c->scan_base,
+                    &c->scan_out, &c->samples, &c->patch_rowptr, &c->patch_col, &c->patch_val,
+                    &c->rc_coords, &c->rc_gamma, &c->rc_abs, &c->rc_c}) {
+    dev_free(*b);
+  }
+  delete c;
+}
+
+fpsketch_status fpsketch_probe(fpsketch_ctx* c, const void* A, const void* B, const void* C,
+                               fpsketch_dtype c_dtype, int32_t* d_dirty, void* stream) {
+  FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  hipEvent_t* ev = nullptr;
+  if (c->timing) {
+    while (c->events.size() < c->events_used + 3) {
+      hipEvent_t e;
+      FPSK_HIP(hipEventCreate(&e));
+      c->events.push_back(e);
+    }
+    ev = c->events.data() + c->events_used;
+    c->events_used += 3;
+  }
+  return run_pass(c, c->probe_round, c->probe_ws, A, B, static_cast<const float*>(C), false, 1,
+                  d_dirty, nullptr, nullptr, nullptr, st, ev);
+}
+
+fpsketch_status fpsketch_timing(fpsketch_ctx* c, int32_t enable) {
+  if (c == nullptr) return fail(FPSK_EINVAL, "null context");
+  c->timing = enable != 0;
+  c->events_used = 0;
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_timing_read(fpsketch_ctx* c, double* stream_ms, double* product_ms,
+                                     int64_t* calls) {
+  if (c == nullptr || stream_ms == nullptr || product_ms == nullptr || calls == nullptr) {
+    return fail(FPSK_EINVAL, "null argument");
+  }
+  FPSK_TRY(set_device(c));
+  double s1 = 0.0, s2 = 0.0;
+  const size_t n = c->events_used / 3;
+  if (n > 0) FPSK_HIP(hipEventSynchronize(c->events[3 * n - 1]));
+  for (size_t k = 0; k < n; ++k) {
+    float a = 0.0f, b = 0.0f;
+    FPSK_HIP(hipEventElapsedTime(&a, c->events[3 * k], c->events[3 * k + 1]));
+    FPSK_HIP(hipEventElapsedTime(&b, c->events[3 * k + 1], c->events[3 * k + 2]));
+    s1 += a;
+    s2 += b;
+  }
+  *stream_ms = s1;
+  *product_ms = s2;
+  *calls = static_cast<int64_t>(n);
+  c->events_used = 0;
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_get_m(fpsketch_ctx* c, int32_t* m_out) {
+  if (c == nullptr || m_out == nullptr) return fail(FPSK_EINVAL, "null argument");
+  *m_out = c->m;
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_probe_stats(fpsketch_ctx* c, double* out, void* stream) {
+  if (c == nullptr || out == nullptr) return fail(FPSK_EINVAL, "null argument");
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_HIP(hipMemcpyAsync(out, c->stats.p, 8 * sizeof(double), hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_get_plan(fpsketch_ctx* c, fpsketch_plan_info* out) {
+  if (c == nullptr || out == nullptr) return fail(FPSK_EINVAL, "null argument");
+  *out = c->last_plan;
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_sketch(fpsketch_ctx* c, const void* A, const void* B, const void* C,
+                                fpsketch_dtype c_dtype, uint64_t seed, int32_t round, int32_t m,
+                                int32_t moments, double* S, double* R, double* T, double* maxab,
+                                void* stream) {
+  FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
+  if (S == nullptr || (moments && (R == nullptr || T == nullptr)) || round < 0) {
+    return fail(FPSK_EINVAL, "null output or bad round");
+  }
+  if (m < 1 || m > fpsk::kMaxM) return fail(FPSK_ESHAPE, "bucket count outside [1, 4096]");
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  HostRound HR;
+  std::vector<double> hS, hR, hT;
+  double ma = 0, mb = 0;
+  FPSK_TRY(sketch_round(c, seed, round, m, moments != 0, A, B, static_cast<const float*>(C),
+                        nullptr, nullptr, nullptr, st, HR, hS, hR, hT, &ma, &mb));
+  std::memcpy(S, hS.data(), hS.size() * sizeof(double));
+  if (moments) {
+    std::memcpy(R, hR.data(), hR.size() * sizeof(double));
+    std::memcpy(T, hT.data(), hT.size() * sizeof(double));
+  }
+  if (maxab) {
+    maxab[0] = ma;
+    maxab[1] = mb;
+  }
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_recheck(fpsketch_ctx* c, const void* A, const void* B,
+                                 const int64_t* coords, int32_t n, double* gamma, double* abssum,
+                                 void* stream) {
+  if (c == nullptr || A == nullptr || B == nullptr || (n > 0 && (coords == nullptr ||
+                                                                 gamma == nullptr ||
+                                                                 abssum == nullptr)) ||
+      n < 0) {
+    return fail(FPSK_EINVAL, "null argument");
+  }
+  for (int32_t t = 0; t < n; ++t) {
+    if (coords[2 * t] < 0 || coords[2 * t] >= c->n1 || coords[2 * t + 1] < 0 ||
+        coords[2 * t + 1] >= c->n3) {
+      return fail(FPSK_EINVAL, "coordinate outside C");
+    }
+  }
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n == 0) return FPSK_OK;
+  const size_t nn = static_cast<size_t>(n);
+  FPSK_TRY(dev_alloc(c->rc_coords, 2 * nn * sizeof(int64_t)));
+  FPSK_TRY(dev_alloc(c->rc_gamma, nn * sizeof(double)));
+  FPSK_TRY(dev_alloc(c->rc_abs, nn * sizeof(double)));
+  FPSK_HIP(hipMemcpyAsync(c->rc_coords.p, coords, 2 * nn * sizeof(int64_t),
+                          hipMemcpyHostToDevice, st));
+  // no C here: the kernel skips the C read when C is null
+  FPSK_HIP(fpsk::launch_recheck(static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B),
+                                nullptr, c->n2, c->n3, c->dt == FPSK_BF16 ? 1 : 0,
+                                as<int64_t>(c->rc_coords), n, as<double>(c->rc_gamma),
+                                as<double>(c->rc_abs), nullptr, st));
+  FPSK_HIP(hipMemcpyAsync(gamma, c->rc_gamma.p, nn * sizeof(double), hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipMemcpyAsync(abssum, c->rc_abs.p, nn * sizeof(double), hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_calibrate_noise(fpsketch_ctx* c, const void* C, fpsketch_dtype c_dtype,
+                                         void* stream, int32_t* m_out, double* sigma_bar_out,
+                                         int32_t* rebuilt_out) {
+  if (c == nullptr) return fail(FPSK_EINVAL, "null context");
+  if (c_dtype != FPSK_F32) return fail(FPSK_EDTYPE, "C must be delivered in FP32");
+  if (C == nullptr) return fail(FPSK_EINVAL, "null C");
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  double acc[2] = {0.0, 0.0};
+  FPSK_HIP(hipMemcpyAsync(acc, c->sigma_acc.p, sizeof(acc), hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  const double sigma_bar = acc[1] > 0 ? acc[0] / acc[1] : std::nan("");
+  int32_t rebuilt = 0;
+  if (acc[1] > 0) {
+    double rms = 0;
+    FPSK_TRY(rms_hat_device(c, static_cast<const float*>(C), st, &rms));
+    int32_t m_new = c->m;
+    recalibrate(c->n1, c->n3, c->m, sigma_bar, rms, c->p, &m_new, &rebuilt);
+    if (rebuilt) {
+      if (m_new > fpsk::kMaxM) m_new = fpsk::kMaxM;
+      FPSK_TRY(build_probe(c, m_new, st));
+      const double zero[2] = {0.0, 0.0};
+      FPSK_HIP(hipMemcpyAsync(c->sigma_acc.p, zero, sizeof(zero), hipMemcpyHostToDevice, st));
+      FPSK_HIP(hipStreamSynchronize(st));
+    }
+  }
+  if (m_out) *m_out = c->m;
+  if (sigma_bar_out) *sigma_bar_out = sigma_bar;
+  if (rebuilt_out) *rebuilt_out = rebuilt;
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B, const void* C,
+                                  fpsketch_dtype c_dtype, uint64_t seed, int32_t sigma_from_probe,
+                                  fpsketch_fault* out, int32_t cap, int32_t* n_out,
+                                  void* stream) {
+  FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
+  if (n_out == nullptr || cap < 0 || (cap > 0 && out == nullptr)) {
+    return fail(FPSK_EINVAL, "bad output arguments");
+  }
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const float* Cf = static_cast<const float*>(C);
+  const int32_t K = cap_K(c->p);
+  std::vector<Found> F;
+
+  // 1. Exact scan and absolute recompute (Sec. III-I; Algorithm 2).
+  std::vector<int64_t> abs_coords;
+  FPSK_TRY(exact_scan(c, Cf, K, st, abs_coords));
+  std::vector<double> g, ab;
+  std::vector<float> cv;
+  FPSK_TRY(recheck_coords(c, A, B, Cf, abs_coords, g, ab, cv, st));
+  const size_t n_abs = abs_coords.size() / 2;
+  for (size_t t = 0; t < n_abs; ++t) {
+    F.push_back({abs_coords[2 * t], abs_coords[2 * t + 1], g[t], 1, 0});
+  }
+  // Patch list (row-major order already): C holds fl32(gamma) at these entries while sketching.
+  const int32_t* prow = nullptr;
+  const int32_t* pcol = nullptr;
+  const float* pval = nullptr;
+  if (n_abs > 0) {
+    std::vector<int32_t> rowptr(static_cast<size_t>(c->n1) + 1, 0), col(n_abs);
+    std::vector<float> val(n_abs);
+    for (size_t t = 0; t < n_abs; ++t) {
+      rowptr[static_cast<size_t>(abs_coords[2 * t]) + 1]++;
+      col[t] = static_cast<int32_t>(abs_coords[2 * t + 1]);
+      val[t] = static_cast<float>(g[t]);
+    }
+    for (int64_t i = 0; i < c->n1; ++i) rowptr[i + 1] += rowptr[i];
+    FPSK_TRY(dev_alloc(c->patch_rowptr, rowptr.size() * sizeof(int32_t)));
+    FPSK_TRY(dev_alloc(c->patch_col, col.size() * sizeof(int32_t)));
+    FPSK_TRY(dev_alloc(c->patch_val, val.size() * sizeof(float)));
+    FPSK_HIP(hipMemcpyAsync(c->patch_rowptr.p, rowptr.data(), rowptr.size() * sizeof(int32_t),
+                            hipMemcpyHostToDevice, st));
+    FPSK_HIP(hipMemcpyAsync(c->patch_col.p, col.data(), col.size() * sizeof(int32_t),
+                            hipMemcpyHostToDevice, st));
+    FPSK_HIP(hipMemcpyAsync(c->patch_val.p, val.data(), val.size() * sizeof(float),
+                            hipMemcpyHostToDevice, st));
+    FPSK_HIP(hipStreamSynchronize(st));
+    prow = as<int32_t>(c->patch_rowptr);
+    pcol = as<int32_t>(c->patch_col);
+    pval = as<float>(c->patch_val);
+  }
+
+  // 2. Plan from the measured noise (Sec. III-G).
+  double rms = 0.0;
+  FPSK_TRY(rms_hat_device(c, Cf, st, &rms));
+  double sigma = std::nan("");
+  if (sigma_from_probe) {
+    double stt[8];
+    FPSK_HIP(hipMemcpyAsync(stt, c->stats.p, sizeof(stt), hipMemcpyDeviceToHost, st));
+    FPSK_HIP(hipStreamSynchronize(st));
+    sigma = stt[0];
+  } else {
+    HostRound HR0;
+    std::vector<double> S0, R0, T0;
+    FPSK_TRY(sketch_round(c, seed, 0, c->m, false, A, B, Cf, prow, pcol, pval, st, HR0, S0, R0,
+                          T0, nullptr, nullptr));
+    sigma = mad_sigma(S0);
+  }
+  const PlanOut plan = plan_localize(c->n1, c->n2, c->n3, c->dt, c->m, sigma, rms, c->p);
+  if (plan.m_loc > fpsk::kMaxM) return fail(FPSK_ESHAPE, "m_loc beyond 4096");
+
+  // 3. Rounds t = 1..k (Algorithm 1).
+  std::unordered_set<int64_t> inF;
+  auto key = [c](int64_t i, int64_t j) { return i * c->n3 + j; };
+  for (const Found& f : F) inF.insert(key(f.i, f.j));
+  const int r = plan.r;
+  std::vector<std::pair<int, int>> offs;
+  for (int di = -r; di <= r; ++di)
+    for (int dj = -r; dj <= r; ++dj) offs.emplace_back(di, dj);
+  std::sort(offs.begin(), offs.end(), [](const std::pair<int, int>& x, const std::pair<int, int>& y) {
+    const int cx = std::max(std::abs(x.first), std::abs(x.second));
+    const int cy = std::max(std::abs(y.first), std::abs(y.second));
+    if (cx != cy) return cx < cy;
+    const int mx = std::abs(x.first) + std::abs(x.second);
+    const int my = std::abs(y.first) + std::abs(y.second);
+    if (mx != my) return mx < my;
+    return x < y;
+  });
+  double tau = 0.0;
+  int32_t n_rechecked = 0;
+  const int m = plan.m_loc;
+  const double L1 = static_cast<double>(c->L1), L3 = static_cast<double>(c->L3);
+  for (int t = 1; t <= c->p.rounds; ++t) {
+    HostRound HR;
+    std::vector<double> S, Rm, T;
+    double maxA = 0, maxB = 0;
+    FPSK_TRY(sketch_round(c, seed, t, m, true, A, B, Cf, prow, pcol, pval, st, HR, S, Rm, T,
+                          &maxA, &maxB));
+    tau = c->p.c_valid * static_cast<double>(c->n2) * std::ldexp(1.0, -23) * maxA * maxB;
+    // peel every finite fault confirmed so far (Sec. III-H)
+    for (const Found& f : F) {
+      if (f.absolute) continue;
+      const size_t o = static_cast<size_t>(HR.h1[f.i]) * m + HR.h2[f.j];
+      const double sv = static_cast<double>(HR.v1[f.i]) * HR.v2[f.j] * f.delta;
+      S[o] -= sv;
+      Rm[o] -= sv * static_cast<double>(f.i + 1) / L1;
+      T[o] -= sv * static_cast<double>(f.j + 1) / L3;
+    }
+    const double sig = mad_sigma(S);
+    const double tau_c = std::min(tau, 2.0 * sig);
+    const double tau_d = static_cast<double>(std::max(c->n1, c->n3)) * sig /
+                         std::max(static_cast<double>(r), 0.5);
+    const double cut = std::max(tau_c, tau_d);
+    std::vector<int64_t> above;
+    for (size_t o = 0; o < S.size(); ++o)
+      if (std::fabs(S[o]) > cut) above.push_back(static_cast<int64_t>(o));
+    std::sort(above.begin(), above.end(), [&S](int64_t x, int64_t y) {
+      const double ax = std::fabs(S[x]), ay = std::fabs(S[y]);
+      if (ax != ay) return ax > ay;
+      return x < y;
+    });
+    if (static_cast<int64_t>(above.size()) > K) above.resize(K);
+    struct Cand {
+      int64_t ci, cj;
+    };
+    std::vector<Cand> live;
+    for (int64_t o : above) {
+      const double s = S[o], rr = Rm[o], tt = T[o];
+      if (!(s != 0.0 && std::isfinite(s) && std::isfinite(rr) && std::isfinite(tt))) continue;
+      const double ri = L1 * rr / s, rj = L3 * tt / s;
+      if (!std::isfinite(ri) || !std::isfinite(rj) || std::fabs(ri) > 0x1p40 ||
+          std::fabs(rj) > 0x1p40) {
+        continue;
+      }
+      live.push_back({static_cast<int64_t>(std::nearbyint(ri)) - 1,
+                      static_cast<int64_t>(std::nearbyint(rj)) - 1});
+    }
+    if (live.empty()) continue;
+    // Acceptance of every window coordinate is a pure function of (i, j): recheck them all,
+    // then replay Algorithm 1's offset-major loop sequentially.
+    std::vector<int64_t> coords;
+    std::unordered_map<int64_t, int32_t> slot;
+    for (const Cand& cd : live) {
+      for (const auto& od : offs) {
+        const int64_t i = cd.ci + od.first, j = cd.cj + od.second;
+        if (i < 0 || i >= c->n1 || j < 0 || j >= c->n3) continue;
+        const int64_t kk = key(i, j);
+        if (inF.count(kk) || slot.count(kk)) continue;
+        slot.emplace(kk, static_cast<int32_t>(coords.size() / 2));
+        coords.push_back(i);
+        coords.push_back(j);
+      }
+    }
+    std::vector<double> gg, aa;
+    std::vector<float> cc;
+    FPSK_TRY(recheck_coords(c, A, B, Cf, coords, gg, aa, cc, st));
+    n_rechecked += static_cast<int32_t>(coords.size() / 2);
+    std::vector<char> alive(live.size(), 1);
+    size_t nlive = live.size();
+    for (const auto& od : offs) {
+      if (nlive == 0) break;
+      for (size_t u = 0; u < live.size(); ++u) {
+        if (!alive[u]) continue;
+        const int64_t i = live[u].ci + od.first, j = live[u].cj + od.second;
+        if (i < 0 || i >= c->n1 || j < 0 || j >= c->n3) continue;
+        const int64_t kk = key(i, j);
+        if (inF.count(kk)) continue;
+        const int32_t sl = slot.at(kk);
+        const double diff = gg[sl] - static_cast<double>(cc[sl]);
+        const double bound = c->p.c_valid * std::ldexp(1.0, -23) * aa[sl];
+        if (std::fabs(diff) > bound) {
+          F.push_back({i, j, diff, 0, t});
+          inF.insert(kk);
+          alive[u] = 0;
+          --nlive;
+        }
+      }
+    }
+  }
+
+  c->last_plan.m = c->m;
+  c->last_plan.m_loc = plan.m_loc;
+  c->last_plan.r = plan.r;
+  c->last_plan.fallback = plan.fallback;
+  c->last_plan.n_abs = static_cast<int32_t>(n_abs);
+  c->last_plan.n_rechecked = n_rechecked;
+  c->last_plan.sigma_hat = sigma;
+  c->last_plan.rms_hat = rms;
+  c->last_plan.B = plan.B;
+  c->last_plan.tau = tau;
+
+  *n_out = static_cast<int32_t>(F.size());
+  const size_t nw = std::min<size_t>(F.size(), static_cast<size_t>(cap));
+  for (size_t t = 0; t < nw; ++t) {
+    out[t].i = F[t].i;
+    out[t].j = F[t].j;
+    out[t].delta = F[t].delta;
+    out[t].absolute = F[t].absolute;
+    out[t].round = F[t].round;
+  }
+  if (F.size() > static_cast<size_t>(cap)) {
+    return fail(FPSK_ECAPACITY, "more fault records than capacity");
+  }
+  return FPSK_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,98 @@
+// Internal interface between the host library and the gfx950 kernels of the FP-Sketch verifier.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace fpsk {
+
+constexpr int kThreads = 256;          // work-group size of every kernel (4 wave64)
+constexpr int kColTile = 512;          // columns per A or C tile: 64 lanes x 8 elements
+constexpr int kBChunkHalfs = 16384;    // halfs of B staged in LDS per chunk (32 KiB)
+constexpr int kMaxM = 4096;            // largest bucket count the kernels accept
+constexpr int kUnroll = 4;             // rows in flight per wave in the row-bucket passes
+constexpr double kHugeLimit = 3.4028234663852886e38 / 16.0;   // fp32max / 16
+
+// One pass over A, B and C producing the factors of Eq. 1 (and their weighted forms).
+struct StreamArgs {
+  const uint16_t* A;          // n1 x n2 half bits
+  const uint16_t* B;          // n2 x n3 half bits
+  const float* C;             // n1 x n3
+  int64_t n1, n2, n3;
+  int m;
+  // row side: rows sorted by bucket; entry = row | (v1 < 0) << 31; off1[m + 1]
+  const int32_t* perm1;
+  const int32_t* off1;
+  // C column tiles of kColTile: per tile, columns sorted by bucket as
+  // (offset in tile) | (v2 < 0) << 15, with coff[t * (m + 1) + b] segment starts
+  const uint16_t* ctab;
+  const int32_t* coff;
+  // B column chunks of cwb columns, same encoding
+  const uint16_t* btab;
+  const int32_t* boff;
+  int cwb;
+  // outputs
+  float* P;        // m x n2       H1 A
+  float* Pw;       // m x n2       H1 W1 A            (moments only)
+  float* Q;        // n2 x m       B H2^T
+  float* Qw;       // n2 x m       B W2 H2^T          (moments only)
+  double* partS;   // npc x m x m  partial H1 C H2^T over column-tile groups
+  double* partR;   // npc x m x m  partial H1 W1 C H2^T
+  double* partT;   // npc x m x m  partial H1 C W2 H2^T
+  float* maxpart;  // nA + nB: max |A| per A work-group, then max |B| per B work-group
+  // C entries replaced while sketching (absolute entries): CSR by row, may be null
+  const int32_t* patch_rowptr;
+  const int32_t* patch_col;
+  const float* patch_val;
+  // decomposition
+  int nA, nB, nC;
+  int TA, TC, TB;
+  int npc, tg;
+  double inv_l1, inv_l3;      // 1 / 2^ceil(log2 n1), 1 / 2^ceil(log2 n3)
+  int vec_a, vec_b, vec_c;    // 16-byte vector loads allowed
+};
+
+// Bucket-space product S = P Q - S_C (and R = Pw Q - R_C, T = P Qw - T_C), plus the probe
+// decision in the last work-group.
+struct ProductArgs {
+  const float* P;
+  const float* Pw;
+  const float* Q;
+  const float* Qw;
+  const double* partS;
+  const double* partR;
+  const double* partT;
+  double* S;
+  double* R;
+  double* T;
+  double* scratch;      // NS x tiles x ts^2 (x 3 with moments) split-K partials
+  uint32_t* tile_cnt;   // tiles arrival counters (self-resetting)
+  uint32_t* glob_cnt;   // tile-completion counter (self-resetting)
+  double* tilestat;     // tiles x 4: sum|S|, max|S|, non-finite count
+  int m, n2, nt, NS, ksl, npc;
+  int mode;             // 0: sketch only; 1: probe decision
+  const float* maxpart;
+  int nA, nB;
+  double* stats;        // [8] sigma_hat, thr, tau, max|S|, finite, dirty, max|A|, max|B|
+  int32_t* d_dirty;     // caller's flag (may be null)
+  double* sigma_acc;    // [2] running sum of clean sigma_hat, count
+  double mu, c_valid;
+};
+
+hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g,
+                         size_t lds_bytes, hipStream_t st);
+hipError_t launch_product(const ProductArgs& a, int ts, bool moments, hipStream_t st);
+hipError_t launch_scan_count(const float* C, int64_t n1, int64_t n3, int32_t* counts,
+                             hipStream_t st);
+hipError_t launch_scan_extract(const float* C, int64_t n3, const int32_t* rows,
+                               const int32_t* base, int nrows, int32_t cap, int64_t* out,
+                               hipStream_t st);
+hipError_t launch_sample(const float* C, int64_t stride, int64_t count, float* out,
+                         hipStream_t st);
+hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, const float* C, int64_t n2,
+                          int64_t n3, int dt, const int64_t* coords, int n, double* gamma,
+                          double* abssum, float* cval, hipStream_t st);
+
+}  // namespace fpsk

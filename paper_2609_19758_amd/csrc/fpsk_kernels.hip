@@ -1,0 +1,913 @@
+// gfx950 kernels of the FP-Sketch post hoc verifier.
+//
+// stream:   one pass over A, B and C forming the factors of Eq. 1 without forming AB:
+//           P = H1 A (row-bucket segmented reduction), Q = B H2^T (column-bucket fold of each
+//           row of B) and the bucket grid of C (row-bucket accumulation, then a column-bucket
+//           fold once per row bucket and tile); with moments, the weighted forms that give the
+//           first-moment sketches R and T (paper, Sec. III-B).  No atomics: every sum has a
+//           fixed order, so sketches are bit-reproducible.  Streaming sums accumulate in FP64.
+// product:  S = P Q - H1 C H2^T (and R, T) with split-K partials in FP64, reduced in fixed
+//           order by the last work-group of each output tile; in probe mode the last tile to
+//           finish computes the clipped-mean noise, the threshold and the verdict (Sec. III-E,
+//           III-I, Algorithm 2).
+// scan / sample / recheck: the exact scan for non-finite and out-of-range entries
+//           (Sec. III-I), strided samples of C for rms-hat (Sec. III-G) and the validation
+//           recomputation of candidates (Sec. III-D).
+#include "fpsk_internal.h"
+
+namespace fpsk {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+
+// ----------------------------------------------------------------------------------------
+// Element helpers.  DT: 0 = FP16, 1 = BF16.
+
+template <int DT>
+__device__ __forceinline__ float lo_half(uint32_t w) {
+  if constexpr (DT == 1) {
+    return __uint_as_float(w << 16);
+  } else {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xffffu)));
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ float hi_half(uint32_t w) {
+  if constexpr (DT == 1) {
+    return __uint_as_float(w & 0xffff0000u);
+  } else {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  return lo_half<DT>(h);
+}
+
+// Running max of |x| over both halves of a word, on the bit patterns (|x| is monotone in the
+// low 15 bits for non-negative patterns).
+__device__ __forceinline__ uint32_t absmax2(uint32_t mx, uint32_t w) {
+  const u16x2 a = __builtin_bit_cast(u16x2, mx);
+  const u16x2 b = __builtin_bit_cast(u16x2, w & 0x7fff7fffu);
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(a, b));
+}
+
+// 8 halfs of a row starting at column col (zero beyond n).
+__device__ __forceinline__ u32x4 load8h(const uint16_t* row, int64_t col, int64_t n, bool vec) {
+  if (vec && col + 8 <= n) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(row + col));
+  }
+  u32x4 r = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    if (col + e < n) {
+      const uint32_t h = row[col + e];
+      r[e >> 1] |= h << (16 * (e & 1));
+    }
+  }
+  return r;
+}
+
+// 8 floats of a row starting at column col (zero beyond n).
+__device__ __forceinline__ void load8f(const float* row, int64_t col, int64_t n, bool vec,
+                                       f32x4& v0, f32x4& v1) {
+  if (vec && col + 8 <= n) {
+    v0 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + col));
+    v1 = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(row + col + 4));
+    return;
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v0[e] = (col + e < n) ? row[col + e] : 0.0f;
+    v1[e] = (col + 4 + e < n) ? row[col + 4 + e] : 0.0f;
+  }
+}
+
+// Replace loaded C values by the recomputed values of absolute entries in this row (compile-time
+// element indices only, so the loaded vectors stay in registers).
+__device__ __forceinline__ void apply_patches(const StreamArgs& s, int64_t row, int64_t col,
+                                              f32x4& v0, f32x4& v1) {
+  const int q0 = s.patch_rowptr[row];
+  const int q1 = s.patch_rowptr[row + 1];
+  for (int q = q0; q < q1; ++q) {
+    const int64_t d = static_cast<int64_t>(s.patch_col[q]) - col;
+    const float pv = s.patch_val[q];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (d == e) v0[e] = pv;
+      if (d == e + 4) v1[e] = pv;
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint32_t o = __shfl_xor(v, off, 64);
+    v = v > o ? v : o;
+  }
+  return v;
+}
+
+// Block-wide max of the half-bit maxima; thread 0 returns the value as a float.
+template <int DT>
+__device__ float block_absmax_half(uint32_t mx, uint32_t* ldsu) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t m16 = (mx & 0xffffu) > (mx >> 16) ? (mx & 0xffffu) : (mx >> 16);
+  m16 = wave_max_u32(m16);
+  if (lane == 0) ldsu[w] = m16;
+  __syncthreads();
+  float r = 0.0f;
+  if (threadIdx.x == 0) {
+    uint32_t b = ldsu[0];
+    for (int i = 1; i < kThreads / 64; ++i) b = ldsu[i] > b ? ldsu[i] : b;
+    r = half_bits_to_float<DT>(b);
+  }
+  __syncthreads();
+  return r;
+}
+
+// ----------------------------------------------------------------------------------------
+// A work-group: bucket a, column tile t of A.  P[a, tile] = sum over the bucket's rows of
+// v1(i) A[i, tile] (and Pw with w_i).  The 4 waves take every 4th row of the bucket and are
+// combined in fixed wave order.
+
+template <int DT, bool MOM>
+__device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int a = u / s.TA, t = u - a * s.TA;
+  const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
+  const int p0 = s.off1[a], p1 = s.off1[a + 1];
+  const bool vec = s.vec_a != 0;
+  double acc[8], accw[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    acc[k] = 0.0;
+    accw[k] = 0.0;
+  }
+  uint32_t mx = 0;
+  for (int p = p0 + w; p < p1; p += 4 * kUnroll) {
+    u32x4 v[kUnroll];
+    float sg[kUnroll];
+    double sw[kUnroll];
+#pragma unroll
+    for (int q = 0; q < kUnroll; ++q) {
+      const int pp = p + 4 * q;
+      if (pp < p1) {
+        const int32_t e = s.perm1[pp];
+        const int64_t row = e & 0x7fffffff;
+        sg[q] = e < 0 ? -1.0f : 1.0f;
+        sw[q] = MOM ? static_cast<double>(sg[q]) * static_cast<double>(row + 1) * s.inv_l1 : 0.0;
+        v[q] = load8h(s.A + row * s.n2, col, s.n2, vec);
+      } else {
+        sg[q] = 0.0f;
+        sw[q] = 0.0;
+        v[q] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kUnroll; ++q) {
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const uint32_t wd = v[q][h];
+        mx = absmax2(mx, wd);
+        const float x0 = lo_half<DT>(wd), x1 = hi_half<DT>(wd);
+        acc[2 * h] += static_cast<double>(sg[q] * x0);
+        acc[2 * h + 1] += static_cast<double>(sg[q] * x1);
+        if (MOM) {
+          accw[2 * h] = fma(sw[q], static_cast<double>(x0), accw[2 * h]);
+          accw[2 * h + 1] = fma(sw[q], static_cast<double>(x1), accw[2 * h + 1]);
+        }
+      }
+    }
+  }
+  // Combine the 4 waves: layout [wave][k][lane].
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    lds[(w * 8 + k) * 64 + lane] = acc[k];
+    if (MOM) lds[2048 + (w * 8 + k) * 64 + lane] = accw[k];
+  }
+  const float amax = block_absmax_half<DT>(mx, ldsu);   // contains __syncthreads
+  for (int c = threadIdx.x; c < kColTile; c += kThreads) {
+    const int ln = c >> 3, k = c & 7;
+    const int64_t gc = static_cast<int64_t>(t) * kColTile + c;
+    if (gc < s.n2) {
+      double v = lds[k * 64 + ln] + lds[(8 + k) * 64 + ln];
+      v += lds[(16 + k) * 64 + ln];
+      v += lds[(24 + k) * 64 + ln];
+      s.P[static_cast<int64_t>(a) * s.n2 + gc] = static_cast<float>(v);
+      if (MOM) {
+        double vw = lds[2048 + k * 64 + ln] + lds[2048 + (8 + k) * 64 + ln];
+        vw += lds[2048 + (16 + k) * 64 + ln];
+        vw += lds[2048 + (24 + k) * 64 + ln];
+        s.Pw[static_cast<int64_t>(a) * s.n2 + gc] = static_cast<float>(vw);
+      }
+    }
+  }
+  if (threadIdx.x == 0) s.maxpart[u] = amax;
+}
+
+// ----------------------------------------------------------------------------------------
+// B work-group: RB consecutive rows of B, all columns, in chunks of cwb = kBChunkHalfs / RB
+// columns staged in LDS column-major ([column][RB rows]).  Thread b folds bucket b (and
+// b + 256, ...) over the chunk's bucket-sorted column list: Q[k, b] = sum v2(j) B[k, j].
+
+template <int RB>
+__device__ __forceinline__ uint32_t pick_half(uint32_t wa, uint32_t wb, int odd) {
+  return odd ? ((wa >> 16) | (wb & 0xffff0000u)) : ((wa & 0xffffu) | (wb << 16));
+}
+
+// Write the 8 columns held by one thread (RB rows x 8 columns) column-major into LDS.
+template <int RB>
+__device__ __forceinline__ void store_cols(uint16_t* dst, const u32x4* v) {
+  if constexpr (RB == 1) {
+    *reinterpret_cast<u32x4*>(dst) = v[0];
+  } else if constexpr (RB == 2) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      reinterpret_cast<uint32_t*>(dst)[e] = pick_half<RB>(v[0][e >> 1], v[1][e >> 1], e & 1);
+    }
+  } else if constexpr (RB == 4) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      u32x2 o;
+      o[0] = pick_half<RB>(v[0][e >> 1], v[1][e >> 1], e & 1);
+      o[1] = pick_half<RB>(v[2][e >> 1], v[3][e >> 1], e & 1);
+      reinterpret_cast<u32x2*>(dst)[e] = o;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      u32x4 o;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) o[rr] = pick_half<RB>(v[2 * rr][e >> 1], v[2 * rr + 1][e >> 1], e & 1);
+      reinterpret_cast<u32x4*>(dst)[e] = o;
+    }
+  }
+}
+
+template <int DT, int RB>
+__device__ __forceinline__ void load_col(const uint16_t* src, float* x) {
+  if constexpr (RB == 1) {
+    x[0] = half_bits_to_float<DT>(*src);
+  } else if constexpr (RB == 2) {
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(src);
+    x[0] = lo_half<DT>(w);
+    x[1] = hi_half<DT>(w);
+  } else if constexpr (RB == 4) {
+    const u32x2 w = *reinterpret_cast<const u32x2*>(src);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      x[2 * h] = lo_half<DT>(w[h]);
+      x[2 * h + 1] = hi_half<DT>(w[h]);
+    }
+  } else {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(src);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      x[2 * h] = lo_half<DT>(w[h]);
+      x[2 * h + 1] = hi_half<DT>(w[h]);
+    }
+  }
+}
+
+template <int DT, bool MOM, int RB, int G>
+__device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint32_t* ldsu) {
+  constexpr int CW = kBChunkHalfs / RB;
+  const int m = s.m;
+  const int64_t k0 = static_cast<int64_t>(u) * RB;
+  const bool vec = s.vec_b != 0;
+  double acc[G][RB], accw[G][RB];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+      acc[g][r] = 0.0;
+      accw[g][r] = 0.0;
+    }
+  }
+  uint32_t mx = 0;
+  for (int c = 0; c < s.TB; ++c) {
+    const int64_t cbase = static_cast<int64_t>(c) * CW;
+    for (int g8 = threadIdx.x; g8 < CW / 8; g8 += kThreads) {
+      const int64_t col = cbase + static_cast<int64_t>(g8) * 8;
+      u32x4 v[RB];
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        if (k0 + r < s.n2 && col < s.n3) {
+          v[r] = load8h(s.B + (k0 + r) * s.n3, col, s.n3, vec);
+        } else {
+          v[r] = u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int h = 0; h < 4; ++h) mx = absmax2(mx, v[r][h]);
+      }
+      store_cols<RB>(L + static_cast<int64_t>(g8) * 8 * RB, v);
+    }
+    __syncthreads();
+    const int32_t* boff = s.boff + static_cast<int64_t>(c) * (m + 1);
+    const uint16_t* btab = s.btab + cbase;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int b = threadIdx.x + kThreads * g;
+      if (b < m) {
+        const int q1 = boff[b + 1];
+        for (int q = boff[b]; q < q1; ++q) {
+          const uint32_t e = btab[q];
+          const int cc = e & 0x7fff;
+          const float sg = (e & 0x8000u) ? -1.0f : 1.0f;
+          float x[RB];
+          load_col<DT, RB>(L + cc * RB, x);
+          const double wj = MOM ? static_cast<double>(cbase + cc + 1) * s.inv_l3 : 0.0;
+#pragma unroll
+          for (int r = 0; r < RB; ++r) {
+            const double d = static_cast<double>(sg * x[r]);
+            acc[g][r] += d;
+            if (MOM) accw[g][r] = fma(d, wj, accw[g][r]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int b = threadIdx.x + kThreads * g;
+    if (b < m) {
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        if (k0 + r < s.n2) {
+          s.Q[(k0 + r) * m + b] = static_cast<float>(acc[g][r]);
+          if (MOM) s.Qw[(k0 + r) * m + b] = static_cast<float>(accw[g][r]);
+        }
+      }
+    }
+  }
+  const float bmax = block_absmax_half<DT>(mx, ldsu);
+  if (threadIdx.x == 0) s.maxpart[s.nA + u] = bmax;
+}
+
+// ----------------------------------------------------------------------------------------
+// C work-group: row bucket a, a group of tg column tiles.  Per tile, the 4 waves accumulate
+// v1(i) C[i, tile] (and w_i v1(i) C) over the bucket's rows, combine in fixed order, and
+// thread b folds the tile's columns of bucket b: S_C[a, b] += sum v2(j) colsum[j]
+// (T_C with w_j, R_C from the row-weighted column sums).  One partial per tile group.
+
+template <bool MOM, int G>
+__device__ void c_unit(const StreamArgs& s, int u, double* lds) {
+  const int m = s.m;
+  const int a = u / s.npc, gi = u - a * s.npc;
+  const int t0 = gi * s.tg;
+  const int t1 = (t0 + s.tg < s.TC) ? t0 + s.tg : s.TC;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int p0 = s.off1[a], p1 = s.off1[a + 1];
+  const bool vec = s.vec_c != 0;
+  double* comb = lds;                          // [2][4][8][64]
+  double* cs = lds + (MOM ? 4096 : 2048);      // [2][512]
+  double fS[G], fR[G], fT[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    fS[g] = 0.0;
+    fR[g] = 0.0;
+    fT[g] = 0.0;
+  }
+  for (int t = t0; t < t1; ++t) {
+    const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
+    double acc[8], accw[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      acc[k] = 0.0;
+      accw[k] = 0.0;
+    }
+    for (int p = p0 + w; p < p1; p += 4 * kUnroll) {
+      f32x4 v0[kUnroll], v1[kUnroll];
+      float sg[kUnroll];
+      double sw[kUnroll];
+#pragma unroll
+      for (int q = 0; q < kUnroll; ++q) {
+        const int pp = p + 4 * q;
+        if (pp < p1) {
+          const int32_t e = s.perm1[pp];
+          const int64_t row = e & 0x7fffffff;
+          sg[q] = e < 0 ? -1.0f : 1.0f;
+          sw[q] = MOM ? static_cast<double>(sg[q]) * static_cast<double>(row + 1) * s.inv_l1
+                      : 0.0;
+          load8f(s.C + row * s.n3, col, s.n3, vec, v0[q], v1[q]);
+          if (s.patch_rowptr != nullptr) apply_patches(s, row, col, v0[q], v1[q]);
+        } else {
+          sg[q] = 0.0f;
+          sw[q] = 0.0;
+          v0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+          v1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kUnroll; ++q) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = e < 4 ? v0[q][e] : v1[q][e - 4];
+          acc[e] += static_cast<double>(sg[q] * x);
+          if (MOM) accw[e] = fma(sw[q], static_cast<double>(x), accw[e]);
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      comb[(w * 8 + k) * 64 + lane] = acc[k];
+      if (MOM) comb[2048 + (w * 8 + k) * 64 + lane] = accw[k];
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < kColTile; c += kThreads) {
+      const int ln = c >> 3, k = c & 7;
+      double v = comb[k * 64 + ln] + comb[(8 + k) * 64 + ln];
+      v += comb[(16 + k) * 64 + ln];
+      v += comb[(24 + k) * 64 + ln];
+      cs[c] = v;
+      if (MOM) {
+        double vw = comb[2048 + k * 64 + ln] + comb[2048 + (8 + k) * 64 + ln];
+        vw += comb[2048 + (16 + k) * 64 + ln];
+        vw += comb[2048 + (24 + k) * 64 + ln];
+        cs[512 + c] = vw;
+      }
+    }
+    __syncthreads();
+    const int32_t* coff = s.coff + static_cast<int64_t>(t) * (m + 1);
+    const uint16_t* ctab = s.ctab + static_cast<int64_t>(t) * kColTile;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int b = threadIdx.x + kThreads * g;
+      if (b < m) {
+        const int q1 = coff[b + 1];
+        for (int q = coff[b]; q < q1; ++q) {
+          const uint32_t e = ctab[q];
+          const int cc = e & 0x7fff;
+          const double sgd = (e & 0x8000u) ? -1.0 : 1.0;
+          const double x = sgd * cs[cc];
+          fS[g] += x;
+          if (MOM) {
+            const double wj = static_cast<double>(static_cast<int64_t>(t) * kColTile + cc + 1) *
+                              s.inv_l3;
+            fT[g] = fma(x, wj, fT[g]);
+            fR[g] += sgd * cs[512 + cc];
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int b = threadIdx.x + kThreads * g;
+    if (b < m) {
+      const int64_t o = (static_cast<int64_t>(gi) * m + a) * m + b;
+      s.partS[o] = fS[g];
+      if (MOM) {
+        s.partR[o] = fR[g];
+        s.partT[o] = fT[g];
+      }
+    }
+  }
+}
+
+template <int DT, bool MOM, int RB, int G>
+__global__ __launch_bounds__(kThreads) void stream_kernel(StreamArgs s) {
+  extern __shared__ double lds_dyn[];
+  __shared__ uint32_t ldsu[kThreads / 64];
+  int u = blockIdx.x;
+  if (u < s.nA) {
+    a_unit<DT, MOM>(s, u, lds_dyn, ldsu);
+    return;
+  }
+  u -= s.nA;
+  if (u < s.nB) {
+    b_unit<DT, MOM, RB, G>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
+    return;
+  }
+  c_unit<MOM, G>(s, u - s.nB, lds_dyn);
+}
+
+// ----------------------------------------------------------------------------------------
+// Product.  Work-group (tile, slice): output tile of ts x ts buckets, k in [slice*ksl, ...).
+
+__device__ double block_sum_d(double v, double* red) {
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int st = kThreads / 2; st > 0; st >>= 1) {
+    if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+    __syncthreads();
+  }
+  const double r = red[0];
+  __syncthreads();
+  return r;
+}
+
+__device__ double block_max_d(double v, double* red) {
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int st = kThreads / 2; st > 0; st >>= 1) {
+    if (threadIdx.x < st) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + st]);
+    __syncthreads();
+  }
+  const double r = red[0];
+  __syncthreads();
+  return r;
+}
+
+// Arrival at a self-resetting counter; returns true in the last of `expected` work-groups.
+__device__ bool arrive_last(uint32_t* cnt, uint32_t expected, int* flag) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    const uint32_t old = atomicAdd(cnt, 1u);
+    const int last = (old == expected - 1) ? 1 : 0;
+    if (last) *cnt = 0u;
+    *flag = last;
+  }
+  __syncthreads();
+  const bool last = *flag != 0;
+  if (last) __threadfence();
+  return last;
+}
+
+template <int TS, bool MOM>
+__global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
+  constexpr int RT = TS / 16;
+  constexpr int KC = 16;
+  constexpr int NX = MOM ? 3 : 1;
+  __shared__ double Ps[MOM ? 2 : 1][TS][KC + 1];
+  __shared__ double Qs[MOM ? 2 : 1][KC][TS + 1];
+  __shared__ double red[kThreads];
+  __shared__ int flag;
+  const int m = pa.m;
+  const int ntiles = pa.nt * pa.nt;
+  const int tile = blockIdx.x, slice = blockIdx.y;
+  const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
+  const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
+  const int k0 = slice * pa.ksl;
+  const int k1 = (k0 + pa.ksl < pa.n2) ? k0 + pa.ksl : pa.n2;
+  double acc[NX][RT][RT];
+#pragma unroll
+  for (int x = 0; x < NX; ++x)
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int j = 0; j < RT; ++j) acc[x][i][j] = 0.0;
+
+  for (int kc = k0; kc < k1; kc += KC) {
+    for (int idx = threadIdx.x; idx < TS * KC; idx += kThreads) {
+      const int r = idx / KC, kk = idx - r * KC;
+      const int row = ta * TS + r, k = kc + kk;
+      const bool ok = row < m && k < k1;
+      const int64_t o = static_cast<int64_t>(row) * pa.n2 + k;
+      Ps[0][r][kk] = ok ? static_cast<double>(pa.P[o]) : 0.0;
+      if (MOM) Ps[1][r][kk] = ok ? static_cast<double>(pa.Pw[o]) : 0.0;
+    }
+    for (int idx = threadIdx.x; idx < KC * TS; idx += kThreads) {
+      const int kk = idx / TS, c = idx - kk * TS;
+      const int colb = tb * TS + c, k = kc + kk;
+      const bool ok = colb < m && k < k1;
+      const int64_t o = static_cast<int64_t>(k) * m + colb;
+      Qs[0][kk][c] = ok ? static_cast<double>(pa.Q[o]) : 0.0;
+      if (MOM) Qs[1][kk][c] = ok ? static_cast<double>(pa.Qw[o]) : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int kk = 0; kk < KC; ++kk) {
+      double pv[RT], qv[RT], pwv[RT], qwv[RT];
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+        pv[i] = Ps[0][ty + 16 * i][kk];
+        if (MOM) pwv[i] = Ps[1][ty + 16 * i][kk];
+      }
+#pragma unroll
+      for (int j = 0; j < RT; ++j) {
+        qv[j] = Qs[0][kk][tx + 16 * j];
+        if (MOM) qwv[j] = Qs[1][kk][tx + 16 * j];
+      }
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+#pragma unroll
+        for (int j = 0; j < RT; ++j) {
+          acc[0][i][j] = fma(pv[i], qv[j], acc[0][i][j]);
+          if (MOM) {
+            acc[1][i][j] = fma(pwv[i], qv[j], acc[1][i][j]);
+            acc[2][i][j] = fma(pv[i], qwv[j], acc[2][i][j]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // Split-K: publish the partial and let the last slice of this tile reduce in slice order.
+  if (pa.NS > 1) {
+    double* sc = pa.scratch;
+#pragma unroll
+    for (int x = 0; x < NX; ++x)
+#pragma unroll
+      for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int j = 0; j < RT; ++j) {
+          const int64_t o = ((static_cast<int64_t>(slice) * ntiles + tile) * NX + x) * TS * TS +
+                            (ty + 16 * i) * TS + tx + 16 * j;
+          sc[o] = acc[x][i][j];
+        }
+    if (!arrive_last(pa.tile_cnt + tile, static_cast<uint32_t>(pa.NS), &flag)) return;
+#pragma unroll
+    for (int x = 0; x < NX; ++x)
+#pragma unroll
+      for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int j = 0; j < RT; ++j) {
+          double v = 0.0;
+          for (int sl = 0; sl < pa.NS; ++sl) {
+            const int64_t o = ((static_cast<int64_t>(sl) * ntiles + tile) * NX + x) * TS * TS +
+                              (ty + 16 * i) * TS + tx + 16 * j;
+            v += __builtin_nontemporal_load(sc + o);
+          }
+          acc[x][i][j] = v;
+        }
+  }
+
+  // Subtract the C grid (sum of its column-group partials) and store S (R, T).
+  double lsum = 0.0, lmax = 0.0, lbad = 0.0;
+#pragma unroll
+  for (int i = 0; i < RT; ++i)
+#pragma unroll
+    for (int j = 0; j < RT; ++j) {
+      const int row = ta * TS + ty + 16 * i, colb = tb * TS + tx + 16 * j;
+      if (row < m && colb < m) {
+        const int64_t o = static_cast<int64_t>(row) * m + colb;
+        const int64_t mm = static_cast<int64_t>(m) * m;
+        double cS = 0.0, cR = 0.0, cT = 0.0;
+        for (int g = 0; g < pa.npc; ++g) {
+          cS += pa.partS[g * mm + o];
+          if (MOM) {
+            cR += pa.partR[g * mm + o];
+            cT += pa.partT[g * mm + o];
+          }
+        }
+        const double sv = acc[0][i][j] - cS;
+        pa.S[o] = sv;
+        if (MOM) {
+          pa.R[o] = acc[1][i][j] - cR;
+          pa.T[o] = acc[2][i][j] - cT;
+        }
+        const double av = fabs(sv);
+        if (__builtin_isfinite(sv)) {
+          lsum += av;
+          lmax = fmax(lmax, av);
+        } else {
+          lbad += 1.0;
+        }
+      }
+    }
+  if (pa.mode != 1) return;
+
+  // Probe decision: per-tile statistics, then the last tile computes the verdict.
+  const double tsum = block_sum_d(lsum, red);
+  const double tmax = block_max_d(lmax, red);
+  const double tbad = block_sum_d(lbad, red);
+  if (threadIdx.x == 0) {
+    pa.tilestat[tile * 4 + 0] = tsum;
+    pa.tilestat[tile * 4 + 1] = tmax;
+    pa.tilestat[tile * 4 + 2] = tbad;
+  }
+  if (!arrive_last(pa.glob_cnt, static_cast<uint32_t>(ntiles), &flag)) return;
+
+  double v = 0.0, vmax = 0.0, vbad = 0.0;
+  for (int t = threadIdx.x; t < ntiles; t += kThreads) {
+    v += pa.tilestat[t * 4 + 0];
+    vmax = fmax(vmax, pa.tilestat[t * 4 + 1]);
+    vbad += pa.tilestat[t * 4 + 2];
+  }
+  const double mm = static_cast<double>(m) * m;
+  const double sum_abs = block_sum_d(v, red);
+  const double max_abs = block_max_d(vmax, red);
+  const double nbad = block_sum_d(vbad, red);
+  // mean|S| over all buckets (a non-finite bucket makes the mean non-finite)
+  const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / mm;
+  const double clip = 5.0 * mean_abs;
+  double c2 = 0.0;
+  for (int64_t idx = threadIdx.x; idx < static_cast<int64_t>(mm); idx += kThreads) {
+    const double a = fabs(pa.S[idx]);
+    c2 += a < clip ? a : clip;
+  }
+  const double clipped = block_sum_d(c2, red);
+  float amax = 0.0f, bmax = 0.0f;
+  for (int i = threadIdx.x; i < pa.nA; i += kThreads) amax = fmaxf(amax, pa.maxpart[i]);
+  for (int i = threadIdx.x; i < pa.nB; i += kThreads) bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
+  const double maxA = block_max_d(static_cast<double>(amax), red);
+  const double maxB = block_max_d(static_cast<double>(bmax), red);
+  if (threadIdx.x == 0) {
+    const double sigma = 1.2533 * (clipped / mm);
+    const double tau = pa.c_valid * static_cast<double>(pa.n2) * 0x1p-23 * maxA * maxB;
+    const double lim = pa.mu * sqrt(2.0 * log(mm)) * sigma;
+    const double thr = fmin(tau, lim);
+    const bool finite = nbad == 0.0;
+    const bool clean = finite && max_abs <= thr;
+    pa.stats[0] = sigma;
+    pa.stats[1] = thr;
+    pa.stats[2] = tau;
+    pa.stats[3] = max_abs;
+    pa.stats[4] = finite ? 1.0 : 0.0;
+    pa.stats[5] = clean ? 0.0 : 1.0;
+    pa.stats[6] = maxA;
+    pa.stats[7] = maxB;
+    if (clean) {
+      pa.sigma_acc[0] += sigma;
+      pa.sigma_acc[1] += 1.0;
+    } else if (pa.d_dirty != nullptr) {
+      *pa.d_dirty = 1;
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------------------
+// Exact scan (non-finite or |C| > fp32max/16), samples, recheck.
+
+__device__ __forceinline__ bool is_absolute_entry(float x) {
+  return !(fabsf(x) <= static_cast<float>(kHugeLimit));
+}
+
+__global__ __launch_bounds__(kThreads) void scan_count_kernel(const float* C, int64_t n3,
+                                                              int32_t* counts) {
+  __shared__ int red[kThreads];
+  const int64_t row = blockIdx.x;
+  int cnt = 0;
+  for (int64_t j = threadIdx.x; j < n3; j += kThreads) cnt += is_absolute_entry(C[row * n3 + j]);
+  red[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int st = kThreads / 2; st > 0; st >>= 1) {
+    if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) counts[row] = red[0];
+}
+
+__global__ __launch_bounds__(kThreads) void scan_extract_kernel(const float* C, int64_t n3,
+                                                                const int32_t* rows,
+                                                                const int32_t* base, int32_t cap,
+                                                                int64_t* out) {
+  __shared__ int wtot[kThreads / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t row = rows[blockIdx.x];
+  int pos = base[blockIdx.x];
+  for (int64_t j0 = 0; j0 < n3; j0 += kThreads) {
+    const int64_t j = j0 + threadIdx.x;
+    const bool f = j < n3 && is_absolute_entry(C[row * n3 + j]);
+    const uint64_t bal = __ballot(f);
+    const uint64_t below = lane == 0 ? 0ull : (bal & (~0ull >> (64 - lane)));
+    const int pre = __popcll(below);
+    if (lane == 0) wtot[w] = __popcll(bal);
+    __syncthreads();
+    int woff = 0, tot = 0;
+    for (int i = 0; i < kThreads / 64; ++i) {
+      if (i < w) woff += wtot[i];
+      tot += wtot[i];
+    }
+    if (f) {
+      const int idx = pos + woff + pre;
+      if (idx < cap) {
+        out[2 * idx] = row;
+        out[2 * idx + 1] = j;
+      }
+    }
+    pos += tot;
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void sample_kernel(const float* C, int64_t stride,
+                                                          int64_t count, float* out) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  if (t < count) out[t] = C[t * stride];
+}
+
+// One wave per coordinate: gamma = sum_k A_ik B_kj and sum_k |A_ik B_kj|, exact products
+// accumulated in FP64, reduced across lanes in fixed butterfly order.
+template <int DT>
+__global__ __launch_bounds__(kThreads) void recheck_kernel(const uint16_t* A, const uint16_t* B,
+                                                           const float* C, int64_t n2, int64_t n3,
+                                                           const int64_t* coords, int n,
+                                                           double* gamma, double* abssum,
+                                                           float* cval) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x * (kThreads / 64) + w;
+  if (c >= n) return;
+  const int64_t i = coords[2 * c], j = coords[2 * c + 1];
+  double g = 0.0, ab = 0.0;
+  for (int64_t k = lane; k < n2; k += 64) {
+    const double a = static_cast<double>(half_bits_to_float<DT>(A[i * n2 + k]));
+    const double b = static_cast<double>(half_bits_to_float<DT>(B[k * n3 + j]));
+    const double p = a * b;
+    g += p;
+    ab += fabs(p);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    g += __shfl_xor(g, off, 64);
+    ab += __shfl_xor(ab, off, 64);
+  }
+  if (lane == 0) {
+    gamma[c] = g;
+    abssum[c] = ab;
+    if (C != nullptr && cval != nullptr) cval[c] = C[i * n3 + j];
+  }
+}
+
+// ----------------------------------------------------------------------------------------
+// Launchers.
+
+template <int DT, bool MOM>
+static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, size_t lds,
+                                  hipStream_t st) {
+  const int grid = s.nA + s.nB + s.nC;
+  if (grid <= 0) return hipSuccess;
+#define FPSK_STREAM_CASE(RB_, G_)                                                     \
+  if (rb == RB_ && g == G_) {                                                         \
+    hipLaunchKernelGGL((stream_kernel<DT, MOM, RB_, G_>), dim3(grid), dim3(kThreads), \
+                       lds, st, s);                                                   \
+    return hipGetLastError();                                                         \
+  }
+  FPSK_STREAM_CASE(8, 1)
+  FPSK_STREAM_CASE(8, 2)
+  FPSK_STREAM_CASE(4, 4)
+  FPSK_STREAM_CASE(2, 8)
+  FPSK_STREAM_CASE(1, 16)
+#undef FPSK_STREAM_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g,
+                         size_t lds_bytes, hipStream_t st) {
+  if (dt == 1) {
+    return moments ? stream_dispatch<1, true>(s, rb, g, lds_bytes, st)
+                   : stream_dispatch<1, false>(s, rb, g, lds_bytes, st);
+  }
+  return moments ? stream_dispatch<0, true>(s, rb, g, lds_bytes, st)
+                 : stream_dispatch<0, false>(s, rb, g, lds_bytes, st);
+}
+
+hipError_t launch_product(const ProductArgs& a, int ts, bool moments, hipStream_t st) {
+  const dim3 grid(a.nt * a.nt, a.NS);
+#define FPSK_PRODUCT_CASE(TS_)                                                               \
+  if (ts == TS_) {                                                                           \
+    if (moments) {                                                                           \
+      hipLaunchKernelGGL((product_kernel<TS_, true>), grid, dim3(kThreads), 0, st, a);      \
+    } else {                                                                                 \
+      hipLaunchKernelGGL((product_kernel<TS_, false>), grid, dim3(kThreads), 0, st, a);     \
+    }                                                                                        \
+    return hipGetLastError();                                                                \
+  }
+  FPSK_PRODUCT_CASE(16)
+  FPSK_PRODUCT_CASE(32)
+  FPSK_PRODUCT_CASE(64)
+#undef FPSK_PRODUCT_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_scan_count(const float* C, int64_t n1, int64_t n3, int32_t* counts,
+                             hipStream_t st) {
+  hipLaunchKernelGGL(scan_count_kernel, dim3(static_cast<unsigned>(n1)), dim3(kThreads), 0, st,
+                     C, n3, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_scan_extract(const float* C, int64_t n3, const int32_t* rows,
+                               const int32_t* base, int nrows, int32_t cap, int64_t* out,
+                               hipStream_t st) {
+  if (nrows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(scan_extract_kernel, dim3(nrows), dim3(kThreads), 0, st, C, n3, rows, base,
+                     cap, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_sample(const float* C, int64_t stride, int64_t count, float* out,
+                         hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  const unsigned grid = static_cast<unsigned>((count + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(sample_kernel, dim3(grid), dim3(kThreads), 0, st, C, stride, count, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, const float* C, int64_t n2,
+                          int64_t n3, int dt, const int64_t* coords, int n, double* gamma,
+                          double* abssum, float* cval, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const unsigned grid = static_cast<unsigned>((n + 3) / 4);
+  if (dt == 1) {
+    hipLaunchKernelGGL(recheck_kernel<1>, dim3(grid), dim3(kThreads), 0, st, A, B, C, n2, n3,
+                       coords, n, gamma, abssum, cval);
+  } else {
+    hipLaunchKernelGGL(recheck_kernel<0>, dim3(grid), dim3(kThreads), 0, st, A, B, C, n2, n3,
+                       coords, n, gamma, abssum, cval);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace fpsk

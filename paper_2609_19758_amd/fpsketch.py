@@ -1,0 +1,316 @@
+"""Python binding of libfpsketch.so (the C ABI in include/fpsketch.h).
+
+Argument marshalling only: every step of the verifier runs in the library's HIP kernels and host
+code.  There is no CPU fallback; if the shared library is missing, loading raises.  Device
+matrices are passed as torch tensors (their data pointers and the current HIP stream) or as raw
+integer device pointers.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfpsketch.so")
+HEADER_PATH = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                           "include", "fpsketch.h")
+
+OK, EINVAL, EDTYPE, ESHAPE, ENOMEM, EHIP, ECAPACITY, ENODEV = range(8)
+F16, BF16, F32 = 0, 1, 2
+DTYPE_CODE = {"fp16": F16, "bf16": BF16, "f32": F32}
+
+
+class FpsketchError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int32), ("rounds", ctypes.c_int32), ("r_star", ctypes.c_int32),
+                ("r_max", ctypes.c_int32), ("s_budget", ctypes.c_int32),
+                ("delta_rc", ctypes.c_int32), ("k_cap", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("rho_min", ctypes.c_double),
+                ("mu", ctypes.c_double), ("c_valid", ctypes.c_double),
+                ("b_star", ctypes.c_double), ("c_coll", ctypes.c_double),
+                ("seed", ctypes.c_uint64)]
+
+
+class Fault(ctypes.Structure):
+    _fields_ = [("i", ctypes.c_int64), ("j", ctypes.c_int64), ("delta", ctypes.c_double),
+                ("absolute", ctypes.c_int32), ("round", ctypes.c_int32)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int32), ("m_loc", ctypes.c_int32), ("r", ctypes.c_int32),
+                ("fallback", ctypes.c_int32), ("n_abs", ctypes.c_int32),
+                ("n_rechecked", ctypes.c_int32), ("sigma_hat", ctypes.c_double),
+                ("rms_hat", ctypes.c_double), ("B", ctypes.c_double), ("tau", ctypes.c_double)]
+
+
+_P = ctypes.c_void_p
+_I32, _I64, _U64, _D = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double
+_SIGS = {
+    "fpsketch_default_params": (None, [ctypes.POINTER(Params)]),
+    "fpsketch_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+    "fpsketch_last_error": (ctypes.c_char_p, []),
+    "fpsketch_create": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, ctypes.POINTER(Params),
+                                       ctypes.POINTER(_P)]),
+    "fpsketch_destroy": (None, [_P]),
+    "fpsketch_probe": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _P, _P]),
+    "fpsketch_localize": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _U64, _I32,
+                                         ctypes.POINTER(Fault), _I32, ctypes.POINTER(_I32), _P]),
+    "fpsketch_calibrate_noise": (ctypes.c_int, [_P, _P, ctypes.c_int, _P, ctypes.POINTER(_I32),
+                                                ctypes.POINTER(_D), ctypes.POINTER(_I32)]),
+    "fpsketch_get_plan": (ctypes.c_int, [_P, ctypes.POINTER(PlanInfo)]),
+    "fpsketch_get_m": (ctypes.c_int, [_P, ctypes.POINTER(_I32)]),
+    "fpsketch_probe_stats": (ctypes.c_int, [_P, ctypes.POINTER(_D), _P]),
+    "fpsketch_sketch": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _U64, _I32, _I32, _I32,
+                                       ctypes.POINTER(_D), ctypes.POINTER(_D),
+                                       ctypes.POINTER(_D), ctypes.POINTER(_D), _P]),
+    "fpsketch_recheck": (ctypes.c_int, [_P, _P, _P, ctypes.POINTER(_I64), _I32,
+                                        ctypes.POINTER(_D), ctypes.POINTER(_D), _P]),
+    "fpsketch_timing": (ctypes.c_int, [_P, _I32]),
+    "fpsketch_timing_read": (ctypes.c_int, [_P, ctypes.POINTER(_D), ctypes.POINTER(_D),
+                                            ctypes.POINTER(_I64)]),
+    "fpsketch_hash_table": (ctypes.c_int, [_U64, _I32, _I32, _I64, _I32,
+                                           ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_int8)]),
+    "fpsketch_m_start": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, ctypes.POINTER(Params),
+                                        ctypes.POINTER(_I32)]),
+    "fpsketch_plan_host": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, _I32, _D, _D,
+                                          ctypes.POINTER(Params), ctypes.POINTER(_I32),
+                                          ctypes.POINTER(_I32), ctypes.POINTER(_D),
+                                          ctypes.POINTER(_I32)]),
+    "fpsketch_recalibrate_host": (ctypes.c_int, [_I64, _I64, _I32, _D, _D,
+                                                 ctypes.POINTER(Params), ctypes.POINTER(_I32),
+                                                 ctypes.POINTER(_I32)]),
+    "fpsketch_rms_hat_samples": (_D, [ctypes.POINTER(ctypes.c_float), _I64]),
+}
+
+_lib = None
+
+
+def header_symbols() -> list[str]:
+    """Names of the functions include/fpsketch.h declares."""
+    text = open(HEADER_PATH).read()
+    return sorted(set(re.findall(r"^\s*(?:[\w\*]+\s+)+\**(fpsketch_\w+)\s*\(", text, re.M)))
+
+
+def load():
+    """Load libfpsketch.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise FpsketchError(-1, "load", f"{LIB_PATH} is missing; build it with "
+                                        "__graft_entry__.build()")
+    lib = ctypes.CDLL(LIB_PATH)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        lib = load()
+        detail = lib.fpsketch_last_error().decode() or lib.fpsketch_status_str(status).decode()
+        raise FpsketchError(status, where, detail)
+
+
+def default_params(**overrides) -> Params:
+    p = Params()
+    load().fpsketch_default_params(ctypes.byref(p))
+    for k, v in overrides.items():
+        if not hasattr(p, k):
+            raise KeyError(k)
+        setattr(p, k, v)
+    return p
+
+
+# ---- pointer helpers ---------------------------------------------------------------------
+
+def _ptr(x) -> int:
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    if not x.is_contiguous():
+        raise ValueError("matrices must be contiguous row-major")
+    return int(x.data_ptr())
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return int(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)
+
+
+def _c_dtype(C, c_dtype: Optional[int]) -> int:
+    if c_dtype is not None:
+        return c_dtype
+    import torch
+    return {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}.get(C.dtype, -1)
+
+
+# ---- host-only helpers (no GPU needed) ---------------------------------------------------
+
+def hash_table(seed: int, rnd: int, side: int, n: int, m: int):
+    b = np.empty(n, dtype=np.int32)
+    s = np.empty(n, dtype=np.int8)
+    _check(load().fpsketch_hash_table(seed, rnd, side, n, m,
+                                      b.ctypes.data_as(ctypes.POINTER(_I32)),
+                                      s.ctypes.data_as(ctypes.POINTER(ctypes.c_int8))),
+           "fpsketch_hash_table")
+    return b, s
+
+
+def m_start(n1: int, n2: int, n3: int, fmt: str, params: Optional[Params] = None) -> int:
+    out = _I32()
+    _check(load().fpsketch_m_start(n1, n2, n3, DTYPE_CODE[fmt],
+                                   ctypes.byref(params) if params else None, ctypes.byref(out)),
+           "fpsketch_m_start")
+    return out.value
+
+
+def plan_host(n1, n2, n3, fmt, m, sigma_hat, rms, params: Optional[Params] = None):
+    ml, r, B, fb = _I32(), _I32(), _D(), _I32()
+    _check(load().fpsketch_plan_host(n1, n2, n3, DTYPE_CODE[fmt], m, sigma_hat, rms,
+                                     ctypes.byref(params) if params else None, ctypes.byref(ml),
+                                     ctypes.byref(r), ctypes.byref(B), ctypes.byref(fb)),
+           "fpsketch_plan_host")
+    return ml.value, r.value, B.value, bool(fb.value)
+
+
+def recalibrate_host(n1, n3, m, sigma_bar, rms, params: Optional[Params] = None):
+    mn, rb = _I32(), _I32()
+    _check(load().fpsketch_recalibrate_host(n1, n3, m, sigma_bar, rms,
+                                            ctypes.byref(params) if params else None,
+                                            ctypes.byref(mn), ctypes.byref(rb)),
+           "fpsketch_recalibrate_host")
+    return mn.value, bool(rb.value)
+
+
+def rms_hat_samples(samples: np.ndarray) -> float:
+    s = np.ascontiguousarray(samples, dtype=np.float32)
+    return float(load().fpsketch_rms_hat_samples(
+        s.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), s.size))
+
+
+# ---- context -----------------------------------------------------------------------------
+
+class Verifier:
+    """One verifier context for products A (n1 x n2) x B (n2 x n3) in `fmt` on the current
+    HIP device."""
+
+    def __init__(self, n1: int, n2: int, n3: int, fmt: str, params: Optional[Params] = None,
+                 **overrides):
+        self.lib = load()
+        self.n1, self.n2, self.n3, self.fmt = n1, n2, n3, fmt
+        self.params = params if params is not None else default_params(**overrides)
+        h = _P()
+        _check(self.lib.fpsketch_create(n1, n2, n3, DTYPE_CODE[fmt], ctypes.byref(self.params),
+                                        ctypes.byref(h)), "fpsketch_create")
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.fpsketch_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def m(self) -> int:
+        out = _I32()
+        _check(self.lib.fpsketch_get_m(self.handle, ctypes.byref(out)), "fpsketch_get_m")
+        return out.value
+
+    def probe_status(self, A, B, C, d_dirty=None, stream=None, c_dtype=None) -> int:
+        """Raw status of fpsketch_probe (used to test error paths)."""
+        return self.lib.fpsketch_probe(self.handle, _ptr(A), _ptr(B), _ptr(C),
+                                       _c_dtype(C, c_dtype), _ptr(d_dirty), _stream(stream))
+
+    def probe(self, A, B, C, d_dirty=None, stream=None, c_dtype=None):
+        _check(self.probe_status(A, B, C, d_dirty, stream, c_dtype), "fpsketch_probe")
+
+    def probe_stats(self, stream=None) -> dict:
+        out = (_D * 8)()
+        _check(self.lib.fpsketch_probe_stats(self.handle, out, _stream(stream)),
+               "fpsketch_probe_stats")
+        keys = ["sigma_hat", "thr", "tau", "max_abs", "finite", "dirty", "max_a", "max_b"]
+        return dict(zip(keys, list(out)))
+
+    def localize(self, A, B, C, seed: int, sigma_from_probe: bool = False, cap: int = 4096,
+                 stream=None, c_dtype=None):
+        buf = (Fault * max(cap, 1))()
+        n = _I32()
+        st = self.lib.fpsketch_localize(self.handle, _ptr(A), _ptr(B), _ptr(C),
+                                        _c_dtype(C, c_dtype), seed, int(sigma_from_probe), buf,
+                                        cap, ctypes.byref(n), _stream(stream))
+        if st not in (OK, ECAPACITY):
+            _check(st, "fpsketch_localize")
+        recs = [(buf[t].i, buf[t].j, buf[t].delta, bool(buf[t].absolute), buf[t].round)
+                for t in range(min(n.value, cap))]
+        return recs, n.value, st
+
+    def timing(self, enable: bool):
+        _check(self.lib.fpsketch_timing(self.handle, int(enable)), "fpsketch_timing")
+
+    def timing_read(self):
+        a, b, n = _D(), _D(), _I64()
+        _check(self.lib.fpsketch_timing_read(self.handle, ctypes.byref(a), ctypes.byref(b),
+                                             ctypes.byref(n)), "fpsketch_timing_read")
+        return a.value, b.value, n.value
+
+    def plan(self) -> dict:
+        pi = PlanInfo()
+        _check(self.lib.fpsketch_get_plan(self.handle, ctypes.byref(pi)), "fpsketch_get_plan")
+        return {k: getattr(pi, k) for k, _ in PlanInfo._fields_}
+
+    def calibrate_noise(self, C, stream=None, c_dtype=None):
+        m, sb, rb = _I32(), _D(), _I32()
+        _check(self.lib.fpsketch_calibrate_noise(self.handle, _ptr(C), _c_dtype(C, c_dtype),
+                                                 _stream(stream), ctypes.byref(m),
+                                                 ctypes.byref(sb), ctypes.byref(rb)),
+               "fpsketch_calibrate_noise")
+        return m.value, sb.value, bool(rb.value)
+
+    def sketch(self, A, B, C, seed: int, rnd: int, m: int, moments: bool = True, stream=None):
+        S = np.empty(m * m, dtype=np.float64)
+        R = np.empty(m * m, dtype=np.float64)
+        T = np.empty(m * m, dtype=np.float64)
+        mx = np.empty(2, dtype=np.float64)
+        dp = ctypes.POINTER(_D)
+        _check(self.lib.fpsketch_sketch(self.handle, _ptr(A), _ptr(B), _ptr(C),
+                                        _c_dtype(C, None), seed, rnd, m, int(moments),
+                                        S.ctypes.data_as(dp), R.ctypes.data_as(dp),
+                                        T.ctypes.data_as(dp), mx.ctypes.data_as(dp),
+                                        _stream(stream)), "fpsketch_sketch")
+        shape = (m, m)
+        return (S.reshape(shape), R.reshape(shape) if moments else None,
+                T.reshape(shape) if moments else None, float(mx[0]), float(mx[1]))
+
+    def recheck(self, A, B, coords, stream=None):
+        cs = np.ascontiguousarray(np.asarray(coords, dtype=np.int64).reshape(-1, 2))
+        n = cs.shape[0]
+        g = np.empty(max(n, 1), dtype=np.float64)
+        a = np.empty(max(n, 1), dtype=np.float64)
+        dp = ctypes.POINTER(_D)
+        _check(self.lib.fpsketch_recheck(self.handle, _ptr(A), _ptr(B),
+                                         cs.ctypes.data_as(ctypes.POINTER(_I64)), n,
+                                         g.ctypes.data_as(dp), a.ctypes.data_as(dp),
+                                         _stream(stream)), "fpsketch_recheck")
+        return g[:n], a[:n]
