@@ -202,6 +202,16 @@ fpsketch_status fpsketch_timing(fpsketch_ctx* ctx, int32_t enable);
 fpsketch_status fpsketch_timing_read(fpsketch_ctx* ctx, double* stream_ms, double* product_ms,
                                      int64_t* calls);
 
+/* Reference streams of known size, for the achievable-bandwidth line and for scaling HBM
+ * traffic counters: a plain read of `bytes` from device memory `src` (16-byte aligned, bytes a
+ * multiple of 16), folded into one word that is written to the device word `d_out` only in a
+ * practically unreachable case, and a plain copy of `bytes` from `src` to `dst`.  `grid`
+ * work-groups of 256 threads stride over the buffer.  Enqueue only. */
+fpsketch_status fpsketch_stream_read(const void* src, int64_t bytes, uint32_t* d_out,
+                                     int32_t grid, void* stream);
+fpsketch_status fpsketch_stream_copy(const void* src, void* dst, int64_t bytes, int32_t grid,
+                                     void* stream);
+
 /* ----------------------------------------------------------------------------------------- */
 /* Host-only helpers (no device work; usable without a GPU).                                  */
 

@@ -299,7 +299,7 @@ T* as(DevBuf& b) {
 struct Decomp {
   int m = 0;
   int TA = 0, nA = 0;
-  int rb = 8, g = 1, cwb = 2048, TB = 0, nB = 0;
+  int rb = 8, g = 1, ng = 1, cwb = 2048, TB = 0, nB = 0;
   int TC = 0, npc = 1, tg = 1, nC = 0;
   int ts = 16, nt = 1, NS = 1, ksl = 0;
   size_t lds_stream = 0;
@@ -311,7 +311,11 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
   d.m = m;
   d.TA = static_cast<int>((n2 + kColTile - 1) / kColTile);
   d.nA = m * d.TA;
-  if (m <= 256) {
+  if (m <= 64) {
+    d.rb = 8, d.g = 1, d.ng = 4;
+  } else if (m <= 128) {
+    d.rb = 8, d.g = 1, d.ng = 2;
+  } else if (m <= 256) {
     d.rb = 8, d.g = 1;
   } else if (m <= 512) {
     d.rb = 8, d.g = 2;
@@ -334,16 +338,19 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
   d.ts = m <= 128 ? 16 : (m <= 512 ? 32 : 64);
   d.nt = (m + d.ts - 1) / d.ts;
   const int tiles = d.nt * d.nt;
-  int ns = (512 + tiles - 1) / tiles;
-  ns = std::max(1, std::min<int>(ns, static_cast<int>(std::max<int64_t>(1, n2 / 128))));
-  int ksl = static_cast<int>((n2 + ns - 1) / ns);
-  ksl = (ksl + 15) / 16 * 16;
-  d.ksl = ksl;
+  // k per staged chunk of the product kernel (16 KiB of FP32 per factor); a slice is a whole
+  // number of chunks, and about 256 (tile, slice) work-groups are formed
+  const int kch = (mom ? 2048 : 4096) / d.ts;
+  int ns = (256 + tiles - 1) / tiles;
+  ns = std::max(1, std::min<int>(ns, static_cast<int>(std::max<int64_t>(1, n2 / kch))));
+  int64_t ksl = (n2 + ns - 1) / ns;
+  ksl = (ksl + kch - 1) / kch * kch;
+  d.ksl = static_cast<int>(ksl);
   d.NS = static_cast<int>((n2 + ksl - 1) / ksl);
-  const size_t a_lds = (mom ? 4096 : 2048) * sizeof(double);
-  const size_t b_lds = static_cast<size_t>(fpsk::kBChunkHalfs) * sizeof(uint16_t);
-  const size_t c_lds = (mom ? 5120 : 2560) * sizeof(double);
-  d.lds_stream = std::max({a_lds, b_lds, c_lds});
+  // [0, 32 or 40 KiB): A/C combine area or the staged B chunk; then the sorted column list of
+  // the current B chunk (cwb halfs) or C tile (512 halfs)
+  d.lds_stream = (mom ? 5120 : 4096) * sizeof(double) +
+                 static_cast<size_t>(std::max(d.cwb, kColTile)) * sizeof(uint16_t);
   return d;
 }
 
@@ -384,8 +391,7 @@ void free_round(DevRound& D) {
 struct Workspace {
   Decomp d;
   bool mom = false;
-  DevBuf P, Pw, Q, Qw, partS, partR, partT, scratch, S, R, T, maxpart, tile_cnt, glob_cnt,
-      tilestat;
+  DevBuf P, Pw, Q, Qw, partS, partR, partT, scratch, S, R, T, maxpart, tilestat;
 };
 
 fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n3, int m,
@@ -413,23 +419,13 @@ fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n
                              : 0;
   FPSK_TRY(dev_alloc(W.scratch, sc));
   FPSK_TRY(dev_alloc(W.maxpart, static_cast<size_t>(d.nA + d.nB) * sizeof(float)));
-  // counters: allocated zeroed once; the kernels leave them at zero after every launch
-  const size_t cnt_bytes = static_cast<size_t>(tiles) * sizeof(uint32_t);
-  if (W.tile_cnt.bytes < cnt_bytes) {
-    FPSK_TRY(dev_alloc(W.tile_cnt, cnt_bytes));
-    FPSK_HIP(hipMemset(W.tile_cnt.p, 0, cnt_bytes));
-  }
-  if (W.glob_cnt.p == nullptr) {
-    FPSK_TRY(dev_alloc(W.glob_cnt, sizeof(uint32_t)));
-    FPSK_HIP(hipMemset(W.glob_cnt.p, 0, sizeof(uint32_t)));
-  }
   FPSK_TRY(dev_alloc(W.tilestat, static_cast<size_t>(tiles) * 4 * sizeof(double)));
   return FPSK_OK;
 }
 
 void free_workspace(Workspace& W) {
   for (DevBuf* b : {&W.P, &W.Pw, &W.Q, &W.Qw, &W.partS, &W.partR, &W.partT, &W.scratch, &W.S,
-                    &W.R, &W.T, &W.maxpart, &W.tile_cnt, &W.glob_cnt, &W.tilestat}) {
+                    &W.R, &W.T, &W.maxpart, &W.tilestat}) {
     dev_free(*b);
   }
 }
@@ -451,6 +447,7 @@ struct fpsketch_ctx {
   DevRound probe_round;
   Workspace probe_ws;
   DevBuf stats;       // 8 doubles
+  DevBuf zero;        // 64 bytes of zeros
   DevBuf sigma_acc;   // 2 doubles
   // localize / diagnostic workspaces
   DevRound aux_round;
@@ -532,9 +529,13 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   s.vec_a = (c->n2 % 8 == 0) && aligned16(A);
   s.vec_b = (c->n3 % 8 == 0) && aligned16(B);
   s.vec_c = (c->n3 % 4 == 0) && aligned16(Cm);
+  // the vector path loads whole 8-element groups: every row length must be a multiple of 8
+  if (c->n2 % 8 != 0 || c->n3 % 8 != 0) s.vec_a = s.vec_b = s.vec_c = 0;
+  s.zero = c->zero.p;
   if (R.cwb != d.cwb || R.m != d.m) return fail(FPSK_EINVAL, "internal: tables do not match");
   if (ev) FPSK_HIP(hipEventRecord(ev[0], st));
-  FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.lds_stream, st));
+  FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.ng, d.lds_stream,
+                               st));
   if (ev) FPSK_HIP(hipEventRecord(ev[1], st));
 
   fpsk::ProductArgs a{};
@@ -549,8 +550,6 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   a.R = mom ? as<double>(W.R) : nullptr;
   a.T = mom ? as<double>(W.T) : nullptr;
   a.scratch = as<double>(W.scratch);
-  a.tile_cnt = as<uint32_t>(W.tile_cnt);
-  a.glob_cnt = as<uint32_t>(W.glob_cnt);
   a.tilestat = as<double>(W.tilestat);
   a.m = d.m;
   a.n2 = static_cast<int>(c->n2);
@@ -861,8 +860,10 @@ fpsketch_status fpsketch_create(int64_t n1, int64_t n2, int64_t n3, fpsketch_dty
   c->inv_l3 = 1.0 / static_cast<double>(c->L3);
   fpsketch_status s = dev_alloc(c->stats, 8 * sizeof(double));
   if (s == FPSK_OK) s = dev_alloc(c->sigma_acc, 2 * sizeof(double));
+  if (s == FPSK_OK) s = dev_alloc(c->zero, 64);
   if (s == FPSK_OK) {
     hipError_t e = hipMemset(c->stats.p, 0, 8 * sizeof(double));
+    if (e == hipSuccess) e = hipMemset(c->zero.p, 0, 64);
     if (e == hipSuccess) e = hipMemset(c->sigma_acc.p, 0, 2 * sizeof(double));
     if (e != hipSuccess) s = fail(FPSK_EHIP, std::string("hipMemset: ") + hipGetErrorString(e));
   }
@@ -884,7 +885,7 @@ void fpsketch_destroy(fpsketch_ctx* c) {
   free_workspace(c->probe_ws);
   free_round(c->aux_round);
   free_workspace(c->aux_ws);
-  for (DevBuf* b : {&c->stats, &c->sigma_acc, &c->scan_counts, &c->scan_rows, &c->scan_base,
+  for (DevBuf* b : {&c->stats, &c->sigma_acc, &c->zero, &c->scan_counts, &c->scan_rows, &c->scan_base,
                     &c->scan_out, &c->samples, &c->patch_rowptr, &c->patch_col, &c->patch_val,
                     &c->rc_coords, &c->rc_gamma, &c->rc_abs, &c->rc_c}) {
     dev_free(*b);
@@ -1260,6 +1261,26 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
   if (F.size() > static_cast<size_t>(cap)) {
     return fail(FPSK_ECAPACITY, "more fault records than capacity");
   }
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_stream_read(const void* src, int64_t bytes, uint32_t* d_out,
+                                     int32_t grid, void* stream) {
+  if (src == nullptr || d_out == nullptr || bytes < 0 || bytes % 16 != 0 || grid < 1 ||
+      (reinterpret_cast<uintptr_t>(src) & 15u) != 0) {
+    return fail(FPSK_EINVAL, "fpsketch_stream_read: bad argument");
+  }
+  FPSK_HIP(fpsk::launch_read(src, bytes, d_out, grid, static_cast<hipStream_t>(stream)));
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_stream_copy(const void* src, void* dst, int64_t bytes, int32_t grid,
+                                     void* stream) {
+  if (src == nullptr || dst == nullptr || bytes < 0 || bytes % 16 != 0 || grid < 1 ||
+      ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15u) != 0) {
+    return fail(FPSK_EINVAL, "fpsketch_stream_copy: bad argument");
+  }
+  FPSK_HIP(fpsk::launch_copy(src, dst, bytes, grid, static_cast<hipStream_t>(stream)));
   return FPSK_OK;
 }
 

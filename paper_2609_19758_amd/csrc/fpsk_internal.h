@@ -12,7 +12,6 @@ constexpr int kThreads = 256;          // work-group size of every kernel (4 wav
 constexpr int kColTile = 512;          // columns per A or C tile: 64 lanes x 8 elements
 constexpr int kBChunkHalfs = 16384;    // halfs of B staged in LDS per chunk (32 KiB)
 constexpr int kMaxM = 4096;            // largest bucket count the kernels accept
-constexpr int kUnroll = 4;             // rows in flight per wave in the row-bucket passes
 constexpr double kHugeLimit = 3.4028234663852886e38 / 16.0;   // fp32max / 16
 
 // One pass over A, B and C producing the factors of Eq. 1 (and their weighted forms).
@@ -52,10 +51,11 @@ struct StreamArgs {
   int npc, tg;
   double inv_l1, inv_l3;      // 1 / 2^ceil(log2 n1), 1 / 2^ceil(log2 n3)
   int vec_a, vec_b, vec_c;    // 16-byte vector loads allowed
+  const void* zero;           // >= 64 bytes of zeros (read in place of invalid rows or lanes)
 };
 
 // Bucket-space product S = P Q - S_C (and R = Pw Q - R_C, T = P Qw - T_C), plus the probe
-// decision in the last work-group.
+// decision.
 struct ProductArgs {
   const float* P;
   const float* Pw;
@@ -68,8 +68,6 @@ struct ProductArgs {
   double* R;
   double* T;
   double* scratch;      // NS x tiles x ts^2 (x 3 with moments) split-K partials
-  uint32_t* tile_cnt;   // tiles arrival counters (self-resetting)
-  uint32_t* glob_cnt;   // tile-completion counter (self-resetting)
   double* tilestat;     // tiles x 4: sum|S|, max|S|, non-finite count
   int m, n2, nt, NS, ksl, npc;
   int mode;             // 0: sketch only; 1: probe decision
@@ -81,7 +79,7 @@ struct ProductArgs {
   double mu, c_valid;
 };
 
-hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g,
+hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g, int ng,
                          size_t lds_bytes, hipStream_t st);
 hipError_t launch_product(const ProductArgs& a, int ts, bool moments, hipStream_t st);
 hipError_t launch_scan_count(const float* C, int64_t n1, int64_t n3, int32_t* counts,
@@ -94,5 +92,8 @@ hipError_t launch_sample(const float* C, int64_t stride, int64_t count, float* o
 hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, const float* C, int64_t n2,
                           int64_t n3, int dt, const int64_t* coords, int n, double* gamma,
                           double* abssum, float* cval, hipStream_t st);
+
+hipError_t launch_read(const void* src, int64_t bytes, uint32_t* out, int grid, hipStream_t st);
+hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int grid, hipStream_t st);
 
 }  // namespace fpsk

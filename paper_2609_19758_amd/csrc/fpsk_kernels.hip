@@ -7,9 +7,8 @@
 //           first-moment sketches R and T (paper, Sec. III-B).  No atomics: every sum has a
 //           fixed order, so sketches are bit-reproducible.  Streaming sums accumulate in FP64.
 // product:  S = P Q - H1 C H2^T (and R, T) with split-K partials in FP64, reduced in fixed
-//           order by the last work-group of each output tile; in probe mode the last tile to
-//           finish computes the clipped-mean noise, the threshold and the verdict (Sec. III-E,
-//           III-I, Algorithm 2).
+//           slice order per output tile; in probe mode one work-group then computes the
+//           clipped-mean noise, the threshold and the verdict (Sec. III-E, III-I, Algorithm 2).
 // scan / sample / recheck: the exact scan for non-finite and out-of-range entries
 //           (Sec. III-I), strided samples of C for rms-hat (Sec. III-G) and the validation
 //           recomputation of candidates (Sec. III-D).
@@ -72,6 +71,20 @@ __device__ __forceinline__ u32x4 load8h(const uint16_t* row, int64_t col, int64_
   return r;
 }
 
+// Branch-free 16-byte loads for the vector path: an invalid row or lane reads the zero buffer
+// instead of branching, so a group of loads issues back to back.
+__device__ __forceinline__ u32x4 load8h_sel(const uint16_t* p, bool ok, const void* zero) {
+  const u32x4* q = ok ? reinterpret_cast<const u32x4*>(p) : static_cast<const u32x4*>(zero);
+  return __builtin_nontemporal_load(q);
+}
+
+__device__ __forceinline__ void load8f_sel(const float* p, bool ok, const void* zero, f32x4& v0,
+                                           f32x4& v1) {
+  const f32x4* q = ok ? reinterpret_cast<const f32x4*>(p) : static_cast<const f32x4*>(zero);
+  v0 = __builtin_nontemporal_load(q);
+  v1 = __builtin_nontemporal_load(q + 1);
+}
+
 // 8 floats of a row starting at column col (zero beyond n).
 __device__ __forceinline__ void load8f(const float* row, int64_t col, int64_t n, bool vec,
                                        f32x4& v0, f32x4& v1) {
@@ -132,17 +145,28 @@ __device__ float block_absmax_half(uint32_t mx, uint32_t* ldsu) {
 }
 
 // ----------------------------------------------------------------------------------------
-// A work-group: bucket a, column tile t of A.  P[a, tile] = sum over the bucket's rows of
-// v1(i) A[i, tile] (and Pw with w_i).  The 4 waves take every 4th row of the bucket and are
-// combined in fixed wave order.
+// Row-bucket passes (A and C work-groups).  Wave w of a work-group takes rows w, w + 4, ... of
+// the bucket's sorted row list.  The row entries of up to 64 of its rows arrive with one vector
+// load and are broadcast with readlane, so a group of row loads issues back to back instead of
+// waiting on an index load per row.
 
-template <int DT, bool MOM>
+// Row entry (row | negative-sign bit) of this wave's r-th row in the current batch.
+__device__ __forceinline__ int32_t row_entry(int32_t pe, int r) {
+  return __builtin_amdgcn_readlane(pe, r);
+}
+
+// A work-group: bucket a, column tile t of A.  P[a, tile] = sum over the bucket's rows of
+// v1(i) A[i, tile] (and Pw with w_i).  Groups of 8 rows are summed in FP32 (their partial sums
+// stay within a few units of the last place of the stored FP32 factor), groups in FP64; the 4
+// waves are combined in fixed wave order.
+template <int DT, bool MOM, bool VEC>
 __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) {
+  constexpr int U = 8;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int a = u / s.TA, t = u - a * s.TA;
   const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
+  const bool lane_ok = col < s.n2;
   const int p0 = s.off1[a], p1 = s.off1[a + 1];
-  const bool vec = s.vec_a != 0;
   double acc[8], accw[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
@@ -150,38 +174,50 @@ __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) 
     accw[k] = 0.0;
   }
   uint32_t mx = 0;
-  for (int p = p0 + w; p < p1; p += 4 * kUnroll) {
-    u32x4 v[kUnroll];
-    float sg[kUnroll];
-    double sw[kUnroll];
+  for (int base = p0 + w; base < p1; base += 4 * 64) {
+    const int nr = min(64, (p1 - base + 3) / 4);
+    const int32_t pe = lane < nr ? s.perm1[base + 4 * lane] : 0;
+    for (int r0 = 0; r0 < nr; r0 += U) {
+      u32x4 v[U];
+      float sg[U], sw[U];
 #pragma unroll
-    for (int q = 0; q < kUnroll; ++q) {
-      const int pp = p + 4 * q;
-      if (pp < p1) {
-        const int32_t e = s.perm1[pp];
+      for (int q = 0; q < U; ++q) {
+        const bool ok = r0 + q < nr;
+        const int32_t e = row_entry(pe, ok ? r0 + q : 0);
         const int64_t row = e & 0x7fffffff;
-        sg[q] = e < 0 ? -1.0f : 1.0f;
-        sw[q] = MOM ? static_cast<double>(sg[q]) * static_cast<double>(row + 1) * s.inv_l1 : 0.0;
-        v[q] = load8h(s.A + row * s.n2, col, s.n2, vec);
-      } else {
-        sg[q] = 0.0f;
-        sw[q] = 0.0;
-        v[q] = u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < kUnroll; ++q) {
-#pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const uint32_t wd = v[q][h];
-        mx = absmax2(mx, wd);
-        const float x0 = lo_half<DT>(wd), x1 = hi_half<DT>(wd);
-        acc[2 * h] += static_cast<double>(sg[q] * x0);
-        acc[2 * h + 1] += static_cast<double>(sg[q] * x1);
-        if (MOM) {
-          accw[2 * h] = fma(sw[q], static_cast<double>(x0), accw[2 * h]);
-          accw[2 * h + 1] = fma(sw[q], static_cast<double>(x1), accw[2 * h + 1]);
+        sg[q] = ok ? (e < 0 ? -1.0f : 1.0f) : 0.0f;
+        sw[q] = MOM ? static_cast<float>(sg[q] * static_cast<double>(row + 1) * s.inv_l1) : 0.0f;
+        if (VEC) {
+          v[q] = load8h_sel(s.A + row * s.n2 + col, ok && lane_ok, s.zero);
+        } else {
+          v[q] = ok ? load8h(s.A + row * s.n2, col, s.n2, false) : u32x4{0u, 0u, 0u, 0u};
         }
+      }
+      float g32[8], gw32[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        g32[k] = 0.0f;
+        gw32[k] = 0.0f;
+      }
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const uint32_t wd = v[q][h];
+          mx = absmax2(mx, wd);
+          const float x0 = lo_half<DT>(wd), x1 = hi_half<DT>(wd);
+          g32[2 * h] = fmaf(sg[q], x0, g32[2 * h]);
+          g32[2 * h + 1] = fmaf(sg[q], x1, g32[2 * h + 1]);
+          if (MOM) {
+            gw32[2 * h] = fmaf(sw[q], x0, gw32[2 * h]);
+            gw32[2 * h + 1] = fmaf(sw[q], x1, gw32[2 * h + 1]);
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        acc[k] += static_cast<double>(g32[k]);
+        if (MOM) accw[k] += static_cast<double>(gw32[k]);
       }
     }
   }
@@ -212,9 +248,11 @@ __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) 
 }
 
 // ----------------------------------------------------------------------------------------
-// B work-group: RB consecutive rows of B, all columns, in chunks of cwb = kBChunkHalfs / RB
-// columns staged in LDS column-major ([column][RB rows]).  Thread b folds bucket b (and
-// b + 256, ...) over the chunk's bucket-sorted column list: Q[k, b] = sum v2(j) B[k, j].
+// B work-group: RB consecutive rows of B, all columns, in chunks of CW = kBChunkHalfs / RB
+// columns.  Per chunk, every thread issues its 8 x 16-byte loads of B and its share of the
+// chunk's bucket-sorted column list at once; B is then staged column-major ([column][RB rows])
+// in LDS and thread (row group rg, bucket b) folds the chunk's columns of bucket b for its
+// RB / NG rows: Q[k, b] = sum v2(j) B[k, j].
 
 template <int RB>
 __device__ __forceinline__ uint32_t pick_half(uint32_t wa, uint32_t wb, int odd) {
@@ -250,15 +288,16 @@ __device__ __forceinline__ void store_cols(uint16_t* dst, const u32x4* v) {
   }
 }
 
-template <int DT, int RB>
+// RBG consecutive halfs of one staged column.
+template <int DT, int RBG>
 __device__ __forceinline__ void load_col(const uint16_t* src, float* x) {
-  if constexpr (RB == 1) {
+  if constexpr (RBG == 1) {
     x[0] = half_bits_to_float<DT>(*src);
-  } else if constexpr (RB == 2) {
+  } else if constexpr (RBG == 2) {
     const uint32_t w = *reinterpret_cast<const uint32_t*>(src);
     x[0] = lo_half<DT>(w);
     x[1] = hi_half<DT>(w);
-  } else if constexpr (RB == 4) {
+  } else if constexpr (RBG == 4) {
     const u32x2 w = *reinterpret_cast<const u32x2*>(src);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -275,17 +314,22 @@ __device__ __forceinline__ void load_col(const uint16_t* src, float* x) {
   }
 }
 
-template <int DT, bool MOM, int RB, int G>
-__device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint32_t* ldsu) {
-  constexpr int CW = kBChunkHalfs / RB;
+template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
+__device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, uint32_t* ldsu) {
+  constexpr int CW = kBChunkHalfs / RB;      // columns per chunk
+  constexpr int RBG = RB / NG;               // rows per fold group
+  constexpr int SLOTS = kThreads / NG;       // bucket slots per fold group
+  constexpr int NV = kBChunkHalfs / 8 / kThreads;   // 16-byte loads of B per thread per chunk
+  constexpr int NT = CW / 8 / kThreads > 0 ? CW / 8 / kThreads : 1;   // table loads
+  static_assert(NV == 8, "each thread stages 64 halfs of B per chunk");
   const int m = s.m;
+  const int rg = threadIdx.x / SLOTS, bslot = threadIdx.x - rg * SLOTS;
   const int64_t k0 = static_cast<int64_t>(u) * RB;
-  const bool vec = s.vec_b != 0;
-  double acc[G][RB], accw[G][RB];
+  double acc[G][RBG], accw[G][RBG];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
 #pragma unroll
-    for (int r = 0; r < RB; ++r) {
+    for (int r = 0; r < RBG; ++r) {
       acc[g][r] = 0.0;
       accw[g][r] = 0.0;
     }
@@ -293,42 +337,69 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint32_t* ldsu) 
   uint32_t mx = 0;
   for (int c = 0; c < s.TB; ++c) {
     const int64_t cbase = static_cast<int64_t>(c) * CW;
-    for (int g8 = threadIdx.x; g8 < CW / 8; g8 += kThreads) {
+    // -- issue every load of this chunk: B, the sorted column list, the segment bounds
+    u32x4 v[NV];
+#pragma unroll
+    for (int it = 0; it < NV / RB; ++it) {
+      const int g8 = threadIdx.x + kThreads * it;
       const int64_t col = cbase + static_cast<int64_t>(g8) * 8;
-      u32x4 v[RB];
 #pragma unroll
       for (int r = 0; r < RB; ++r) {
-        if (k0 + r < s.n2 && col < s.n3) {
-          v[r] = load8h(s.B + (k0 + r) * s.n3, col, s.n3, vec);
+        const bool ok = k0 + r < s.n2 && col < s.n3;
+        if (VEC) {
+          v[it * RB + r] = load8h_sel(s.B + (k0 + r) * s.n3 + col, ok, s.zero);
         } else {
-          v[r] = u32x4{0u, 0u, 0u, 0u};
+          v[it * RB + r] = ok ? load8h(s.B + (k0 + r) * s.n3, col, s.n3, false)
+                              : u32x4{0u, 0u, 0u, 0u};
         }
-#pragma unroll
-        for (int h = 0; h < 4; ++h) mx = absmax2(mx, v[r][h]);
       }
-      store_cols<RB>(L + static_cast<int64_t>(g8) * 8 * RB, v);
     }
-    __syncthreads();
+    u32x4 tv[NT];
+#pragma unroll
+    for (int it = 0; it < NT; ++it) {
+      const int o = (threadIdx.x + kThreads * it) * 8;
+      tv[it] = o < CW ? *reinterpret_cast<const u32x4*>(s.btab + cbase + o) : u32x4{0u, 0u, 0u, 0u};
+    }
     const int32_t* boff = s.boff + static_cast<int64_t>(c) * (m + 1);
-    const uint16_t* btab = s.btab + cbase;
+    int qb[G], qe[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const int b = threadIdx.x + kThreads * g;
-      if (b < m) {
-        const int q1 = boff[b + 1];
-        for (int q = boff[b]; q < q1; ++q) {
-          const uint32_t e = btab[q];
-          const int cc = e & 0x7fff;
-          const float sg = (e & 0x8000u) ? -1.0f : 1.0f;
-          float x[RB];
-          load_col<DT, RB>(L + cc * RB, x);
-          const double wj = MOM ? static_cast<double>(cbase + cc + 1) * s.inv_l3 : 0.0;
+      const int b = bslot + SLOTS * g;
+      qb[g] = b < m ? boff[b] : 0;
+      qe[g] = b < m ? boff[b + 1] : 0;
+    }
+    // -- stage into LDS
 #pragma unroll
-          for (int r = 0; r < RB; ++r) {
-            const double d = static_cast<double>(sg * x[r]);
-            acc[g][r] += d;
-            if (MOM) accw[g][r] = fma(d, wj, accw[g][r]);
-          }
+    for (int it = 0; it < NV / RB; ++it) {
+      const int g8 = threadIdx.x + kThreads * it;
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) mx = absmax2(mx, v[it * RB + r][h]);
+      }
+      store_cols<RB>(L + static_cast<int64_t>(g8) * 8 * RB, v + it * RB);
+    }
+#pragma unroll
+    for (int it = 0; it < NT; ++it) {
+      const int o = (threadIdx.x + kThreads * it) * 8;
+      if (o < CW) *reinterpret_cast<u32x4*>(tabL + o) = tv[it];
+    }
+    __syncthreads();
+    // -- fold
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      for (int q = qb[g]; q < qe[g]; ++q) {
+        const uint32_t e = tabL[q];
+        const int cc = e & 0x7fff;
+        const float sg = (e & 0x8000u) ? -1.0f : 1.0f;
+        float x[RBG];
+        load_col<DT, RBG>(L + cc * RB + rg * RBG, x);
+        const double wj = MOM ? static_cast<double>(cbase + cc + 1) * s.inv_l3 : 0.0;
+#pragma unroll
+        for (int r = 0; r < RBG; ++r) {
+          const double d = static_cast<double>(sg * x[r]);
+          acc[g][r] += d;
+          if (MOM) accw[g][r] = fma(d, wj, accw[g][r]);
         }
       }
     }
@@ -336,13 +407,14 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint32_t* ldsu) 
   }
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    const int b = threadIdx.x + kThreads * g;
+    const int b = bslot + SLOTS * g;
     if (b < m) {
 #pragma unroll
-      for (int r = 0; r < RB; ++r) {
-        if (k0 + r < s.n2) {
-          s.Q[(k0 + r) * m + b] = static_cast<float>(acc[g][r]);
-          if (MOM) s.Qw[(k0 + r) * m + b] = static_cast<float>(accw[g][r]);
+      for (int r = 0; r < RBG; ++r) {
+        const int64_t k = k0 + rg * RBG + r;
+        if (k < s.n2) {
+          s.Q[k * m + b] = static_cast<float>(acc[g][r]);
+          if (MOM) s.Qw[k * m + b] = static_cast<float>(accw[g][r]);
         }
       }
     }
@@ -353,19 +425,21 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint32_t* ldsu) 
 
 // ----------------------------------------------------------------------------------------
 // C work-group: row bucket a, a group of tg column tiles.  Per tile, the 4 waves accumulate
-// v1(i) C[i, tile] (and w_i v1(i) C) over the bucket's rows, combine in fixed order, and
-// thread b folds the tile's columns of bucket b: S_C[a, b] += sum v2(j) colsum[j]
-// (T_C with w_j, R_C from the row-weighted column sums).  One partial per tile group.
+// v1(i) C[i, tile] (and w_i v1(i) C) over the bucket's rows in FP64, combine in fixed order,
+// and thread b folds the tile's columns of bucket b from the tile's bucket-sorted column list
+// (staged in LDS with the row loads): S_C[a, b] += sum v2(j) colsum[j] (T_C with w_j, R_C from
+// the row-weighted sums).  One partial per tile group.
 
-template <bool MOM, int G>
-__device__ void c_unit(const StreamArgs& s, int u, double* lds) {
+template <bool MOM, int G, bool VEC>
+__device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) {
+  constexpr int U = 4;
   const int m = s.m;
   const int a = u / s.npc, gi = u - a * s.npc;
   const int t0 = gi * s.tg;
   const int t1 = (t0 + s.tg < s.TC) ? t0 + s.tg : s.TC;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int p0 = s.off1[a], p1 = s.off1[a + 1];
-  const bool vec = s.vec_c != 0;
+  const bool patched = s.patch_rowptr != nullptr;
   double* comb = lds;                          // [2][4][8][64]
   double* cs = lds + (MOM ? 4096 : 2048);      // [2][512]
   double fS[G], fR[G], fT[G];
@@ -377,44 +451,66 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds) {
   }
   for (int t = t0; t < t1; ++t) {
     const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
+    const bool lane_ok = col < s.n3;
+    // fold tables of this tile, loaded with the first rows
+    const uint32_t tabw =
+        reinterpret_cast<const uint32_t*>(s.ctab + static_cast<int64_t>(t) * kColTile)[threadIdx.x];
+    const int32_t* coff = s.coff + static_cast<int64_t>(t) * (m + 1);
+    int qb[G], qe[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int b = threadIdx.x + kThreads * g;
+      qb[g] = b < m ? coff[b] : 0;
+      qe[g] = b < m ? coff[b + 1] : 0;
+    }
     double acc[8], accw[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       acc[k] = 0.0;
       accw[k] = 0.0;
     }
-    for (int p = p0 + w; p < p1; p += 4 * kUnroll) {
-      f32x4 v0[kUnroll], v1[kUnroll];
-      float sg[kUnroll];
-      double sw[kUnroll];
+    for (int base = p0 + w; base < p1; base += 4 * 64) {
+      const int nr = min(64, (p1 - base + 3) / 4);
+      const int32_t pe = lane < nr ? s.perm1[base + 4 * lane] : 0;
+      for (int r0 = 0; r0 < nr; r0 += U) {
+        f32x4 v0[U], v1[U];
+        double sg[U], sw[U];
+        int64_t rows[U];
 #pragma unroll
-      for (int q = 0; q < kUnroll; ++q) {
-        const int pp = p + 4 * q;
-        if (pp < p1) {
-          const int32_t e = s.perm1[pp];
+        for (int q = 0; q < U; ++q) {
+          const bool ok = r0 + q < nr;
+          const int32_t e = row_entry(pe, ok ? r0 + q : 0);
           const int64_t row = e & 0x7fffffff;
-          sg[q] = e < 0 ? -1.0f : 1.0f;
-          sw[q] = MOM ? static_cast<double>(sg[q]) * static_cast<double>(row + 1) * s.inv_l1
-                      : 0.0;
-          load8f(s.C + row * s.n3, col, s.n3, vec, v0[q], v1[q]);
-          if (s.patch_rowptr != nullptr) apply_patches(s, row, col, v0[q], v1[q]);
-        } else {
-          sg[q] = 0.0f;
-          sw[q] = 0.0;
-          v0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-          v1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+          rows[q] = row;
+          sg[q] = ok ? (e < 0 ? -1.0 : 1.0) : 0.0;
+          sw[q] = MOM ? sg[q] * static_cast<double>(row + 1) * s.inv_l1 : 0.0;
+          if (VEC) {
+            load8f_sel(s.C + row * s.n3 + col, ok && lane_ok, s.zero, v0[q], v1[q]);
+          } else if (ok) {
+            load8f(s.C + row * s.n3, col, s.n3, false, v0[q], v1[q]);
+          } else {
+            v0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+            v1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
         }
-      }
+        if (patched) {
 #pragma unroll
-      for (int q = 0; q < kUnroll; ++q) {
+          for (int q = 0; q < U; ++q) {
+            if (r0 + q < nr) apply_patches(s, rows[q], col, v0[q], v1[q]);
+          }
+        }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float x = e < 4 ? v0[q][e] : v1[q][e - 4];
-          acc[e] += static_cast<double>(sg[q] * x);
-          if (MOM) accw[e] = fma(sw[q], static_cast<double>(x), accw[e]);
+        for (int q = 0; q < U; ++q) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const double x = static_cast<double>(e < 4 ? v0[q][e] : v1[q][e - 4]);
+            acc[e] = fma(x, sg[q], acc[e]);
+            if (MOM) accw[e] = fma(x, sw[q], accw[e]);
+          }
         }
       }
     }
+    reinterpret_cast<uint32_t*>(tabL)[threadIdx.x] = tabw;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       comb[(w * 8 + k) * 64 + lane] = acc[k];
@@ -435,25 +531,19 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds) {
       }
     }
     __syncthreads();
-    const int32_t* coff = s.coff + static_cast<int64_t>(t) * (m + 1);
-    const uint16_t* ctab = s.ctab + static_cast<int64_t>(t) * kColTile;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const int b = threadIdx.x + kThreads * g;
-      if (b < m) {
-        const int q1 = coff[b + 1];
-        for (int q = coff[b]; q < q1; ++q) {
-          const uint32_t e = ctab[q];
-          const int cc = e & 0x7fff;
-          const double sgd = (e & 0x8000u) ? -1.0 : 1.0;
-          const double x = sgd * cs[cc];
-          fS[g] += x;
-          if (MOM) {
-            const double wj = static_cast<double>(static_cast<int64_t>(t) * kColTile + cc + 1) *
-                              s.inv_l3;
-            fT[g] = fma(x, wj, fT[g]);
-            fR[g] += sgd * cs[512 + cc];
-          }
+      for (int q = qb[g]; q < qe[g]; ++q) {
+        const uint32_t e = tabL[q];
+        const int cc = e & 0x7fff;
+        const double sgd = (e & 0x8000u) ? -1.0 : 1.0;
+        const double x = sgd * cs[cc];
+        fS[g] += x;
+        if (MOM) {
+          const double wj = static_cast<double>(static_cast<int64_t>(t) * kColTile + cc + 1) *
+                            s.inv_l3;
+          fT[g] = fma(x, wj, fT[g]);
+          fR[g] += sgd * cs[512 + cc];
         }
       }
     }
@@ -473,167 +563,67 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds) {
   }
 }
 
-template <int DT, bool MOM, int RB, int G>
+// LDS layout of the stream kernel (dynamic): the A/C combine area or the staged B chunk first,
+// then the sorted column list of the current B chunk or C tile.
+template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
 __global__ __launch_bounds__(kThreads) void stream_kernel(StreamArgs s) {
   extern __shared__ double lds_dyn[];
   __shared__ uint32_t ldsu[kThreads / 64];
+  // tables follow the larger of the B chunk (32 KiB) and the combine area (20 or 40 KiB)
+  uint16_t* tabL = reinterpret_cast<uint16_t*>(lds_dyn + (MOM ? 5120 : 4096));
   int u = blockIdx.x;
   if (u < s.nA) {
-    a_unit<DT, MOM>(s, u, lds_dyn, ldsu);
+    a_unit<DT, MOM, VEC>(s, u, lds_dyn, ldsu);
     return;
   }
   u -= s.nA;
   if (u < s.nB) {
-    b_unit<DT, MOM, RB, G>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
+    b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
     return;
   }
-  c_unit<MOM, G>(s, u - s.nB, lds_dyn);
+  c_unit<MOM, G, VEC>(s, u - s.nB, lds_dyn, tabL);
 }
 
 // ----------------------------------------------------------------------------------------
-// Product.  Work-group (tile, slice): output tile of ts x ts buckets, k in [slice*ksl, ...).
+// Product and decision: three kernels ordered by their kernel boundaries, with no
+// cross-work-group synchronization inside any of them.
+//   product_kernel  (tile, slice): partial P Q over one k-slab (FP64 accumulation of the FP32
+//                   factors); with a single slice it finishes the tile itself;
+//   reduce_kernel   (tile): sums the slices in slice order, subtracts the C grid, stores S (R, T)
+//                   and, for the probe, the tile's sum |S|, max |S| and non-finite count;
+//   decide_kernel   (one work-group): clipped-mean noise, threshold and verdict.
 
+// Block reductions: fixed butterfly within each wave, then the 4 wave results in order.
 __device__ double block_sum_d(double v, double* red) {
-  red[threadIdx.x] = v;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
-  for (int st = kThreads / 2; st > 0; st >>= 1) {
-    if (threadIdx.x < st) red[threadIdx.x] += red[threadIdx.x + st];
-    __syncthreads();
-  }
-  const double r = red[0];
+  const double r = (red[0] + red[1]) + (red[2] + red[3]);
   __syncthreads();
   return r;
 }
 
 __device__ double block_max_d(double v, double* red) {
-  red[threadIdx.x] = v;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
-  for (int st = kThreads / 2; st > 0; st >>= 1) {
-    if (threadIdx.x < st) red[threadIdx.x] = fmax(red[threadIdx.x], red[threadIdx.x + st]);
-    __syncthreads();
-  }
-  const double r = red[0];
+  const double r = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
   __syncthreads();
   return r;
 }
 
-// Arrival at a self-resetting counter; returns true in the last of `expected` work-groups.
-__device__ bool arrive_last(uint32_t* cnt, uint32_t expected, int* flag) {
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    const uint32_t old = atomicAdd(cnt, 1u);
-    const int last = (old == expected - 1) ? 1 : 0;
-    if (last) *cnt = 0u;
-    *flag = last;
-  }
-  __syncthreads();
-  const bool last = *flag != 0;
-  if (last) __threadfence();
-  return last;
-}
-
+// Subtract the C grid (sum of its column-group partials), store S (R, T) and, in probe mode,
+// the tile statistics.  acc holds the full P Q (and Pw Q, P Qw) of this thread's outputs.
 template <int TS, bool MOM>
-__global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
+__device__ void finish_tile(const ProductArgs& pa, int tile,
+                            const double (&acc)[MOM ? 3 : 1][TS / 16][TS / 16], double* red) {
   constexpr int RT = TS / 16;
-  constexpr int KC = 16;
-  constexpr int NX = MOM ? 3 : 1;
-  __shared__ double Ps[MOM ? 2 : 1][TS][KC + 1];
-  __shared__ double Qs[MOM ? 2 : 1][KC][TS + 1];
-  __shared__ double red[kThreads];
-  __shared__ int flag;
   const int m = pa.m;
-  const int ntiles = pa.nt * pa.nt;
-  const int tile = blockIdx.x, slice = blockIdx.y;
   const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
   const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
-  const int k0 = slice * pa.ksl;
-  const int k1 = (k0 + pa.ksl < pa.n2) ? k0 + pa.ksl : pa.n2;
-  double acc[NX][RT][RT];
-#pragma unroll
-  for (int x = 0; x < NX; ++x)
-#pragma unroll
-    for (int i = 0; i < RT; ++i)
-#pragma unroll
-      for (int j = 0; j < RT; ++j) acc[x][i][j] = 0.0;
-
-  for (int kc = k0; kc < k1; kc += KC) {
-    for (int idx = threadIdx.x; idx < TS * KC; idx += kThreads) {
-      const int r = idx / KC, kk = idx - r * KC;
-      const int row = ta * TS + r, k = kc + kk;
-      const bool ok = row < m && k < k1;
-      const int64_t o = static_cast<int64_t>(row) * pa.n2 + k;
-      Ps[0][r][kk] = ok ? static_cast<double>(pa.P[o]) : 0.0;
-      if (MOM) Ps[1][r][kk] = ok ? static_cast<double>(pa.Pw[o]) : 0.0;
-    }
-    for (int idx = threadIdx.x; idx < KC * TS; idx += kThreads) {
-      const int kk = idx / TS, c = idx - kk * TS;
-      const int colb = tb * TS + c, k = kc + kk;
-      const bool ok = colb < m && k < k1;
-      const int64_t o = static_cast<int64_t>(k) * m + colb;
-      Qs[0][kk][c] = ok ? static_cast<double>(pa.Q[o]) : 0.0;
-      if (MOM) Qs[1][kk][c] = ok ? static_cast<double>(pa.Qw[o]) : 0.0;
-    }
-    __syncthreads();
-#pragma unroll 4
-    for (int kk = 0; kk < KC; ++kk) {
-      double pv[RT], qv[RT], pwv[RT], qwv[RT];
-#pragma unroll
-      for (int i = 0; i < RT; ++i) {
-        pv[i] = Ps[0][ty + 16 * i][kk];
-        if (MOM) pwv[i] = Ps[1][ty + 16 * i][kk];
-      }
-#pragma unroll
-      for (int j = 0; j < RT; ++j) {
-        qv[j] = Qs[0][kk][tx + 16 * j];
-        if (MOM) qwv[j] = Qs[1][kk][tx + 16 * j];
-      }
-#pragma unroll
-      for (int i = 0; i < RT; ++i) {
-#pragma unroll
-        for (int j = 0; j < RT; ++j) {
-          acc[0][i][j] = fma(pv[i], qv[j], acc[0][i][j]);
-          if (MOM) {
-            acc[1][i][j] = fma(pwv[i], qv[j], acc[1][i][j]);
-            acc[2][i][j] = fma(pv[i], qwv[j], acc[2][i][j]);
-          }
-        }
-      }
-    }
-    __syncthreads();
-  }
-
-  // Split-K: publish the partial and let the last slice of this tile reduce in slice order.
-  if (pa.NS > 1) {
-    double* sc = pa.scratch;
-#pragma unroll
-    for (int x = 0; x < NX; ++x)
-#pragma unroll
-      for (int i = 0; i < RT; ++i)
-#pragma unroll
-        for (int j = 0; j < RT; ++j) {
-          const int64_t o = ((static_cast<int64_t>(slice) * ntiles + tile) * NX + x) * TS * TS +
-                            (ty + 16 * i) * TS + tx + 16 * j;
-          sc[o] = acc[x][i][j];
-        }
-    if (!arrive_last(pa.tile_cnt + tile, static_cast<uint32_t>(pa.NS), &flag)) return;
-#pragma unroll
-    for (int x = 0; x < NX; ++x)
-#pragma unroll
-      for (int i = 0; i < RT; ++i)
-#pragma unroll
-        for (int j = 0; j < RT; ++j) {
-          double v = 0.0;
-          for (int sl = 0; sl < pa.NS; ++sl) {
-            const int64_t o = ((static_cast<int64_t>(sl) * ntiles + tile) * NX + x) * TS * TS +
-                              (ty + 16 * i) * TS + tx + 16 * j;
-            v += __builtin_nontemporal_load(sc + o);
-          }
-          acc[x][i][j] = v;
-        }
-  }
-
-  // Subtract the C grid (sum of its column-group partials) and store S (R, T).
+  const int64_t mm = static_cast<int64_t>(m) * m;
   double lsum = 0.0, lmax = 0.0, lbad = 0.0;
 #pragma unroll
   for (int i = 0; i < RT; ++i)
@@ -642,8 +632,8 @@ __global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
       const int row = ta * TS + ty + 16 * i, colb = tb * TS + tx + 16 * j;
       if (row < m && colb < m) {
         const int64_t o = static_cast<int64_t>(row) * m + colb;
-        const int64_t mm = static_cast<int64_t>(m) * m;
         double cS = 0.0, cR = 0.0, cT = 0.0;
+#pragma unroll 8
         for (int g = 0; g < pa.npc; ++g) {
           cS += pa.partS[g * mm + o];
           if (MOM) {
@@ -667,8 +657,6 @@ __global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
       }
     }
   if (pa.mode != 1) return;
-
-  // Probe decision: per-tile statistics, then the last tile computes the verdict.
   const double tsum = block_sum_d(lsum, red);
   const double tmax = block_max_d(lmax, red);
   const double tbad = block_sum_d(lbad, red);
@@ -677,9 +665,148 @@ __global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
     pa.tilestat[tile * 4 + 1] = tmax;
     pa.tilestat[tile * 4 + 2] = tbad;
   }
-  if (!arrive_last(pa.glob_cnt, static_cast<uint32_t>(ntiles), &flag)) return;
+}
 
+// Product partials.  Each k-chunk of the slab (KCH columns of P and rows of Q, 16 KiB of FP32
+// per factor) is fetched with every thread issuing all of its loads before any is used, so a
+// chunk costs one memory round trip; the FMAs run in FP64 on the FP32 factors.
+template <int TS, bool MOM>
+__global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
+  constexpr int RT = TS / 16;
+  constexpr int NX = MOM ? 3 : 1;
+  constexpr int NF = MOM ? 2 : 1;                 // factors per side
+  constexpr int KCH = (MOM ? 2048 : 4096) / TS;   // k per chunk
+  constexpr int PER = TS * KCH / kThreads;        // loads per thread per factor
+  __shared__ float Ps[NF][TS][KCH + 1];
+  __shared__ float Qs[NF][KCH][TS + 1];
+  __shared__ double red[kThreads / 64];
+  const int m = pa.m;
+  const int ntiles = pa.nt * pa.nt;
+  const int tile = blockIdx.x, slice = blockIdx.y;
+  const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
+  const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
+  const int k0 = slice * pa.ksl;
+  const int k1 = (k0 + pa.ksl < pa.n2) ? k0 + pa.ksl : pa.n2;
+  double acc[NX][RT][RT];
+#pragma unroll
+  for (int x = 0; x < NX; ++x)
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int j = 0; j < RT; ++j) acc[x][i][j] = 0.0;
+
+  for (int kc = k0; kc < k1; kc += KCH) {
+    float pv[NF][PER], qv[NF][PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int idx = threadIdx.x + kThreads * e;
+      {
+        const int r = idx / KCH, kk = idx - r * KCH;
+        const int row = ta * TS + r, k = kc + kk;
+        const bool ok = row < m && k < k1;
+        const int64_t o = static_cast<int64_t>(row) * pa.n2 + k;
+        pv[0][e] = ok ? pa.P[o] : 0.0f;
+        if (MOM) pv[NF - 1][e] = ok ? pa.Pw[o] : 0.0f;
+      }
+      {
+        const int kk = idx / TS, c = idx - kk * TS;
+        const int colb = tb * TS + c, k = kc + kk;
+        const bool ok = colb < m && k < k1;
+        const int64_t o = static_cast<int64_t>(k) * m + colb;
+        qv[0][e] = ok ? pa.Q[o] : 0.0f;
+        if (MOM) qv[NF - 1][e] = ok ? pa.Qw[o] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const int idx = threadIdx.x + kThreads * e;
+      const int r = idx / KCH, kk = idx - r * KCH;
+      const int kq = idx / TS, c = idx - kq * TS;
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        Ps[f][r][kk] = pv[f][e];
+        Qs[f][kq][c] = qv[f][e];
+      }
+    }
+    __syncthreads();
+    const int kn = (k1 - kc < KCH) ? k1 - kc : KCH;
+#pragma unroll 4
+    for (int kk = 0; kk < kn; ++kk) {
+      double a[RT], aw[RT], b[RT], bw[RT];
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+        a[i] = static_cast<double>(Ps[0][ty + 16 * i][kk]);
+        aw[i] = MOM ? static_cast<double>(Ps[NF - 1][ty + 16 * i][kk]) : 0.0;
+      }
+#pragma unroll
+      for (int j = 0; j < RT; ++j) {
+        b[j] = static_cast<double>(Qs[0][kk][tx + 16 * j]);
+        bw[j] = MOM ? static_cast<double>(Qs[NF - 1][kk][tx + 16 * j]) : 0.0;
+      }
+#pragma unroll
+      for (int i = 0; i < RT; ++i) {
+#pragma unroll
+        for (int j = 0; j < RT; ++j) {
+          acc[0][i][j] = fma(a[i], b[j], acc[0][i][j]);
+          if (MOM) {
+            acc[NX - 2][i][j] = fma(aw[i], b[j], acc[NX - 2][i][j]);
+            acc[NX - 1][i][j] = fma(a[i], bw[j], acc[NX - 1][i][j]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  if (pa.NS > 1) {
+#pragma unroll
+    for (int x = 0; x < NX; ++x)
+#pragma unroll
+      for (int i = 0; i < RT; ++i)
+#pragma unroll
+        for (int j = 0; j < RT; ++j) {
+          const int64_t o = ((static_cast<int64_t>(slice) * ntiles + tile) * NX + x) * TS * TS +
+                            (ty + 16 * i) * TS + tx + 16 * j;
+          pa.scratch[o] = acc[x][i][j];
+        }
+    return;
+  }
+  finish_tile<TS, MOM>(pa, tile, acc, red);
+}
+
+template <int TS, bool MOM>
+__global__ __launch_bounds__(kThreads) void reduce_kernel(ProductArgs pa) {
+  constexpr int RT = TS / 16;
+  constexpr int NX = MOM ? 3 : 1;
+  __shared__ double red[kThreads / 64];
+  const int ntiles = pa.nt * pa.nt;
+  const int tile = blockIdx.x;
+  const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
+  double acc[NX][RT][RT];
+#pragma unroll
+  for (int x = 0; x < NX; ++x)
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int j = 0; j < RT; ++j) {
+        double v = 0.0;
+#pragma unroll 8
+        for (int sl = 0; sl < pa.NS; ++sl) {
+          const int64_t o = ((static_cast<int64_t>(sl) * ntiles + tile) * NX + x) * TS * TS +
+                            (ty + 16 * i) * TS + tx + 16 * j;
+          v += pa.scratch[o];
+        }
+        acc[x][i][j] = v;
+      }
+  finish_tile<TS, MOM>(pa, tile, acc, red);
+}
+
+__global__ __launch_bounds__(kThreads) void decide_kernel(ProductArgs pa) {
+  __shared__ double red[kThreads / 64];
+  const int m = pa.m;
+  const int ntiles = pa.nt * pa.nt;
   double v = 0.0, vmax = 0.0, vbad = 0.0;
+#pragma unroll 4
   for (int t = threadIdx.x; t < ntiles; t += kThreads) {
     v += pa.tilestat[t * 4 + 0];
     vmax = fmax(vmax, pa.tilestat[t * 4 + 1]);
@@ -693,13 +820,16 @@ __global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
   const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / mm;
   const double clip = 5.0 * mean_abs;
   double c2 = 0.0;
+#pragma unroll 8
   for (int64_t idx = threadIdx.x; idx < static_cast<int64_t>(mm); idx += kThreads) {
     const double a = fabs(pa.S[idx]);
     c2 += a < clip ? a : clip;
   }
   const double clipped = block_sum_d(c2, red);
   float amax = 0.0f, bmax = 0.0f;
+#pragma unroll 8
   for (int i = threadIdx.x; i < pa.nA; i += kThreads) amax = fmaxf(amax, pa.maxpart[i]);
+#pragma unroll 8
   for (int i = threadIdx.x; i < pa.nB; i += kThreads) bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
   const double maxA = block_max_d(static_cast<double>(amax), red);
   const double maxB = block_max_d(static_cast<double>(bmax), red);
@@ -821,52 +951,89 @@ __global__ __launch_bounds__(kThreads) void recheck_kernel(const uint16_t* A, co
 }
 
 // ----------------------------------------------------------------------------------------
+// Reference streams of known size: a plain read (XOR-folded so no load is dropped) and a
+// plain copy, 16 bytes per lane, grid-stride.
+
+__global__ __launch_bounds__(kThreads) void read_kernel(const u32x4* src, int64_t n16,
+                                                        uint32_t* out) {
+  uint32_t x = 0;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n16;
+       i += stride) {
+    const u32x4 v = __builtin_nontemporal_load(src + i);
+    x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+  }
+  if (x == 0x9E3779B9u) out[0] = x;   // practically never taken; keeps the loads alive
+}
+
+__global__ __launch_bounds__(kThreads) void copy_kernel(const u32x4* src, u32x4* dst,
+                                                        int64_t n16) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n16;
+       i += stride) {
+    dst[i] = __builtin_nontemporal_load(src + i);
+  }
+}
+
+// ----------------------------------------------------------------------------------------
 // Launchers.
 
 template <int DT, bool MOM>
-static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, size_t lds,
+static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, int ng, size_t lds,
                                   hipStream_t st) {
   const int grid = s.nA + s.nB + s.nC;
   if (grid <= 0) return hipSuccess;
-#define FPSK_STREAM_CASE(RB_, G_)                                                     \
-  if (rb == RB_ && g == G_) {                                                         \
-    hipLaunchKernelGGL((stream_kernel<DT, MOM, RB_, G_>), dim3(grid), dim3(kThreads), \
-                       lds, st, s);                                                   \
-    return hipGetLastError();                                                         \
+  const bool vec = s.vec_a && s.vec_b && s.vec_c;
+#define FPSK_STREAM_CASE(RB_, G_, NG_)                                                        \
+  if (rb == RB_ && g == G_ && ng == NG_) {                                                    \
+    if (vec) {                                                                                \
+      hipLaunchKernelGGL((stream_kernel<DT, MOM, RB_, G_, NG_, true>), dim3(grid),            \
+                         dim3(kThreads), lds, st, s);                                         \
+    } else {                                                                                  \
+      hipLaunchKernelGGL((stream_kernel<DT, MOM, RB_, G_, NG_, false>), dim3(grid),           \
+                         dim3(kThreads), lds, st, s);                                         \
+    }                                                                                         \
+    return hipGetLastError();                                                                 \
   }
-  FPSK_STREAM_CASE(8, 1)
-  FPSK_STREAM_CASE(8, 2)
-  FPSK_STREAM_CASE(4, 4)
-  FPSK_STREAM_CASE(2, 8)
-  FPSK_STREAM_CASE(1, 16)
+  FPSK_STREAM_CASE(8, 1, 4)
+  FPSK_STREAM_CASE(8, 1, 2)
+  FPSK_STREAM_CASE(8, 1, 1)
+  FPSK_STREAM_CASE(8, 2, 1)
+  FPSK_STREAM_CASE(4, 4, 1)
+  FPSK_STREAM_CASE(2, 8, 1)
+  FPSK_STREAM_CASE(1, 16, 1)
 #undef FPSK_STREAM_CASE
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g,
+hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g, int ng,
                          size_t lds_bytes, hipStream_t st) {
   if (dt == 1) {
-    return moments ? stream_dispatch<1, true>(s, rb, g, lds_bytes, st)
-                   : stream_dispatch<1, false>(s, rb, g, lds_bytes, st);
+    return moments ? stream_dispatch<1, true>(s, rb, g, ng, lds_bytes, st)
+                   : stream_dispatch<1, false>(s, rb, g, ng, lds_bytes, st);
   }
-  return moments ? stream_dispatch<0, true>(s, rb, g, lds_bytes, st)
-                 : stream_dispatch<0, false>(s, rb, g, lds_bytes, st);
+  return moments ? stream_dispatch<0, true>(s, rb, g, ng, lds_bytes, st)
+                 : stream_dispatch<0, false>(s, rb, g, ng, lds_bytes, st);
 }
 
 hipError_t launch_product(const ProductArgs& a, int ts, bool moments, hipStream_t st) {
   const dim3 grid(a.nt * a.nt, a.NS);
-#define FPSK_PRODUCT_CASE(TS_)                                                               \
-  if (ts == TS_) {                                                                           \
-    if (moments) {                                                                           \
-      hipLaunchKernelGGL((product_kernel<TS_, true>), grid, dim3(kThreads), 0, st, a);      \
-    } else {                                                                                 \
-      hipLaunchKernelGGL((product_kernel<TS_, false>), grid, dim3(kThreads), 0, st, a);     \
-    }                                                                                        \
-    return hipGetLastError();                                                                \
+  const dim3 rgrid(a.nt * a.nt);
+#define FPSK_PRODUCT_CASE(TS_, MOM_)                                                       \
+  if (ts == TS_ && moments == MOM_) {                                                      \
+    hipLaunchKernelGGL((product_kernel<TS_, MOM_>), grid, dim3(kThreads), 0, st, a);       \
+    if (a.NS > 1) {                                                                        \
+      hipLaunchKernelGGL((reduce_kernel<TS_, MOM_>), rgrid, dim3(kThreads), 0, st, a);     \
+    }                                                                                      \
+    if (a.mode == 1) hipLaunchKernelGGL(decide_kernel, dim3(1), dim3(kThreads), 0, st, a); \
+    return hipGetLastError();                                                              \
   }
-  FPSK_PRODUCT_CASE(16)
-  FPSK_PRODUCT_CASE(32)
-  FPSK_PRODUCT_CASE(64)
+  FPSK_PRODUCT_CASE(16, false)
+  FPSK_PRODUCT_CASE(16, true)
+  FPSK_PRODUCT_CASE(32, false)
+  FPSK_PRODUCT_CASE(32, true)
+  FPSK_PRODUCT_CASE(64, false)
+  FPSK_PRODUCT_CASE(64, true)
 #undef FPSK_PRODUCT_CASE
   return hipErrorInvalidValue;
 }
@@ -907,6 +1074,18 @@ hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, const float* C, 
     hipLaunchKernelGGL(recheck_kernel<0>, dim3(grid), dim3(kThreads), 0, st, A, B, C, n2, n3,
                        coords, n, gamma, abssum, cval);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_read(const void* src, int64_t bytes, uint32_t* out, int grid, hipStream_t st) {
+  hipLaunchKernelGGL(read_kernel, dim3(grid), dim3(kThreads), 0, st,
+                     static_cast<const u32x4*>(src), bytes / 16, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int grid, hipStream_t st) {
+  hipLaunchKernelGGL(copy_kernel, dim3(grid), dim3(kThreads), 0, st,
+                     static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), bytes / 16);
   return hipGetLastError();
 }
 

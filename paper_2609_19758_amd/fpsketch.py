@@ -76,6 +76,8 @@ _SIGS = {
     "fpsketch_timing": (ctypes.c_int, [_P, _I32]),
     "fpsketch_timing_read": (ctypes.c_int, [_P, ctypes.POINTER(_D), ctypes.POINTER(_D),
                                             ctypes.POINTER(_I64)]),
+    "fpsketch_stream_read": (ctypes.c_int, [_P, _I64, _P, _I32, _P]),
+    "fpsketch_stream_copy": (ctypes.c_int, [_P, _P, _I64, _I32, _P]),
     "fpsketch_hash_table": (ctypes.c_int, [_U64, _I32, _I32, _I64, _I32,
                                            ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_int8)]),
     "fpsketch_m_start": (ctypes.c_int, [_I64, _I64, _I64, ctypes.c_int, ctypes.POINTER(Params),
@@ -203,6 +205,16 @@ def rms_hat_samples(samples: np.ndarray) -> float:
     s = np.ascontiguousarray(samples, dtype=np.float32)
     return float(load().fpsketch_rms_hat_samples(
         s.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), s.size))
+
+
+def stream_read(src, nbytes: int, d_out, grid: int = 2048, stream=None):
+    _check(load().fpsketch_stream_read(_ptr(src), nbytes, _ptr(d_out), grid, _stream(stream)),
+           "fpsketch_stream_read")
+
+
+def stream_copy(src, dst, nbytes: int, grid: int = 2048, stream=None):
+    _check(load().fpsketch_stream_copy(_ptr(src), _ptr(dst), nbytes, grid, _stream(stream)),
+           "fpsketch_stream_copy")
 
 
 # ---- context -----------------------------------------------------------------------------

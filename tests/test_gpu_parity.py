@@ -124,7 +124,9 @@ def test_probe_verdicts_match_oracle(fk):
         assert int(flag.item()) == int(expect_dirty)
         assert abs(st["sigma_hat"] / ref.sigma_hat - 1) < 0.05
         assert abs(st["tau"] / ref.tau - 1) < 1e-12
-        assert abs(st["max_abs"] / ref.max_abs - 1) < 1e-3 or ref.max_abs < 1e-6
+        # on a clean product max|S| is itself noise: compare within the FP32-storage bound
+        DS, _, _ = o.abs_contributions(a64, b64, cc.astype(np.float64), hr)
+        assert abs(st["max_abs"] - ref.max_abs) <= 2.0 ** -20 * DS.max()
     v.close()
 
 
