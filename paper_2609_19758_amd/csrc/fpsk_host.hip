@@ -212,55 +212,97 @@ double rms_hat_from_samples(const float* s, int64_t count) {
 
 struct HostRound {
   int m = 0;
+  int cap = 0;
+  bool mom = false;
   std::vector<int32_t> h1, h2;
   std::vector<int8_t> v1, v2;
-  std::vector<int32_t> perm1, off1, coff, boff;
+  std::vector<int32_t> perm, coff, boff;
   std::vector<uint16_t> ctab, btab;
+  std::vector<uint8_t> bsign;
 };
 
-// Column tiles of width W sorted by bucket (stable in column order).
+// Bucket segments are padded to a multiple of 8 for m <= 256 (the kernels then fold 8 list
+// entries per step); above that the lists are unpadded.
+int table_pad(int m) { return m <= 256 ? 8 : 1; }
+
+int64_t table_stride(int m, int64_t W) {
+  const int64_t s = W + static_cast<int64_t>(table_pad(m) - 1) * m;
+  return (s + 7) / 8 * 8;
+}
+
+// Staged LDS slot of column offset cc in a B chunk of W columns (W: the zero sentinel slot);
+// groups of 8 columns are XOR-swizzled so that neighbouring groups start on different banks.
+int64_t b_slot(int64_t cc, int64_t W) { return cc < W ? (cc ^ ((cc >> 3) & 7)) : W; }
+
+// Column tiles of width W sorted by bucket (stable in column order); segment starts per tile,
+// segments padded with the sentinel W.  Entry format: 0 = offset | (v2 < 0) << 15 (C tiles),
+// 1 = offset (B chunks with moments), 2 = staged slot (B chunks of the probe).
 void build_col_tables(const std::vector<int32_t>& h2, const std::vector<int8_t>& v2, int m,
-                      int64_t W, std::vector<uint16_t>& tab, std::vector<int32_t>& off) {
+                      int64_t W, int format, std::vector<uint16_t>& tab,
+                      std::vector<int32_t>& off) {
   const int64_t n3 = static_cast<int64_t>(h2.size());
   const int64_t T = (n3 + W - 1) / W;
-  tab.assign(static_cast<size_t>(T * W), 0);
+  const int pad = table_pad(m);
+  const int64_t stride = table_stride(m, W);
+  tab.assign(static_cast<size_t>(T * stride), static_cast<uint16_t>(W));
   off.assign(static_cast<size_t>(T * (m + 1)), 0);
-  std::vector<int32_t> cnt(static_cast<size_t>(m) + 1);
+  std::vector<int32_t> cnt(static_cast<size_t>(m) + 1), pos(static_cast<size_t>(m));
   for (int64_t t = 0; t < T; ++t) {
     const int64_t j0 = t * W, j1 = std::min(n3, j0 + W);
     std::fill(cnt.begin(), cnt.end(), 0);
     for (int64_t j = j0; j < j1; ++j) cnt[static_cast<size_t>(h2[j]) + 1]++;
-    for (int b = 0; b < m; ++b) cnt[b + 1] += cnt[b];
     int32_t* o = off.data() + t * (m + 1);
-    for (int b = 0; b <= m; ++b) o[b] = cnt[b];
+    o[0] = 0;
+    for (int b = 0; b < m; ++b) {
+      const int32_t padded = (cnt[b + 1] + pad - 1) / pad * pad;
+      o[b + 1] = o[b] + padded;
+      pos[b] = o[b];
+    }
     for (int64_t j = j0; j < j1; ++j) {
-      const int32_t pos = cnt[h2[j]]++;
-      tab[static_cast<size_t>(t * W + pos)] =
-          static_cast<uint16_t>((j - j0) | (v2[j] < 0 ? 0x8000 : 0));
+      const int32_t p = pos[h2[j]]++;
+      const int64_t cc = j - j0;
+      uint16_t e;
+      if (format == 0) {
+        e = static_cast<uint16_t>(cc | (v2[j] < 0 ? 0x8000 : 0));
+      } else if (format == 1) {
+        e = static_cast<uint16_t>(cc);
+      } else {
+        e = static_cast<uint16_t>(b_slot(cc, W));
+      }
+      tab[static_cast<size_t>(t * stride + p)] = e;
     }
   }
 }
 
-void build_round(uint64_t seed, int round, int64_t n1, int64_t n3, int m, int64_t cwb,
+void build_round(uint64_t seed, int round, int64_t n1, int64_t n3, int m, int64_t cwb, bool mom,
                  HostRound& R) {
   R.m = m;
+  R.mom = mom;
   R.h1.resize(n1);
   R.v1.resize(n1);
   R.h2.resize(n3);
   R.v2.resize(n3);
   hash_side(seed, round, 0, n1, m, R.h1.data(), R.v1.data());
   hash_side(seed, round, 1, n3, m, R.h2.data(), R.v2.data());
-  R.off1.assign(static_cast<size_t>(m) + 1, 0);
-  for (int64_t i = 0; i < n1; ++i) R.off1[static_cast<size_t>(R.h1[i]) + 1]++;
-  for (int b = 0; b < m; ++b) R.off1[b + 1] += R.off1[b];
-  std::vector<int32_t> pos(R.off1.begin(), R.off1.end() - 1);
-  R.perm1.resize(n1);
+  // rows of each bucket, ascending, padded to the largest bucket with -1
+  std::vector<int32_t> cnt(static_cast<size_t>(m), 0);
+  for (int64_t i = 0; i < n1; ++i) cnt[R.h1[i]]++;
+  R.cap = std::max(1, *std::max_element(cnt.begin(), cnt.end()));
+  R.perm.assign(static_cast<size_t>(m) * R.cap, -1);
+  std::fill(cnt.begin(), cnt.end(), 0);
   for (int64_t i = 0; i < n1; ++i) {
-    R.perm1[pos[R.h1[i]]++] =
+    const int b = R.h1[i];
+    R.perm[static_cast<size_t>(b) * R.cap + cnt[b]++] =
         static_cast<int32_t>(static_cast<uint32_t>(i) | (R.v1[i] < 0 ? 0x80000000u : 0u));
   }
-  build_col_tables(R.h2, R.v2, m, kColTile, R.ctab, R.coff);
-  build_col_tables(R.h2, R.v2, m, cwb, R.btab, R.boff);
+  build_col_tables(R.h2, R.v2, m, kColTile, 0, R.ctab, R.coff);
+  build_col_tables(R.h2, R.v2, m, cwb, mom ? 1 : 2, R.btab, R.boff);
+  // column signs as bits, padded to whole B chunks
+  const int64_t TB = (n3 + cwb - 1) / cwb;
+  R.bsign.assign(static_cast<size_t>(TB * cwb / 8), 0);
+  for (int64_t j = 0; j < n3; ++j) {
+    if (R.v2[j] < 0) R.bsign[static_cast<size_t>(j / 8)] |= static_cast<uint8_t>(1u << (j % 8));
+  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -284,6 +326,14 @@ fpsketch_status dev_alloc(DevBuf& b, size_t bytes) {
   return FPSK_OK;
 }
 
+// As dev_alloc, and a new allocation is zero-filled.
+fpsketch_status dev_alloc_zero(DevBuf& b, size_t bytes) {
+  if (b.p != nullptr && b.bytes >= bytes) return FPSK_OK;
+  FPSK_TRY(dev_alloc(b, bytes));
+  if (bytes != 0) FPSK_HIP(hipMemset(b.p, 0, bytes));
+  return FPSK_OK;
+}
+
 void dev_free(DevBuf& b) {
   if (b.p != nullptr) (void)hipFree(b.p);
   b.p = nullptr;
@@ -301,8 +351,12 @@ struct Decomp {
   int TA = 0, nA = 0;
   int rb = 8, g = 1, ng = 1, cwb = 2048, TB = 0, nB = 0;
   int TC = 0, npc = 1, tg = 1, nC = 0;
+  int ctab_stride = 0, btab_stride = 0, tab_off = 0;
   int ts = 16, nt = 1, NS = 1, ksl = 0;
   size_t lds_stream = 0;
+  int ldp = 0;                 // row length of the factors: n2 rounded up to a multiple of 4
+  // probe block product (nX > 0): work-groups of xb x xb outputs over xns k-slices
+  int xb = 0, xnb = 0, xns = 0, nX = 0;
 };
 
 Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
@@ -347,29 +401,51 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
   ksl = (ksl + kch - 1) / kch * kch;
   d.ksl = static_cast<int>(ksl);
   d.NS = static_cast<int>((n2 + ksl - 1) / ksl);
-  // [0, 32 or 40 KiB): A/C combine area or the staged B chunk; then the sorted column list of
-  // the current B chunk (cwb halfs) or C tile (512 halfs)
-  d.lds_stream = (mom ? 5120 : 4096) * sizeof(double) +
-                 static_cast<size_t>(std::max(d.cwb, kColTile)) * sizeof(uint16_t);
+  // dynamic LDS of the stream kernel: a data area (A/C combine and column sums, or the staged
+  // B chunk plus its zero column), then the staged sorted column list
+  d.ctab_stride = static_cast<int>(table_stride(m, kColTile));
+  d.btab_stride = static_cast<int>(table_stride(m, d.cwb));
+  const size_t comb = (mom ? 4096 : 2048) * sizeof(double);
+  const size_t cs = (mom ? 1040 : 520) * sizeof(double);
+  const size_t bdata = (static_cast<size_t>(fpsk::kBChunkHalfs) + d.rb) * sizeof(uint16_t);
+  const size_t data = (std::max(comb + cs, bdata) + 15) / 16 * 16;
+  d.tab_off = static_cast<int>(data);
+  d.lds_stream = data + static_cast<size_t>(std::max(d.ctab_stride, d.btab_stride)) *
+                            sizeof(uint16_t);
+  d.ldp = static_cast<int>((n2 + 3) / 4 * 4);
+  // The probe's product for m <= 64 (at most a 16 x 16 grid of output blocks) and
+  // n2 <= kMaxXSlices * kXSlice: block products over whole k-slices, then one deciding
+  // work-group.
+  const int xns = static_cast<int>((d.ldp + fpsk::kXSlice - 1) / fpsk::kXSlice);
+  if (!mom && m <= 64 && xns <= fpsk::kMaxXSlices) {
+    d.xb = (m + 15) / 16;
+    d.xnb = (m + d.xb - 1) / d.xb;
+    d.xns = xns;
+    d.nX = d.xnb * d.xnb * d.xns;
+  }
   return d;
 }
 
 struct DevRound {
   int m = 0;
+  int cap = 0;
+  bool mom = false;
   int64_t cwb = 0;
-  DevBuf perm1, off1, ctab, coff, btab, boff;
+  DevBuf perm, ctab, coff, btab, boff, bsign;
 };
 
 fpsketch_status upload_round(const HostRound& R, int64_t cwb, DevRound& D, hipStream_t st) {
   D.m = R.m;
+  D.cap = R.cap;
+  D.mom = R.mom;
   D.cwb = cwb;
   auto up = [st](DevBuf& b, const void* src, size_t bytes) -> fpsketch_status {
     FPSK_TRY(dev_alloc(b, bytes));
     if (bytes) FPSK_HIP(hipMemcpyAsync(b.p, src, bytes, hipMemcpyHostToDevice, st));
     return FPSK_OK;
   };
-  FPSK_TRY(up(D.perm1, R.perm1.data(), R.perm1.size() * 4));
-  FPSK_TRY(up(D.off1, R.off1.data(), R.off1.size() * 4));
+  FPSK_TRY(up(D.perm, R.perm.data(), R.perm.size() * 4));
+  FPSK_TRY(up(D.bsign, R.bsign.data(), R.bsign.size()));
   FPSK_TRY(up(D.ctab, R.ctab.data(), R.ctab.size() * 2));
   FPSK_TRY(up(D.coff, R.coff.data(), R.coff.size() * 4));
   FPSK_TRY(up(D.btab, R.btab.data(), R.btab.size() * 2));
@@ -380,8 +456,8 @@ fpsketch_status upload_round(const HostRound& R, int64_t cwb, DevRound& D, hipSt
 }
 
 void free_round(DevRound& D) {
-  dev_free(D.perm1);
-  dev_free(D.off1);
+  dev_free(D.perm);
+  dev_free(D.bsign);
   dev_free(D.ctab);
   dev_free(D.coff);
   dev_free(D.btab);
@@ -392,6 +468,7 @@ struct Workspace {
   Decomp d;
   bool mom = false;
   DevBuf P, Pw, Q, Qw, partS, partR, partT, scratch, S, R, T, maxpart, tilestat;
+  DevBuf xpart;                // probe block-product partials
 };
 
 fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n3, int m,
@@ -399,33 +476,35 @@ fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n
   const Decomp d = decompose(n1, n2, n3, m, mom);
   W.d = d;
   W.mom = mom;
-  const size_t fm = static_cast<size_t>(m) * static_cast<size_t>(n2) * sizeof(float);
+  // factor rows are ldp long; the padding past n2 is never written and stays zero
+  const size_t fm = static_cast<size_t>(m) * static_cast<size_t>(d.ldp) * sizeof(float);
   const size_t mm = static_cast<size_t>(m) * static_cast<size_t>(m) * sizeof(double);
-  FPSK_TRY(dev_alloc(W.P, fm));
-  FPSK_TRY(dev_alloc(W.Q, fm));
+  FPSK_TRY(dev_alloc_zero(W.P, fm));
+  FPSK_TRY(dev_alloc_zero(W.Q, fm));
   FPSK_TRY(dev_alloc(W.partS, mm * d.npc));
   FPSK_TRY(dev_alloc(W.S, mm));
   if (mom) {
-    FPSK_TRY(dev_alloc(W.Pw, fm));
-    FPSK_TRY(dev_alloc(W.Qw, fm));
+    FPSK_TRY(dev_alloc_zero(W.Pw, fm));
+    FPSK_TRY(dev_alloc_zero(W.Qw, fm));
     FPSK_TRY(dev_alloc(W.partR, mm * d.npc));
     FPSK_TRY(dev_alloc(W.partT, mm * d.npc));
     FPSK_TRY(dev_alloc(W.R, mm));
     FPSK_TRY(dev_alloc(W.T, mm));
   }
   const int tiles = d.nt * d.nt;
-  const size_t sc = d.NS > 1 ? static_cast<size_t>(d.NS) * tiles * d.ts * d.ts * (mom ? 3 : 1) *
-                                   sizeof(double)
-                             : 0;
+  // slice partials (also used with a single slice when the probe's decision is fused)
+  const size_t sc =
+      static_cast<size_t>(d.NS) * tiles * d.ts * d.ts * (mom ? 3 : 1) * sizeof(double);
   FPSK_TRY(dev_alloc(W.scratch, sc));
   FPSK_TRY(dev_alloc(W.maxpart, static_cast<size_t>(d.nA + d.nB) * sizeof(float)));
   FPSK_TRY(dev_alloc(W.tilestat, static_cast<size_t>(tiles) * 4 * sizeof(double)));
+  if (d.nX > 0) FPSK_TRY(dev_alloc(W.xpart, static_cast<size_t>(d.xns) * mm));
   return FPSK_OK;
 }
 
 void free_workspace(Workspace& W) {
   for (DevBuf* b : {&W.P, &W.Pw, &W.Q, &W.Qw, &W.partS, &W.partR, &W.partT, &W.scratch, &W.S,
-                    &W.R, &W.T, &W.maxpart, &W.tilestat}) {
+                    &W.R, &W.T, &W.maxpart, &W.tilestat, &W.xpart}) {
     dev_free(*b);
   }
 }
@@ -455,6 +534,7 @@ struct fpsketch_ctx {
   DevBuf scan_counts, scan_rows, scan_base, scan_out, samples, patch_rowptr, patch_col,
       patch_val, rc_coords, rc_gamma, rc_abs, rc_c;
   fpsketch_plan_info last_plan{};
+
   // optional per-probe event triples around the stream and product kernels
   bool timing = false;
   std::vector<hipEvent_t> events;
@@ -497,13 +577,17 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   s.n2 = c->n2;
   s.n3 = c->n3;
   s.m = d.m;
-  s.perm1 = static_cast<const int32_t*>(R.perm1.p);
-  s.off1 = static_cast<const int32_t*>(R.off1.p);
+  s.perm = static_cast<const int32_t*>(R.perm.p);
+  s.cap = R.cap;
+  s.bsign = static_cast<const uint8_t*>(R.bsign.p);
   s.ctab = static_cast<const uint16_t*>(R.ctab.p);
   s.coff = static_cast<const int32_t*>(R.coff.p);
   s.btab = static_cast<const uint16_t*>(R.btab.p);
   s.boff = static_cast<const int32_t*>(R.boff.p);
   s.cwb = d.cwb;
+  s.ctab_stride = d.ctab_stride;
+  s.btab_stride = d.btab_stride;
+  s.tab_off = d.tab_off;
   s.P = as<float>(W.P);
   s.Pw = mom ? as<float>(W.Pw) : nullptr;
   s.Q = as<float>(W.Q);
@@ -532,11 +616,10 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   // the vector path loads whole 8-element groups: every row length must be a multiple of 8
   if (c->n2 % 8 != 0 || c->n3 % 8 != 0) s.vec_a = s.vec_b = s.vec_c = 0;
   s.zero = c->zero.p;
-  if (R.cwb != d.cwb || R.m != d.m) return fail(FPSK_EINVAL, "internal: tables do not match");
-  if (ev) FPSK_HIP(hipEventRecord(ev[0], st));
-  FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.ng, d.lds_stream,
-                               st));
-  if (ev) FPSK_HIP(hipEventRecord(ev[1], st));
+  if (R.cwb != d.cwb || R.m != d.m || R.mom != mom) {
+    return fail(FPSK_EINVAL, "internal: tables do not match the pass");
+  }
+  s.ldp = d.ldp;
 
   fpsk::ProductArgs a{};
   a.P = s.P;
@@ -553,6 +636,7 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   a.tilestat = as<double>(W.tilestat);
   a.m = d.m;
   a.n2 = static_cast<int>(c->n2);
+  a.ldp = d.ldp;
   a.nt = d.nt;
   a.NS = d.NS;
   a.ksl = d.ksl;
@@ -566,6 +650,20 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   a.sigma_acc = as<double>(c->sigma_acc);
   a.mu = c->p.mu;
   a.c_valid = c->p.c_valid;
+  const double mmd = static_cast<double>(d.m) * d.m;
+  a.lim_factor = c->p.mu * std::sqrt(2.0 * std::log(mmd));
+
+  if (mode == 1 && !mom && d.nX > 0) {
+    a.nX = d.nX;
+    a.xb = d.xb;
+    a.xnb = d.xnb;
+    a.xns = d.xns;
+    a.xpart = as<double>(W.xpart);
+  }
+  if (ev) FPSK_HIP(hipEventRecord(ev[0], st));
+  FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.ng,
+                               d.lds_stream, st));
+  if (ev) FPSK_HIP(hipEventRecord(ev[1], st));
   FPSK_HIP(fpsk::launch_product(a, d.ts, mom, st));
   if (ev) FPSK_HIP(hipEventRecord(ev[2], st));
   return FPSK_OK;
@@ -574,7 +672,7 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
 fpsketch_status build_probe(fpsketch_ctx* c, int m, hipStream_t st) {
   HostRound R;
   const Decomp d = decompose(c->n1, c->n2, c->n3, m, false);
-  build_round(c->p.seed, 0, c->n1, c->n3, m, d.cwb, R);
+  build_round(c->p.seed, 0, c->n1, c->n3, m, d.cwb, false, R);
   FPSK_TRY(upload_round(R, d.cwb, c->probe_round, st));
   FPSK_TRY(ensure_workspace(c->probe_ws, c->n1, c->n2, c->n3, m, false));
   c->m = m;
@@ -681,7 +779,7 @@ fpsketch_status sketch_round(fpsketch_ctx* c, uint64_t seed, int round, int m, b
                              HostRound& HR, std::vector<double>& S, std::vector<double>& Rm,
                              std::vector<double>& T, double* maxA, double* maxB) {
   const Decomp d = decompose(c->n1, c->n2, c->n3, m, mom);
-  build_round(seed, round, c->n1, c->n3, m, d.cwb, HR);
+  build_round(seed, round, c->n1, c->n3, m, d.cwb, mom, HR);
   FPSK_TRY(upload_round(HR, d.cwb, c->aux_round, st));
   FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, mom));
   FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, C, mom, 0, nullptr, prow, pcol, pval, st));

@@ -13,6 +13,9 @@ constexpr int kColTile = 512;          // columns per A or C tile: 64 lanes x 8 
 constexpr int kBChunkHalfs = 16384;    // halfs of B staged in LDS per chunk (32 KiB)
 constexpr int kMaxM = 4096;            // largest bucket count the kernels accept
 constexpr double kHugeLimit = 3.4028234663852886e38 / 16.0;   // fp32max / 16
+// block product of the probe (m <= 64)
+constexpr int kXSlice = 4096;            // k per block-product work-group
+constexpr int kMaxXSlices = 4;           // n2 <= kMaxXSlices * kXSlice
 
 // One pass over A, B and C producing the factors of Eq. 1 (and their weighted forms).
 struct StreamArgs {
@@ -21,22 +24,31 @@ struct StreamArgs {
   const float* C;             // n1 x n3
   int64_t n1, n2, n3;
   int m;
-  // row side: rows sorted by bucket; entry = row | (v1 < 0) << 31; off1[m + 1]
-  const int32_t* perm1;
-  const int32_t* off1;
-  // C column tiles of kColTile: per tile, columns sorted by bucket as
-  // (offset in tile) | (v2 < 0) << 15, with coff[t * (m + 1) + b] segment starts
+  // row side: per bucket a, its rows at perm[a * cap + i] (ascending) as row | (v1 < 0) << 31,
+  // padded to cap entries with -1
+  const int32_t* perm;
+  int cap;
+  // C column tiles of kColTile: per tile (ctab_stride entries), columns sorted by bucket as
+  // (offset in tile) | (v2 < 0) << 15, with coff[t * (m + 1) + b] segment starts; for m <= 256
+  // each segment is padded to a multiple of 8 with the sentinel offset kColTile (a zero column)
   const uint16_t* ctab;
   const int32_t* coff;
-  // B column chunks of cwb columns, same encoding
+  // B column chunks of cwb columns: sorted lists without signs (the signs v2(j) are applied when
+  // a chunk is staged, from the bit mask bsign: bit j % 8 of byte j / 8); entries are the
+  // column offset with moments, else the column's staged LDS slot (sentinel cwb)
+  const uint8_t* bsign;
   const uint16_t* btab;
   const int32_t* boff;
   int cwb;
+  int ctab_stride, btab_stride;
+  int tab_off;                // byte offset of the staged column list in dynamic LDS
   // outputs
-  float* P;        // m x n2       H1 A
-  float* Pw;       // m x n2       H1 W1 A            (moments only)
-  float* Q;        // n2 x m       B H2^T
-  float* Qw;       // n2 x m       B W2 H2^T          (moments only)
+  // factors, row length ldp (n2 rounded up to a multiple of 4, the padding kept at zero)
+  float* P;        // m x ldp      H1 A
+  float* Pw;       // m x ldp      H1 W1 A            (moments only)
+  float* Q;        // m x ldp      (B H2^T)^T: row b holds column b of B H2^T
+  float* Qw;       // m x ldp      (B W2 H2^T)^T      (moments only)
+  int ldp;
   double* partS;   // npc x m x m  partial H1 C H2^T over column-tile groups
   double* partR;   // npc x m x m  partial H1 W1 C H2^T
   double* partT;   // npc x m x m  partial H1 C W2 H2^T
@@ -67,9 +79,10 @@ struct ProductArgs {
   double* S;
   double* R;
   double* T;
-  double* scratch;      // NS x tiles x ts^2 (x 3 with moments) split-K partials
+  double* scratch;      // NS x tiles x ts^2 (x 3 with moments) slice partials
   double* tilestat;     // tiles x 4: sum|S|, max|S|, non-finite count
   int m, n2, nt, NS, ksl, npc;
+  int ldp;              // row length of the factors
   int mode;             // 0: sketch only; 1: probe decision
   const float* maxpart;
   int nA, nB;
@@ -77,6 +90,11 @@ struct ProductArgs {
   int32_t* d_dirty;     // caller's flag (may be null)
   double* sigma_acc;    // [2] running sum of clean sigma_hat, count
   double mu, c_valid;
+  double lim_factor;    // mu sqrt(2 ln m^2): the noise limit in units of sigma_hat
+  // probe with m <= 64 (nX > 0): nX = xnb^2 xns block-product work-groups of xb x xb outputs
+  // over k-slices of kXSlice, their partials in xpart (xns x m x m, slice 0 minus the C grid)
+  int nX, xb, xnb, xns;
+  double* xpart;
 };
 
 hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g, int ng,

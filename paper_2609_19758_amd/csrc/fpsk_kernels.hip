@@ -166,7 +166,7 @@ __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) 
   const int a = u / s.TA, t = u - a * s.TA;
   const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
   const bool lane_ok = col < s.n2;
-  const int p0 = s.off1[a], p1 = s.off1[a + 1];
+  const int32_t* prow = s.perm + static_cast<int64_t>(a) * s.cap;
   double acc[8], accw[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
@@ -174,9 +174,10 @@ __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) 
     accw[k] = 0.0;
   }
   uint32_t mx = 0;
-  for (int base = p0 + w; base < p1; base += 4 * 64) {
-    const int nr = min(64, (p1 - base + 3) / 4);
-    const int32_t pe = lane < nr ? s.perm1[base + 4 * lane] : 0;
+  for (int base = w; base < s.cap; base += 4 * 64) {
+    const int32_t pe = base + 4 * lane < s.cap ? prow[base + 4 * lane] : -1;
+    const int nr = __popcll(__ballot(pe != -1));   // valid entries are a prefix of the lanes
+    if (nr == 0) break;
     for (int r0 = 0; r0 < nr; r0 += U) {
       u32x4 v[U];
       float sg[U], sw[U];
@@ -235,12 +236,12 @@ __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) 
       double v = lds[k * 64 + ln] + lds[(8 + k) * 64 + ln];
       v += lds[(16 + k) * 64 + ln];
       v += lds[(24 + k) * 64 + ln];
-      s.P[static_cast<int64_t>(a) * s.n2 + gc] = static_cast<float>(v);
+      s.P[static_cast<int64_t>(a) * s.ldp + gc] = static_cast<float>(v);
       if (MOM) {
         double vw = lds[2048 + k * 64 + ln] + lds[2048 + (8 + k) * 64 + ln];
         vw += lds[2048 + (16 + k) * 64 + ln];
         vw += lds[2048 + (24 + k) * 64 + ln];
-        s.Pw[static_cast<int64_t>(a) * s.n2 + gc] = static_cast<float>(vw);
+        s.Pw[static_cast<int64_t>(a) * s.ldp + gc] = static_cast<float>(vw);
       }
     }
   }
@@ -259,33 +260,35 @@ __device__ __forceinline__ uint32_t pick_half(uint32_t wa, uint32_t wb, int odd)
   return odd ? ((wa >> 16) | (wb & 0xffff0000u)) : ((wa & 0xffffu) | (wb << 16));
 }
 
-// Write the 8 columns held by one thread (RB rows x 8 columns) column-major into LDS.
+// Write the 8 columns held by one thread (RB rows x 8 columns) column-major into LDS.  Column e
+// of the group goes to slot e ^ sw: neighbouring groups start on different banks.
 template <int RB>
-__device__ __forceinline__ void store_cols(uint16_t* dst, const u32x4* v) {
-  if constexpr (RB == 1) {
-    *reinterpret_cast<u32x4*>(dst) = v[0];
-  } else if constexpr (RB == 2) {
+__device__ __forceinline__ void store_cols(uint16_t* dst, const u32x4* v, int sw) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      reinterpret_cast<uint32_t*>(dst)[e] = pick_half<RB>(v[0][e >> 1], v[1][e >> 1], e & 1);
-    }
-  } else if constexpr (RB == 4) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
+  for (int e = 0; e < 8; ++e) {
+    uint16_t* d = dst + (e ^ sw) * RB;
+    if constexpr (RB == 1) {
+      d[0] = static_cast<uint16_t>(v[0][e >> 1] >> (16 * (e & 1)));
+    } else if constexpr (RB == 2) {
+      *reinterpret_cast<uint32_t*>(d) = pick_half<RB>(v[0][e >> 1], v[1][e >> 1], e & 1);
+    } else if constexpr (RB == 4) {
       u32x2 o;
       o[0] = pick_half<RB>(v[0][e >> 1], v[1][e >> 1], e & 1);
       o[1] = pick_half<RB>(v[2][e >> 1], v[3][e >> 1], e & 1);
-      reinterpret_cast<u32x2*>(dst)[e] = o;
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
+      *reinterpret_cast<u32x2*>(d) = o;
+    } else {
       u32x4 o;
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) o[rr] = pick_half<RB>(v[2 * rr][e >> 1], v[2 * rr + 1][e >> 1], e & 1);
-      reinterpret_cast<u32x4*>(dst)[e] = o;
+      *reinterpret_cast<u32x4*>(d) = o;
     }
   }
+}
+
+// Staged slot of column cc of a chunk of CW columns (CW itself is the zero sentinel slot).
+template <int CW>
+__device__ __forceinline__ int col_slot(int cc) {
+  return cc < CW ? (cc ^ ((cc >> 3) & 7)) : CW;
 }
 
 // RBG consecutive halfs of one staged column.
@@ -314,15 +317,30 @@ __device__ __forceinline__ void load_col(const uint16_t* src, float* x) {
   }
 }
 
+// Loads of one B chunk in flight: 8 x 16 bytes of B, the sign bits of the thread's columns,
+// the chunk's staged column list and this thread's segment bounds.
+template <int RB, int G, int NT>
+struct BChunk {
+  static constexpr int NV = kBChunkHalfs / 8 / kThreads;
+  static constexpr int NI = NV / RB;
+  u32x4 v[NV];
+  u32x4 tv[NT];
+  uint32_t sb[NI];
+  int qb[G], qe[G];
+};
+
 template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
 __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, uint32_t* ldsu) {
   constexpr int CW = kBChunkHalfs / RB;      // columns per chunk
   constexpr int RBG = RB / NG;               // rows per fold group
   constexpr int SLOTS = kThreads / NG;       // bucket slots per fold group
-  constexpr int NV = kBChunkHalfs / 8 / kThreads;   // 16-byte loads of B per thread per chunk
-  constexpr int NT = CW / 8 / kThreads > 0 ? CW / 8 / kThreads : 1;   // table loads
-  static_assert(NV == 8, "each thread stages 64 halfs of B per chunk");
+  constexpr int PADG = (RB == 8 && G == 1) ? 8 : 1; // bucket segments padded to this multiple
+  constexpr int NT = PADG == 8 ? 2 : (CW / 8 / kThreads > 0 ? CW / 8 / kThreads : 1);
+  using Chunk = BChunk<RB, G, NT>;
+  constexpr int NI = Chunk::NI;
+  static_assert(Chunk::NV == 8, "each thread stages 64 halfs of B per chunk");
   const int m = s.m;
+  const int stride = s.btab_stride;
   const int rg = threadIdx.x / SLOTS, bslot = threadIdx.x - rg * SLOTS;
   const int64_t k0 = static_cast<int64_t>(u) * RB;
   double acc[G][RBG], accw[G][RBG];
@@ -334,76 +352,130 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
       accw[g][r] = 0.0;
     }
   }
+  if (threadIdx.x < RB) L[CW * RB + threadIdx.x] = 0;   // zero sentinel column
   uint32_t mx = 0;
-  for (int c = 0; c < s.TB; ++c) {
+
+  // Every load of chunk c, unconditionally (a chunk past the end reads the zero buffer).
+  auto issue = [&](Chunk& ch, int c) {
+    const bool live = c < s.TB;
     const int64_t cbase = static_cast<int64_t>(c) * CW;
-    // -- issue every load of this chunk: B, the sorted column list, the segment bounds
-    u32x4 v[NV];
 #pragma unroll
-    for (int it = 0; it < NV / RB; ++it) {
+    for (int it = 0; it < NI; ++it) {
       const int g8 = threadIdx.x + kThreads * it;
       const int64_t col = cbase + static_cast<int64_t>(g8) * 8;
 #pragma unroll
       for (int r = 0; r < RB; ++r) {
-        const bool ok = k0 + r < s.n2 && col < s.n3;
+        const bool ok = live && k0 + r < s.n2 && col < s.n3;
         if (VEC) {
-          v[it * RB + r] = load8h_sel(s.B + (k0 + r) * s.n3 + col, ok, s.zero);
+          ch.v[it * RB + r] = load8h_sel(s.B + (k0 + r) * s.n3 + col, ok, s.zero);
         } else {
-          v[it * RB + r] = ok ? load8h(s.B + (k0 + r) * s.n3, col, s.n3, false)
-                              : u32x4{0u, 0u, 0u, 0u};
+          ch.v[it * RB + r] = ok ? load8h(s.B + (k0 + r) * s.n3, col, s.n3, false)
+                                 : u32x4{0u, 0u, 0u, 0u};
         }
       }
+      const uint8_t* sp = live ? s.bsign + cbase / 8 + g8 : static_cast<const uint8_t*>(s.zero);
+      ch.sb[it] = *sp;
     }
-    u32x4 tv[NT];
+    const uint16_t* btab = s.btab + static_cast<int64_t>(live ? c : 0) * stride;
 #pragma unroll
     for (int it = 0; it < NT; ++it) {
       const int o = (threadIdx.x + kThreads * it) * 8;
-      tv[it] = o < CW ? *reinterpret_cast<const u32x4*>(s.btab + cbase + o) : u32x4{0u, 0u, 0u, 0u};
+      const u32x4* tp = (live && o < stride) ? reinterpret_cast<const u32x4*>(btab + o)
+                                             : static_cast<const u32x4*>(s.zero);
+      ch.tv[it] = *tp;
     }
-    const int32_t* boff = s.boff + static_cast<int64_t>(c) * (m + 1);
-    int qb[G], qe[G];
+    const int32_t* boff = s.boff + static_cast<int64_t>(live ? c : 0) * (m + 1);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const int b = bslot + SLOTS * g;
-      qb[g] = b < m ? boff[b] : 0;
-      qe[g] = b < m ? boff[b + 1] : 0;
+      const int32_t* bp = (live && b < m) ? boff + b : static_cast<const int32_t*>(s.zero);
+      ch.qb[g] = bp[0];
+      ch.qe[g] = bp[1];
     }
-    // -- stage into LDS
+  };
+
+  // Stage chunk c (signs v2(j) applied to the halves) and fold it.
+  auto process = [&](Chunk& ch, int c) {
+    const int64_t cbase = static_cast<int64_t>(c) * CW;
 #pragma unroll
-    for (int it = 0; it < NV / RB; ++it) {
+    for (int it = 0; it < NI; ++it) {
       const int g8 = threadIdx.x + kThreads * it;
+      u32x4 smask;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        smask[h] = (((ch.sb[it] >> (2 * h)) & 1u) << 15) | (((ch.sb[it] >> (2 * h + 1)) & 1u) << 31);
+      }
 #pragma unroll
       for (int r = 0; r < RB; ++r) {
 #pragma unroll
-        for (int h = 0; h < 4; ++h) mx = absmax2(mx, v[it * RB + r][h]);
+        for (int h = 0; h < 4; ++h) mx = absmax2(mx, ch.v[it * RB + r][h]);
+        ch.v[it * RB + r] ^= smask;
       }
-      store_cols<RB>(L + static_cast<int64_t>(g8) * 8 * RB, v + it * RB);
+      store_cols<RB>(L + static_cast<int64_t>(g8) * 8 * RB, ch.v + it * RB, g8 & 7);
     }
 #pragma unroll
     for (int it = 0; it < NT; ++it) {
       const int o = (threadIdx.x + kThreads * it) * 8;
-      if (o < CW) *reinterpret_cast<u32x4*>(tabL + o) = tv[it];
+      if (o < stride) *reinterpret_cast<u32x4*>(tabL + o) = ch.tv[it];
     }
     __syncthreads();
-    // -- fold
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      for (int q = qb[g]; q < qe[g]; ++q) {
-        const uint32_t e = tabL[q];
-        const int cc = e & 0x7fff;
-        const float sg = (e & 0x8000u) ? -1.0f : 1.0f;
-        float x[RBG];
-        load_col<DT, RBG>(L + cc * RB + rg * RBG, x);
-        const double wj = MOM ? static_cast<double>(cbase + cc + 1) * s.inv_l3 : 0.0;
+      if constexpr (PADG == 8) {
+        // segments are whole multiples of 8 entries (sentinels read the zero slot): 8 list
+        // entries with one LDS read, their 8 columns summed in FP32, then added in FP64
+        for (int q = ch.qb[g]; q < ch.qe[g]; q += 8) {
+          const u32x4 tw = *reinterpret_cast<const u32x4*>(tabL + q);
+          float part[RBG], partw[RBG];
 #pragma unroll
-        for (int r = 0; r < RBG; ++r) {
-          const double d = static_cast<double>(sg * x[r]);
-          acc[g][r] += d;
-          if (MOM) accw[g][r] = fma(d, wj, accw[g][r]);
+          for (int r = 0; r < RBG; ++r) {
+            part[r] = 0.0f;
+            partw[r] = 0.0f;
+          }
+#pragma unroll
+          for (int z = 0; z < 8; ++z) {
+            const int e = static_cast<int>((tw[z >> 1] >> (16 * (z & 1))) & 0xffffu);
+            float x[RBG];
+            if (MOM) {
+              // MOM tables hold column offsets: slot swizzle and weight w_j per column
+              load_col<DT, RBG>(L + col_slot<CW>(e) * RB + rg * RBG, x);
+              const float wj = static_cast<float>(static_cast<double>(cbase + e + 1) * s.inv_l3);
+#pragma unroll
+              for (int r = 0; r < RBG; ++r) partw[r] = fmaf(wj, x[r], partw[r]);
+            } else {
+              load_col<DT, RBG>(L + e * RB + rg * RBG, x);   // pre-swizzled slot
+            }
+#pragma unroll
+            for (int r = 0; r < RBG; ++r) part[r] += x[r];
+          }
+#pragma unroll
+          for (int r = 0; r < RBG; ++r) {
+            acc[g][r] += static_cast<double>(part[r]);
+            if (MOM) accw[g][r] += static_cast<double>(partw[r]);
+          }
+        }
+      } else {
+        for (int q = ch.qb[g]; q < ch.qe[g]; ++q) {
+          const int e = tabL[q];
+          float x[RBG];
+          load_col<DT, RBG>(L + (MOM ? col_slot<CW>(e) : e) * RB + rg * RBG, x);
+          const double wj = MOM ? static_cast<double>(cbase + e + 1) * s.inv_l3 : 0.0;
+#pragma unroll
+          for (int r = 0; r < RBG; ++r) {
+            const double d = static_cast<double>(x[r]);
+            acc[g][r] += d;
+            if (MOM) accw[g][r] = fma(d, wj, accw[g][r]);
+          }
         }
       }
     }
     __syncthreads();
+  };
+
+  for (int c = 0; c < s.TB; ++c) {
+    Chunk ch;
+    issue(ch, c);
+    process(ch, c);
   }
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -413,8 +485,8 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
       for (int r = 0; r < RBG; ++r) {
         const int64_t k = k0 + rg * RBG + r;
         if (k < s.n2) {
-          s.Q[k * m + b] = static_cast<float>(acc[g][r]);
-          if (MOM) s.Qw[k * m + b] = static_cast<float>(accw[g][r]);
+          s.Q[static_cast<int64_t>(b) * s.ldp + k] = static_cast<float>(acc[g][r]);
+          if (MOM) s.Qw[static_cast<int64_t>(b) * s.ldp + k] = static_cast<float>(accw[g][r]);
         }
       }
     }
@@ -432,16 +504,17 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
 
 template <bool MOM, int G, bool VEC>
 __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) {
-  constexpr int U = 4;
+  constexpr int U = 8;
+  constexpr int PADG = G == 1 ? 8 : 1;       // bucket segments padded to this multiple
   const int m = s.m;
   const int a = u / s.npc, gi = u - a * s.npc;
   const int t0 = gi * s.tg;
   const int t1 = (t0 + s.tg < s.TC) ? t0 + s.tg : s.TC;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int p0 = s.off1[a], p1 = s.off1[a + 1];
+  const int32_t* prow = s.perm + static_cast<int64_t>(a) * s.cap;
   const bool patched = s.patch_rowptr != nullptr;
   double* comb = lds;                          // [2][4][8][64]
-  double* cs = lds + (MOM ? 4096 : 2048);      // [2][512]
+  double* cs = lds + (MOM ? 4096 : 2048);      // column sums [513] (+ weighted at 520)
   double fS[G], fR[G], fT[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -453,8 +526,14 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
     const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
     const bool lane_ok = col < s.n3;
     // fold tables of this tile, loaded with the first rows
-    const uint32_t tabw =
-        reinterpret_cast<const uint32_t*>(s.ctab + static_cast<int64_t>(t) * kColTile)[threadIdx.x];
+    const int stride = s.ctab_stride;
+    const uint16_t* ctab = s.ctab + static_cast<int64_t>(t) * stride;
+    u32x4 tv[2];
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int o = (threadIdx.x + kThreads * it) * 8;
+      tv[it] = o < stride ? *reinterpret_cast<const u32x4*>(ctab + o) : u32x4{0u, 0u, 0u, 0u};
+    }
     const int32_t* coff = s.coff + static_cast<int64_t>(t) * (m + 1);
     int qb[G], qe[G];
 #pragma unroll
@@ -469,9 +548,10 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
       acc[k] = 0.0;
       accw[k] = 0.0;
     }
-    for (int base = p0 + w; base < p1; base += 4 * 64) {
-      const int nr = min(64, (p1 - base + 3) / 4);
-      const int32_t pe = lane < nr ? s.perm1[base + 4 * lane] : 0;
+    for (int base = w; base < s.cap; base += 4 * 64) {
+      const int32_t pe = base + 4 * lane < s.cap ? prow[base + 4 * lane] : -1;
+      const int nr = __popcll(__ballot(pe != -1));
+      if (nr == 0) break;
       for (int r0 = 0; r0 < nr; r0 += U) {
         f32x4 v0[U], v1[U];
         double sg[U], sw[U];
@@ -510,7 +590,11 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
         }
       }
     }
-    reinterpret_cast<uint32_t*>(tabL)[threadIdx.x] = tabw;
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int o = (threadIdx.x + kThreads * it) * 8;
+      if (o < stride) *reinterpret_cast<u32x4*>(tabL + o) = tv[it];
+    }
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       comb[(w * 8 + k) * 64 + lane] = acc[k];
@@ -527,23 +611,37 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
         double vw = comb[2048 + k * 64 + ln] + comb[2048 + (8 + k) * 64 + ln];
         vw += comb[2048 + (16 + k) * 64 + ln];
         vw += comb[2048 + (24 + k) * 64 + ln];
-        cs[512 + c] = vw;
+        cs[520 + c] = vw;
       }
+    }
+    if (threadIdx.x == 0) {
+      cs[kColTile] = 0.0;            // zero sentinel column
+      if (MOM) cs[520 + kColTile] = 0.0;
     }
     __syncthreads();
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      for (int q = qb[g]; q < qe[g]; ++q) {
-        const uint32_t e = tabL[q];
-        const int cc = e & 0x7fff;
-        const double sgd = (e & 0x8000u) ? -1.0 : 1.0;
-        const double x = sgd * cs[cc];
-        fS[g] += x;
-        if (MOM) {
-          const double wj = static_cast<double>(static_cast<int64_t>(t) * kColTile + cc + 1) *
-                            s.inv_l3;
-          fT[g] = fma(x, wj, fT[g]);
-          fR[g] += sgd * cs[512 + cc];
+      for (int q = qb[g]; q < qe[g]; q += PADG) {
+        uint32_t ez[PADG];
+        if constexpr (PADG == 8) {
+          const u32x4 tw = *reinterpret_cast<const u32x4*>(tabL + q);
+#pragma unroll
+          for (int z = 0; z < 8; ++z) ez[z] = (tw[z >> 1] >> (16 * (z & 1))) & 0xffffu;
+        } else {
+          ez[0] = tabL[q];
+        }
+#pragma unroll
+        for (int z = 0; z < PADG; ++z) {
+          const int cc = ez[z] & 0x7fff;
+          const double sgd = (ez[z] & 0x8000u) ? -1.0 : 1.0;
+          const double x = sgd * cs[cc];
+          fS[g] += x;
+          if (MOM) {
+            const double wj =
+                static_cast<double>(static_cast<int64_t>(t) * kColTile + cc + 1) * s.inv_l3;
+            fT[g] = fma(x, wj, fT[g]);
+            fR[g] += sgd * cs[520 + cc];
+          }
         }
       }
     }
@@ -563,59 +661,346 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
   }
 }
 
-// LDS layout of the stream kernel (dynamic): the A/C combine area or the staged B chunk first,
-// then the sorted column list of the current B chunk or C tile.
-template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
-__global__ __launch_bounds__(kThreads) void stream_kernel(StreamArgs s) {
-  extern __shared__ double lds_dyn[];
-  __shared__ uint32_t ldsu[kThreads / 64];
-  // tables follow the larger of the B chunk (32 KiB) and the combine area (20 or 40 KiB)
-  uint16_t* tabL = reinterpret_cast<uint16_t*>(lds_dyn + (MOM ? 5120 : 4096));
-  int u = blockIdx.x;
-  if (u < s.nA) {
-    a_unit<DT, MOM, VEC>(s, u, lds_dyn, ldsu);
-    return;
-  }
-  u -= s.nA;
-  if (u < s.nB) {
-    b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
-    return;
-  }
-  c_unit<MOM, G, VEC>(s, u - s.nB, lds_dyn, tabL);
-}
-
 // ----------------------------------------------------------------------------------------
-// Product and decision: three kernels ordered by their kernel boundaries, with no
-// cross-work-group synchronization inside any of them.
-//   product_kernel  (tile, slice): partial P Q over one k-slab (FP64 accumulation of the FP32
-//                   factors); with a single slice it finishes the tile itself;
-//   reduce_kernel   (tile): sums the slices in slice order, subtracts the C grid, stores S (R, T)
-//                   and, for the probe, the tile's sum |S|, max |S| and non-finite count;
-//   decide_kernel   (one work-group): clipped-mean noise, threshold and verdict.
+// Reductions and the probe decision shared by the fused and separate product paths.
 
-// Block reductions: fixed butterfly within each wave, then the 4 wave results in order.
+// Block reductions: fixed butterfly within each wave, then the wave results in order.
+template <int NW>
 __device__ double block_sum_d(double v, double* red) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
-  const double r = (red[0] + red[1]) + (red[2] + red[3]);
+  double r = 0.0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) r += red[w];
   __syncthreads();
   return r;
 }
 
+template <int NW>
 __device__ double block_max_d(double v, double* red) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
   __syncthreads();
-  const double r = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+  double r = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) r = fmax(r, red[w]);
   __syncthreads();
   return r;
 }
 
-// Subtract the C grid (sum of its column-group partials), store S (R, T) and, in probe mode,
-// the tile statistics.  acc holds the full P Q (and Pw Q, P Qw) of this thread's outputs.
+// Fixed-order work-group reduction of NV values per thread through LDS (cross-lane shuffles
+// of doubles cost tens of cycles each).  Levels of 16: at a level over N entries, thread
+// g < N / 16 of value i combines entries g, g + N / 16, ..., g + 15 N / 16 (consecutive threads
+// read consecutive addresses; the 16 reads are issued together), until at most 16 remain,
+// which one thread per value combines in order.  Bit i of max_mask selects max instead of sum
+// for value i.  buf holds NV * (2 NT / 16 + NT + 1) doubles; every thread receives the results.
+template <int N, int NV>
+__device__ __forceinline__ void lds_reduce_level(const double* src, double* dst,
+                                                 uint32_t max_mask) {
+  if constexpr (N <= 16) {
+    if (static_cast<int>(threadIdx.x) < NV) {
+      const int i = threadIdx.x;
+      const bool mx = (max_mask >> i) & 1u;
+      double e[N];
+#pragma unroll
+      for (int q = 0; q < N; ++q) e[q] = src[i * N + q];
+      double r = e[0];
+#pragma unroll
+      for (int q = 1; q < N; ++q) r = mx ? fmax(r, e[q]) : r + e[q];
+      dst[i] = r;
+    }
+    __syncthreads();
+  } else {
+    constexpr int GN = N / 16;
+    if (static_cast<int>(threadIdx.x) < NV * GN) {
+      const int i = threadIdx.x / GN, g = threadIdx.x - i * GN;
+      const bool mx = (max_mask >> i) & 1u;
+      const double* b = src + i * N + g;
+      double e[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) e[q] = b[q * GN];
+      double r = e[0];
+#pragma unroll
+      for (int q = 1; q < 16; ++q) r = mx ? fmax(r, e[q]) : r + e[q];
+      dst[i * GN + g] = r;
+    }
+    __syncthreads();
+    lds_reduce_level<GN, NV>(dst, dst + NV * GN, max_mask);
+  }
+}
+
+template <int NT, int NV>
+__device__ void lds_reduce(double (&v)[NV], double* buf, uint32_t max_mask) {
+  static_assert(NT % 16 == 0 && NT <= 4096, "levels of 16");
+#pragma unroll
+  for (int i = 0; i < NV; ++i) buf[i * NT + threadIdx.x] = v[i];
+  __syncthreads();
+  double* tmp = buf + NV * NT;
+  lds_reduce_level<NT, NV>(buf, tmp, max_mask);
+  // the results follow the last level's inputs: locate them by replaying the level sizes
+  int n = NT;
+  double* res = tmp;
+  while (n > 16) {
+    res += NV * (n / 16);
+    n /= 16;
+  }
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = res[i];
+  __syncthreads();
+}
+
+// The probe's decision from the reduced statistics (Sec. III-B): clipped-mean noise estimate,
+// validity bound from max|A| and max|B|, threshold and verdict.
+__device__ void decide_tail(const ProductArgs& pa, double sum_abs, double max_abs, double nbad,
+                            double clipped, double maxA, double maxB) {
+  const double mm = static_cast<double>(pa.m) * pa.m;
+  const double sigma = 1.2533 * (clipped / mm);
+  const double tau = pa.c_valid * static_cast<double>(pa.n2) * 0x1p-23 * maxA * maxB;
+  const double lim = pa.lim_factor * sigma;
+  const double thr = fmin(tau, lim);
+  const bool finite = nbad == 0.0;
+  const bool clean = finite && max_abs <= thr;
+  (void)sum_abs;
+  pa.stats[0] = sigma;
+  pa.stats[1] = thr;
+  pa.stats[2] = tau;
+  pa.stats[3] = max_abs;
+  pa.stats[4] = finite ? 1.0 : 0.0;
+  pa.stats[5] = clean ? 0.0 : 1.0;
+  pa.stats[6] = maxA;
+  pa.stats[7] = maxB;
+  if (clean) {
+    pa.sigma_acc[0] += sigma;
+    pa.sigma_acc[1] += 1.0;
+  } else if (pa.d_dirty != nullptr) {
+    *pa.d_dirty = 1;
+  }
+}
+
+// LDS layout of the stream kernel (dynamic): the A/C combine area or the staged B chunk first,
+// then the sorted column list of the current B chunk or C tile.
+template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
+__global__ __launch_bounds__(kThreads, MOM ? 2 : 4) void stream_kernel(StreamArgs s) {
+  extern __shared__ double lds_dyn[];
+  __shared__ uint32_t ldsu[kThreads / 64];
+  // the sorted column list of the current B chunk or C tile follows the data area
+  uint16_t* tabL = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(lds_dyn) + s.tab_off);
+  // Work-groups are dispatched in index order: the C work-groups (the largest) come first, then
+  // B, then A, so the short A work-groups fill the tail.
+  int u = blockIdx.x;
+  if (u < s.nC) {
+    c_unit<MOM, G, VEC>(s, u, lds_dyn, tabL);
+    return;
+  }
+  u -= s.nC;
+  if (u < s.nB) {
+    b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
+    return;
+  }
+  a_unit<DT, MOM, VEC>(s, u - s.nB, lds_dyn, ldsu);
+}
+
+// ----------------------------------------------------------------------------------------
+// Probe product for m <= 64: block_product_kernel, then block_decide_kernel.
+//   block_product_kernel (block, slice): outputs (a0 .. a0 + XB) x (b0 .. b0 + XB) over the
+//     k-slice [slice * kXSlice, + kXSlice).  Thread t takes k = 4 (t + 256 j) within the slice;
+//     the dot products run in FP64 on the FP32 factors (rows of P and of the transposed Q, both
+//     k-contiguous, read with 16-byte loads that the work-groups of an XCD share through its L2);
+//     the 4 waves are combined in fixed order.  Slice 0 subtracts the C grid (the sum of the
+//     column-group partials).
+//   block_decide_kernel (one work-group): S = sum of the slice partials in slice order, the
+//     probe statistics and the verdict.
+
+template <int XB>
+__global__ __launch_bounds__(kThreads) void block_product_kernel(ProductArgs pa) {
+  constexpr int NV = XB * XB;
+  __shared__ double red[NV * (kThreads + 2 * kThreads / 16 + 1)];
+  const int m = pa.m;
+  const int64_t mm = static_cast<int64_t>(m) * m;
+  const int x = blockIdx.x;
+  const int nb2 = pa.xnb * pa.xnb;
+  const int slice = x / nb2, blk = x - slice * nb2;
+  const int rbk = blk / pa.xnb, cbk = blk - rbk * pa.xnb;
+  const int a0 = rbk * XB, b0 = cbk * XB;
+  // uniform row bases (rows past m repeat row m - 1; their results are dropped)
+  const float* prow[XB];
+  const float* qrow[XB];
+#pragma unroll
+  for (int i = 0; i < XB; ++i) {
+    prow[i] = pa.P + static_cast<int64_t>(a0 + i < m ? a0 + i : m - 1) * pa.ldp;
+    qrow[i] = pa.Q + static_cast<int64_t>(b0 + i < m ? b0 + i : m - 1) * pa.ldp;
+  }
+  // every load is issued before the first is used: the slice's factor rows, then the C grid of
+  // the block (slice 0; thread (v = t & 15, group t >> 4) takes every 16th column-group partial)
+  const int kb = slice * kXSlice;
+  // the slice in 4 / JH round trips of JH 16-byte loads per row (JH = 2 for the largest block
+  // keeps the loads within the register file)
+  constexpr int JH = XB <= 3 ? 4 : 2;
+  double acc[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) acc[v] = 0.0;
+  double c4[4];
+  const int cv = threadIdx.x & 15, gs = threadIdx.x >> 4;
+  const int ci = cv / XB, cj = cv - (cv / XB) * XB;
+  const bool vok = slice == 0 && cv < NV && a0 + ci < m && b0 + cj < m;
+  const int64_t co = vok ? static_cast<int64_t>(a0 + ci) * m + b0 + cj : 0;
+#pragma unroll
+  for (int h = 0; h < 4 / JH; ++h) {
+  float4 pv[XB][JH], qv[XB][JH];
+#pragma unroll
+  for (int j = 0; j < JH; ++j) {
+    const int k = kb + 4 * (static_cast<int>(threadIdx.x) + kThreads * (h * JH + j));
+    const bool kok = k < pa.ldp;
+    const int kk = kok ? k : 0;
+#pragma unroll
+    for (int i = 0; i < XB; ++i) {
+      const float4 p = *reinterpret_cast<const float4*>(prow[i] + kk);
+      const float4 q = *reinterpret_cast<const float4*>(qrow[i] + kk);
+      const float4 z = {0.f, 0.f, 0.f, 0.f};
+      pv[i][j] = kok ? p : z;
+      qv[i][j] = kok ? q : z;
+    }
+  }
+  if (h == 0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int g = gs + 16 * q;
+      const double c = pa.partS[static_cast<int64_t>(g < pa.npc ? g : 0) * mm + co];
+      c4[q] = (vok && g < pa.npc) ? c : 0.0;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < JH; ++j)
+#pragma unroll
+    for (int i = 0; i < XB; ++i)
+#pragma unroll
+      for (int c = 0; c < XB; ++c) {
+        double t = acc[i * XB + c];
+        t = fma(static_cast<double>(pv[i][j].x), static_cast<double>(qv[c][j].x), t);
+        t = fma(static_cast<double>(pv[i][j].y), static_cast<double>(qv[c][j].y), t);
+        t = fma(static_cast<double>(pv[i][j].z), static_cast<double>(qv[c][j].z), t);
+        t = fma(static_cast<double>(pv[i][j].w), static_cast<double>(qv[c][j].w), t);
+        acc[i * XB + c] = t;
+      }
+  }
+  double cp = (c4[0] + c4[1]) + (c4[2] + c4[3]);
+  for (int g = gs + 64; g < pa.npc; g += 16) {   // more than 64 column groups (small m)
+    cp += vok ? pa.partS[static_cast<int64_t>(g) * mm + co] : 0.0;
+  }
+  lds_reduce<kThreads, NV>(acc, red, 0u);
+  // C grid of output v: the 16 column-group sums of threads v, 16 + v, ... in order
+  red[threadIdx.x] = cp;
+  __syncthreads();
+  if (static_cast<int>(threadIdx.x) < NV) {
+    const int v = threadIdx.x;
+    const int i = v / XB, c = v - (v / XB) * XB;
+    double cg = 0.0;
+    for (int g = 0; g < 16; ++g) cg += red[g * 16 + v];
+    if (a0 + i < m && b0 + c < m) {
+      pa.xpart[slice * mm + static_cast<int64_t>(a0 + i) * m + b0 + c] = acc[v] - cg;
+    }
+  }
+}
+
+constexpr int kDecideThreads = 1024;
+
+__global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArgs pa) {
+  constexpr int NQ = 4;                       // m <= 64: m^2 <= 4096 outputs
+  __shared__ double red[5 * (kDecideThreads + 2 * kDecideThreads / 16 + 1)];
+  const int m = pa.m;
+  const int mm = m * m;
+  // every load of the work-group is issued before the first is used
+  double x[kMaxXSlices][NQ];
+#pragma unroll
+  for (int sl = 0; sl < kMaxXSlices; ++sl)
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
+      const int sc = sl < pa.xns ? sl : 0;
+      x[sl][q] = pa.xpart[static_cast<int64_t>(sc) * mm + (o < mm ? o : mm - 1)];
+    }
+  constexpr int NM = 4;                       // maxima per thread in the first pass
+  float am[NM], bm[NM];
+#pragma unroll
+  for (int q = 0; q < NM; ++q) {
+    const int i = static_cast<int>(threadIdx.x) + kDecideThreads * q;
+    am[q] = pa.maxpart[i < pa.nA ? i : pa.nA - 1];
+    bm[q] = pa.maxpart[pa.nA + (i < pa.nB ? i : pa.nB - 1)];
+  }
+  double v[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    double acc = 0.0;
+#pragma unroll
+    for (int sl = 0; sl < kMaxXSlices; ++sl) acc += sl < pa.xns ? x[sl][q] : 0.0;
+    v[q] = acc;
+  }
+  float amax = am[0], bmax = bm[0];
+#pragma unroll
+  for (int q = 1; q < NM; ++q) {
+    amax = fmaxf(amax, am[q]);
+    bmax = fmaxf(bmax, bm[q]);
+  }
+  for (int i = threadIdx.x + kDecideThreads * NM; i < pa.nA; i += kDecideThreads) {
+    amax = fmaxf(amax, pa.maxpart[i]);
+  }
+  for (int i = threadIdx.x + kDecideThreads * NM; i < pa.nB; i += kDecideThreads) {
+    bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
+  }
+  double lsum = 0.0, lmax = 0.0, lbad = 0.0;
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
+    if (o < mm) {
+      const double av = fabs(v[q]);
+      if (__builtin_isfinite(v[q])) {
+        lsum += av;
+        lmax = fmax(lmax, av);
+      } else {
+        lbad += 1.0;
+      }
+    }
+  }
+  // the five first-phase reductions in one pass (sums: 0, 2; maxima: 1, 3, 4)
+  double r5[5] = {lsum, lmax, lbad, static_cast<double>(amax), static_cast<double>(bmax)};
+  lds_reduce<kDecideThreads, 5>(r5, red, 0x1au);
+  const double sum_abs = r5[0], max_abs = r5[1], nbad = r5[2];
+  const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / static_cast<double>(mm);
+  const double clip = 5.0 * mean_abs;
+  double c2 = 0.0;
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
+    if (o < mm) {
+      const double a = fabs(v[q]);
+      c2 += a < clip ? a : clip;
+    }
+  }
+  double r1[1] = {c2};
+  lds_reduce<kDecideThreads, 1>(r1, red, 0u);
+  if (threadIdx.x == 0) decide_tail(pa, sum_abs, max_abs, nbad, r1[0], r5[3], r5[4]);
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
+    if (o < mm) pa.S[o] = v[q];
+  }
+}
+
+// ----------------------------------------------------------------------------------------
+// Product and decision, ordered by kernel boundaries only (no cross-work-group
+// synchronization inside a kernel):
+//   product_kernel  (tile, slice): partial P Q over one k-slab, FP64 accumulation of the FP32
+//                   factors; slice 0 also subtracts the C grid (the sum of its column-group
+//                   partials).  With a single slice it finishes the tile.
+//   reduce_kernel   (tile): sums the slices in slice order, stores S (R, T) and, for the probe,
+//                   the tile's sum |S|, max |S| and non-finite count;
+//   decide_kernel   (one work-group): clipped-mean noise, threshold and verdict.
+
+// Store S (R, T) of this thread's outputs and, in probe mode, the tile statistics.  acc holds
+// the full P Q - C grid (and Pw Q - R grid, P Qw - T grid).
 template <int TS, bool MOM>
 __device__ void finish_tile(const ProductArgs& pa, int tile,
                             const double (&acc)[MOM ? 3 : 1][TS / 16][TS / 16], double* red) {
@@ -623,7 +1008,6 @@ __device__ void finish_tile(const ProductArgs& pa, int tile,
   const int m = pa.m;
   const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
   const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
-  const int64_t mm = static_cast<int64_t>(m) * m;
   double lsum = 0.0, lmax = 0.0, lbad = 0.0;
 #pragma unroll
   for (int i = 0; i < RT; ++i)
@@ -632,20 +1016,11 @@ __device__ void finish_tile(const ProductArgs& pa, int tile,
       const int row = ta * TS + ty + 16 * i, colb = tb * TS + tx + 16 * j;
       if (row < m && colb < m) {
         const int64_t o = static_cast<int64_t>(row) * m + colb;
-        double cS = 0.0, cR = 0.0, cT = 0.0;
-#pragma unroll 8
-        for (int g = 0; g < pa.npc; ++g) {
-          cS += pa.partS[g * mm + o];
-          if (MOM) {
-            cR += pa.partR[g * mm + o];
-            cT += pa.partT[g * mm + o];
-          }
-        }
-        const double sv = acc[0][i][j] - cS;
+        const double sv = acc[0][i][j];
         pa.S[o] = sv;
         if (MOM) {
-          pa.R[o] = acc[1][i][j] - cR;
-          pa.T[o] = acc[2][i][j] - cT;
+          pa.R[o] = acc[1][i][j];
+          pa.T[o] = acc[2][i][j];
         }
         const double av = fabs(sv);
         if (__builtin_isfinite(sv)) {
@@ -657,9 +1032,9 @@ __device__ void finish_tile(const ProductArgs& pa, int tile,
       }
     }
   if (pa.mode != 1) return;
-  const double tsum = block_sum_d(lsum, red);
-  const double tmax = block_max_d(lmax, red);
-  const double tbad = block_sum_d(lbad, red);
+  const double tsum = block_sum_d<kThreads / 64>(lsum, red);
+  const double tmax = block_max_d<kThreads / 64>(lmax, red);
+  const double tbad = block_sum_d<kThreads / 64>(lbad, red);
   if (threadIdx.x == 0) {
     pa.tilestat[tile * 4 + 0] = tsum;
     pa.tilestat[tile * 4 + 1] = tmax;
@@ -667,18 +1042,20 @@ __device__ void finish_tile(const ProductArgs& pa, int tile,
   }
 }
 
-// Product partials.  Each k-chunk of the slab (KCH columns of P and rows of Q, 16 KiB of FP32
-// per factor) is fetched with every thread issuing all of its loads before any is used, so a
-// chunk costs one memory round trip; the FMAs run in FP64 on the FP32 factors.
+// Product partials.  Each k-chunk of the slab (KCH columns of P and of the transposed Q, 16 KiB
+// of FP32 per factor) is fetched with every thread issuing all of its loads before any is used,
+// so a chunk costs one memory round trip.  Both factors are staged k-contiguous, so the inner
+// loop reads four k at a time with 16-byte LDS reads; the FMAs run in FP64.
 template <int TS, bool MOM>
 __global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
   constexpr int RT = TS / 16;
   constexpr int NX = MOM ? 3 : 1;
   constexpr int NF = MOM ? 2 : 1;                 // factors per side
   constexpr int KCH = (MOM ? 2048 : 4096) / TS;   // k per chunk
+  constexpr int KP = KCH + 4;                     // padded LDS row (floats)
   constexpr int PER = TS * KCH / kThreads;        // loads per thread per factor
-  __shared__ float Ps[NF][TS][KCH + 1];
-  __shared__ float Qs[NF][KCH][TS + 1];
+  __shared__ __align__(16) float Ps[NF][TS][KP];
+  __shared__ __align__(16) float Qt[NF][TS][KP];
   __shared__ double red[kThreads / 64];
   const int m = pa.m;
   const int ntiles = pa.nt * pa.nt;
@@ -687,76 +1064,126 @@ __global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
   const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
   const int k0 = slice * pa.ksl;
   const int k1 = (k0 + pa.ksl < pa.n2) ? k0 + pa.ksl : pa.n2;
+  const int64_t mm = static_cast<int64_t>(m) * m;
   double acc[NX][RT][RT];
+  // slice 0 carries minus the C grid: the sum of the column-group partials of each output
+  double cg[NX][RT][RT];
 #pragma unroll
-  for (int x = 0; x < NX; ++x)
+  for (int i = 0; i < RT; ++i)
 #pragma unroll
-    for (int i = 0; i < RT; ++i)
+    for (int j = 0; j < RT; ++j) {
+      const int row = ta * TS + ty + 16 * i, colb = tb * TS + tx + 16 * j;
+      const bool ok = slice == 0 && row < m && colb < m;
+      const int64_t o = ok ? static_cast<int64_t>(row) * m + colb : 0;
+      double cS = 0.0, cR = 0.0, cT = 0.0;
+      if (ok) {
+        for (int g = 0; g < pa.npc; ++g) {
+          cS += pa.partS[g * mm + o];
+          if (MOM) {
+            cR += pa.partR[g * mm + o];
+            cT += pa.partT[g * mm + o];
+          }
+        }
+      }
+      cg[0][i][j] = cS;
+      if (MOM) {
+        cg[1][i][j] = cR;
+        cg[2][i][j] = cT;
+      }
 #pragma unroll
-      for (int j = 0; j < RT; ++j) acc[x][i][j] = 0.0;
+      for (int x = 0; x < NX; ++x) acc[x][i][j] = 0.0;
+    }
 
   for (int kc = k0; kc < k1; kc += KCH) {
     float pv[NF][PER], qv[NF][PER];
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
       const int idx = threadIdx.x + kThreads * e;
+      const int r = idx / KCH, kk = idx - r * KCH;
+      const int k = kc + kk;
       {
-        const int r = idx / KCH, kk = idx - r * KCH;
-        const int row = ta * TS + r, k = kc + kk;
+        const int row = ta * TS + r;
         const bool ok = row < m && k < k1;
-        const int64_t o = static_cast<int64_t>(row) * pa.n2 + k;
-        pv[0][e] = ok ? pa.P[o] : 0.0f;
-        if (MOM) pv[NF - 1][e] = ok ? pa.Pw[o] : 0.0f;
+        const int64_t o = ok ? static_cast<int64_t>(row) * pa.ldp + k : 0;
+        const float x = pa.P[o];
+        pv[0][e] = ok ? x : 0.0f;
+        if (MOM) {
+          const float y = pa.Pw[o];
+          pv[NF - 1][e] = ok ? y : 0.0f;
+        }
       }
       {
-        const int kk = idx / TS, c = idx - kk * TS;
-        const int colb = tb * TS + c, k = kc + kk;
+        const int colb = tb * TS + r;
         const bool ok = colb < m && k < k1;
-        const int64_t o = static_cast<int64_t>(k) * m + colb;
-        qv[0][e] = ok ? pa.Q[o] : 0.0f;
-        if (MOM) qv[NF - 1][e] = ok ? pa.Qw[o] : 0.0f;
+        const int64_t o = ok ? static_cast<int64_t>(colb) * pa.ldp + k : 0;
+        const float x = pa.Q[o];
+        qv[0][e] = ok ? x : 0.0f;
+        if (MOM) {
+          const float y = pa.Qw[o];
+          qv[NF - 1][e] = ok ? y : 0.0f;
+        }
       }
     }
 #pragma unroll
     for (int e = 0; e < PER; ++e) {
       const int idx = threadIdx.x + kThreads * e;
       const int r = idx / KCH, kk = idx - r * KCH;
-      const int kq = idx / TS, c = idx - kq * TS;
 #pragma unroll
       for (int f = 0; f < NF; ++f) {
         Ps[f][r][kk] = pv[f][e];
-        Qs[f][kq][c] = qv[f][e];
+        Qt[f][r][kk] = qv[f][e];
       }
     }
     __syncthreads();
+    // entries past k1 were staged as zeros, so whole groups of four can be used
     const int kn = (k1 - kc < KCH) ? k1 - kc : KCH;
-#pragma unroll 4
-    for (int kk = 0; kk < kn; ++kk) {
-      double a[RT], aw[RT], b[RT], bw[RT];
+    const int kn4 = (kn + 3) & ~3;
+#pragma unroll 2
+    for (int kk = 0; kk < kn4; kk += 4) {
+      float4 a[NF][RT], b[NF][RT];
 #pragma unroll
-      for (int i = 0; i < RT; ++i) {
-        a[i] = static_cast<double>(Ps[0][ty + 16 * i][kk]);
-        aw[i] = MOM ? static_cast<double>(Ps[NF - 1][ty + 16 * i][kk]) : 0.0;
-      }
+      for (int f = 0; f < NF; ++f)
 #pragma unroll
-      for (int j = 0; j < RT; ++j) {
-        b[j] = static_cast<double>(Qs[0][kk][tx + 16 * j]);
-        bw[j] = MOM ? static_cast<double>(Qs[NF - 1][kk][tx + 16 * j]) : 0.0;
-      }
+        for (int i = 0; i < RT; ++i) {
+          a[f][i] = *reinterpret_cast<const float4*>(&Ps[f][ty + 16 * i][kk]);
+          b[f][i] = *reinterpret_cast<const float4*>(&Qt[f][tx + 16 * i][kk]);
+        }
 #pragma unroll
-      for (int i = 0; i < RT; ++i) {
+      for (int i = 0; i < RT; ++i)
 #pragma unroll
         for (int j = 0; j < RT; ++j) {
-          acc[0][i][j] = fma(a[i], b[j], acc[0][i][j]);
+          const float4 ai = a[0][i], bj = b[0][j];
+          double s0 = acc[0][i][j];
+          s0 = fma(static_cast<double>(ai.x), static_cast<double>(bj.x), s0);
+          s0 = fma(static_cast<double>(ai.y), static_cast<double>(bj.y), s0);
+          s0 = fma(static_cast<double>(ai.z), static_cast<double>(bj.z), s0);
+          s0 = fma(static_cast<double>(ai.w), static_cast<double>(bj.w), s0);
+          acc[0][i][j] = s0;
           if (MOM) {
-            acc[NX - 2][i][j] = fma(aw[i], b[j], acc[NX - 2][i][j]);
-            acc[NX - 1][i][j] = fma(a[i], bw[j], acc[NX - 1][i][j]);
+            const float4 awi = a[NF - 1][i], bwj = b[NF - 1][j];
+            double s1 = acc[NX - 2][i][j];
+            s1 = fma(static_cast<double>(awi.x), static_cast<double>(bj.x), s1);
+            s1 = fma(static_cast<double>(awi.y), static_cast<double>(bj.y), s1);
+            s1 = fma(static_cast<double>(awi.z), static_cast<double>(bj.z), s1);
+            s1 = fma(static_cast<double>(awi.w), static_cast<double>(bj.w), s1);
+            acc[NX - 2][i][j] = s1;
+            double s2 = acc[NX - 1][i][j];
+            s2 = fma(static_cast<double>(ai.x), static_cast<double>(bwj.x), s2);
+            s2 = fma(static_cast<double>(ai.y), static_cast<double>(bwj.y), s2);
+            s2 = fma(static_cast<double>(ai.z), static_cast<double>(bwj.z), s2);
+            s2 = fma(static_cast<double>(ai.w), static_cast<double>(bwj.w), s2);
+            acc[NX - 1][i][j] = s2;
           }
         }
-      }
     }
     __syncthreads();
   }
+#pragma unroll
+  for (int x = 0; x < NX; ++x)
+#pragma unroll
+    for (int i = 0; i < RT; ++i)
+#pragma unroll
+      for (int j = 0; j < RT; ++j) acc[x][i][j] -= cg[x][i][j];
 
   if (pa.NS > 1) {
 #pragma unroll
@@ -813,9 +1240,9 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(ProductArgs pa) {
     vbad += pa.tilestat[t * 4 + 2];
   }
   const double mm = static_cast<double>(m) * m;
-  const double sum_abs = block_sum_d(v, red);
-  const double max_abs = block_max_d(vmax, red);
-  const double nbad = block_sum_d(vbad, red);
+  const double sum_abs = block_sum_d<kThreads / 64>(v, red);
+  const double max_abs = block_max_d<kThreads / 64>(vmax, red);
+  const double nbad = block_sum_d<kThreads / 64>(vbad, red);
   // mean|S| over all buckets (a non-finite bucket makes the mean non-finite)
   const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / mm;
   const double clip = 5.0 * mean_abs;
@@ -825,36 +1252,15 @@ __global__ __launch_bounds__(kThreads) void decide_kernel(ProductArgs pa) {
     const double a = fabs(pa.S[idx]);
     c2 += a < clip ? a : clip;
   }
-  const double clipped = block_sum_d(c2, red);
+  const double clipped = block_sum_d<kThreads / 64>(c2, red);
   float amax = 0.0f, bmax = 0.0f;
 #pragma unroll 8
   for (int i = threadIdx.x; i < pa.nA; i += kThreads) amax = fmaxf(amax, pa.maxpart[i]);
 #pragma unroll 8
   for (int i = threadIdx.x; i < pa.nB; i += kThreads) bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
-  const double maxA = block_max_d(static_cast<double>(amax), red);
-  const double maxB = block_max_d(static_cast<double>(bmax), red);
-  if (threadIdx.x == 0) {
-    const double sigma = 1.2533 * (clipped / mm);
-    const double tau = pa.c_valid * static_cast<double>(pa.n2) * 0x1p-23 * maxA * maxB;
-    const double lim = pa.mu * sqrt(2.0 * log(mm)) * sigma;
-    const double thr = fmin(tau, lim);
-    const bool finite = nbad == 0.0;
-    const bool clean = finite && max_abs <= thr;
-    pa.stats[0] = sigma;
-    pa.stats[1] = thr;
-    pa.stats[2] = tau;
-    pa.stats[3] = max_abs;
-    pa.stats[4] = finite ? 1.0 : 0.0;
-    pa.stats[5] = clean ? 0.0 : 1.0;
-    pa.stats[6] = maxA;
-    pa.stats[7] = maxB;
-    if (clean) {
-      pa.sigma_acc[0] += sigma;
-      pa.sigma_acc[1] += 1.0;
-    } else if (pa.d_dirty != nullptr) {
-      *pa.d_dirty = 1;
-    }
-  }
+  const double maxA = block_max_d<kThreads / 64>(static_cast<double>(amax), red);
+  const double maxB = block_max_d<kThreads / 64>(static_cast<double>(bmax), red);
+  if (threadIdx.x == 0) decide_tail(pa, sum_abs, max_abs, nbad, clipped, maxA, maxB);
 }
 
 // ----------------------------------------------------------------------------------------
@@ -1016,7 +1422,26 @@ hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int 
                  : stream_dispatch<0, false>(s, rb, g, ng, lds_bytes, st);
 }
 
-hipError_t launch_product(const ProductArgs& a, int ts, bool moments, hipStream_t st) {
+hipError_t launch_product(const ProductArgs& a0, int ts, bool moments, hipStream_t st) {
+  ProductArgs a = a0;
+  if (a.mode == 1 && !moments && a.nX > 0) {
+    switch (a.xb) {
+      case 1:
+        hipLaunchKernelGGL(block_product_kernel<1>, dim3(a.nX), dim3(kThreads), 0, st, a);
+        break;
+      case 2:
+        hipLaunchKernelGGL(block_product_kernel<2>, dim3(a.nX), dim3(kThreads), 0, st, a);
+        break;
+      case 3:
+        hipLaunchKernelGGL(block_product_kernel<3>, dim3(a.nX), dim3(kThreads), 0, st, a);
+        break;
+      default:
+        hipLaunchKernelGGL(block_product_kernel<4>, dim3(a.nX), dim3(kThreads), 0, st, a);
+        break;
+    }
+    hipLaunchKernelGGL(block_decide_kernel, dim3(1), dim3(kDecideThreads), 0, st, a);
+    return hipGetLastError();
+  }
   const dim3 grid(a.nt * a.nt, a.NS);
   const dim3 rgrid(a.nt * a.nt);
 #define FPSK_PRODUCT_CASE(TS_, MOM_)                                                       \
