@@ -274,8 +274,12 @@ void build_col_tables(const std::vector<int32_t>& h2, const std::vector<int8_t>&
   }
 }
 
+// size_order: the row lists are stored largest bucket first (list slot a holds the a-th largest
+// bucket), so that the row-bucket work-groups, dispatched in list order, start with the longest.
+// The sketch rows then come out in that order; only the probe, whose statistics do not depend
+// on the numbering of the buckets, uses it.
 void build_round(uint64_t seed, int round, int64_t n1, int64_t n3, int m, int64_t cwb, bool mom,
-                 HostRound& R) {
+                 HostRound& R, bool size_order = false) {
   R.m = m;
   R.mom = mom;
   R.h1.resize(n1);
@@ -288,11 +292,19 @@ void build_round(uint64_t seed, int round, int64_t n1, int64_t n3, int m, int64_
   std::vector<int32_t> cnt(static_cast<size_t>(m), 0);
   for (int64_t i = 0; i < n1; ++i) cnt[R.h1[i]]++;
   R.cap = std::max(1, *std::max_element(cnt.begin(), cnt.end()));
+  std::vector<int32_t> slot(static_cast<size_t>(m));
+  for (int b = 0; b < m; ++b) slot[b] = b;
+  if (size_order) {
+    std::vector<int32_t> byz(static_cast<size_t>(m));
+    for (int b = 0; b < m; ++b) byz[b] = b;
+    std::stable_sort(byz.begin(), byz.end(), [&](int32_t x, int32_t y) { return cnt[x] > cnt[y]; });
+    for (int a = 0; a < m; ++a) slot[byz[a]] = a;
+  }
   R.perm.assign(static_cast<size_t>(m) * R.cap, -1);
   std::fill(cnt.begin(), cnt.end(), 0);
   for (int64_t i = 0; i < n1; ++i) {
     const int b = R.h1[i];
-    R.perm[static_cast<size_t>(b) * R.cap + cnt[b]++] =
+    R.perm[static_cast<size_t>(slot[b]) * R.cap + cnt[b]++] =
         static_cast<int32_t>(static_cast<uint32_t>(i) | (R.v1[i] < 0 ? 0x80000000u : 0u));
   }
   build_col_tables(R.h2, R.v2, m, kColTile, 0, R.ctab, R.coff);
@@ -407,11 +419,13 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
   d.btab_stride = static_cast<int>(table_stride(m, d.cwb));
   const size_t comb = (mom ? 4096 : 2048) * sizeof(double);
   const size_t cs = (mom ? 1040 : 520) * sizeof(double);
-  const size_t bdata = (static_cast<size_t>(fpsk::kBChunkHalfs) + d.rb) * sizeof(uint16_t);
+  const size_t bdata = (static_cast<size_t>(d.cwb) * d.rb + d.rb) * sizeof(uint16_t);
   const size_t data = (std::max(comb + cs, bdata) + 15) / 16 * 16;
   d.tab_off = static_cast<int>(data);
+  // (the probe's B group fold stages the m + 1 segment starts after the column list)
   d.lds_stream = data + static_cast<size_t>(std::max(d.ctab_stride, d.btab_stride)) *
-                            sizeof(uint16_t);
+                            sizeof(uint16_t) +
+                 (static_cast<size_t>(m) + 1) * sizeof(int32_t);
   d.ldp = static_cast<int>((n2 + 3) / 4 * 4);
   // The probe's product for m <= 64 (at most a 16 x 16 grid of output blocks) and
   // n2 <= kMaxXSlices * kXSlice: block products over whole k-slices, then one deciding
@@ -644,7 +658,7 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   a.mode = mode;
   a.maxpart = s.maxpart;
   a.nA = d.nA;
-  a.nB = d.nB;
+  a.nB = s.nB;
   a.stats = as<double>(c->stats);
   a.d_dirty = d_dirty;
   a.sigma_acc = as<double>(c->sigma_acc);
@@ -672,7 +686,7 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
 fpsketch_status build_probe(fpsketch_ctx* c, int m, hipStream_t st) {
   HostRound R;
   const Decomp d = decompose(c->n1, c->n2, c->n3, m, false);
-  build_round(c->p.seed, 0, c->n1, c->n3, m, d.cwb, false, R);
+  build_round(c->p.seed, 0, c->n1, c->n3, m, d.cwb, false, R, true);
   FPSK_TRY(upload_round(R, d.cwb, c->probe_round, st));
   FPSK_TRY(ensure_workspace(c->probe_ws, c->n1, c->n2, c->n3, m, false));
   c->m = m;

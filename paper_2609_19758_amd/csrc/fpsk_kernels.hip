@@ -336,6 +336,15 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
   constexpr int SLOTS = kThreads / NG;       // bucket slots per fold group
   constexpr int PADG = (RB == 8 && G == 1) ? 8 : 1; // bucket segments padded to this multiple
   constexpr int NT = PADG == 8 ? 2 : (CW / 8 / kThreads > 0 ? CW / 8 / kThreads : 1);
+  // Group fold (probe, 8 rows, m <= 256): thread t sums the 8 columns of entry groups t and
+  // t + 256 of the chunk's sorted list (each group lies in one bucket, as segments are padded
+  // to whole groups) over all 8 rows with one 16-byte LDS read per column; thread (b, r) then
+  // adds the group partials of bucket b, row r in FP64.
+  constexpr bool GF = !MOM && PADG == 8;
+  constexpr int GFP = 8 / NG;                // (bucket, row) pairs per thread: 8 m <= 2048 / NG
+  double qacc[GF ? GFP : 1];
+#pragma unroll
+  for (int i = 0; i < (GF ? GFP : 1); ++i) qacc[i] = 0.0;
   using Chunk = BChunk<RB, G, NT>;
   constexpr int NI = Chunk::NI;
   static_assert(Chunk::NV == 8, "each thread stages 64 halfs of B per chunk");
@@ -385,12 +394,22 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
       ch.tv[it] = *tp;
     }
     const int32_t* boff = s.boff + static_cast<int64_t>(live ? c : 0) * (m + 1);
+    if constexpr (GF) {
+      // segment starts m + 1 <= 257: entries t and t + 256, staged in LDS after the list
+      const int t = threadIdx.x;
+      const int32_t* p0 = (live && t <= m) ? boff + t : static_cast<const int32_t*>(s.zero);
+      const int32_t* p1 = (live && t + kThreads <= m) ? boff + t + kThreads
+                                                      : static_cast<const int32_t*>(s.zero);
+      ch.qb[0] = *p0;
+      ch.qe[0] = *p1;
+    } else {
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const int b = bslot + SLOTS * g;
-      const int32_t* bp = (live && b < m) ? boff + b : static_cast<const int32_t*>(s.zero);
-      ch.qb[g] = bp[0];
-      ch.qe[g] = bp[1];
+      for (int g = 0; g < G; ++g) {
+        const int b = bslot + SLOTS * g;
+        const int32_t* bp = (live && b < m) ? boff + b : static_cast<const int32_t*>(s.zero);
+        ch.qb[g] = bp[0];
+        ch.qe[g] = bp[1];
+      }
     }
   };
 
@@ -418,9 +437,72 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
       const int o = (threadIdx.x + kThreads * it) * 8;
       if (o < stride) *reinterpret_cast<u32x4*>(tabL + o) = ch.tv[it];
     }
+    if constexpr (GF) {
+      int32_t* boffL = reinterpret_cast<int32_t*>(tabL + stride);
+      const int t = threadIdx.x;
+      if (t <= m) boffL[t] = ch.qb[0];
+      if (t + kThreads <= m) boffL[t + kThreads] = ch.qe[0];
+    }
     __syncthreads();
+    if constexpr (GF) {
+      const int32_t* boffL = reinterpret_cast<const int32_t*>(tabL + stride);
+      const int ngroups = boffL[m] >> 3;
+      float part[2][8];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
+      for (int h = 0; h < 2; ++h) {
+        const int grp = threadIdx.x + kThreads * h;
+        const bool gok = grp < ngroups;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) part[h][r] = 0.0f;
+        if (h == 1 && ngroups <= kThreads) break;   // uniform: no second groups
+        // a missing group reads the zero sentinel column
+        const u32x4 tw = *reinterpret_cast<const u32x4*>(tabL + 8 * (gok ? grp : 0));
+#pragma unroll
+        for (int z0 = 0; z0 < 8; z0 += 4) {
+          u32x4 cv[4];
+#pragma unroll
+          for (int z = 0; z < 4; ++z) {
+            const int zz = z0 + z;
+            const int e = gok ? static_cast<int>((tw[zz >> 1] >> (16 * (zz & 1))) & 0xffffu) : CW;
+            cv[z] = *reinterpret_cast<const u32x4*>(L + e * RB);
+          }
+#pragma unroll
+          for (int z = 0; z < 4; ++z)
+#pragma unroll
+            for (int w2 = 0; w2 < 4; ++w2) {
+              part[h][2 * w2] += lo_half<DT>(cv[z][w2]);
+              part[h][2 * w2 + 1] += hi_half<DT>(cv[z][w2]);
+            }
+        }
+      }
+      __syncthreads();
+      // group partials [group][row] over the staged data (the zero column lies beyond them)
+      float* PL = reinterpret_cast<float*>(L);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int grp = threadIdx.x + kThreads * h;
+        if (grp < ngroups) {
+          *reinterpret_cast<f32x4*>(PL + grp * 8) =
+              f32x4{part[h][0], part[h][1], part[h][2], part[h][3]};
+          *reinterpret_cast<f32x4*>(PL + grp * 8 + 4) =
+              f32x4{part[h][4], part[h][5], part[h][6], part[h][7]};
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < GFP; ++i) {
+        const int p = threadIdx.x + kThreads * i;
+        if (p < 8 * m) {
+          const int b = p >> 3, r = p & 7;
+          const int g1 = boffL[b + 1] >> 3;
+          double sum = 0.0;
+          for (int g = boffL[b] >> 3; g < g1; ++g) sum += static_cast<double>(PL[g * 8 + r]);
+          qacc[i] += sum;
+        }
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < (GF ? 0 : G); ++g) {
       if constexpr (PADG == 8) {
         // segments are whole multiples of 8 entries (sentinels read the zero slot): 8 list
         // entries with one LDS read, their 8 columns summed in FP32, then added in FP64
@@ -477,8 +559,18 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
     issue(ch, c);
     process(ch, c);
   }
+  if constexpr (GF) {
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
+    for (int i = 0; i < GFP; ++i) {
+      const int p = threadIdx.x + kThreads * i;
+      const int64_t k = k0 + (p & 7);
+      if (p < 8 * m && k < s.n2) {
+        s.Q[static_cast<int64_t>(p >> 3) * s.ldp + k] = static_cast<float>(qacc[i]);
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < (GF ? 0 : G); ++g) {
     const int b = bslot + SLOTS * g;
     if (b < m) {
 #pragma unroll
@@ -912,42 +1004,28 @@ __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArg
   __shared__ double red[5 * (kDecideThreads + 2 * kDecideThreads / 16 + 1)];
   const int m = pa.m;
   const int mm = m * m;
-  // every load of the work-group is issued before the first is used
-  double x[kMaxXSlices][NQ];
-#pragma unroll
-  for (int sl = 0; sl < kMaxXSlices; ++sl)
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
-      const int sc = sl < pa.xns ? sl : 0;
-      x[sl][q] = pa.xpart[static_cast<int64_t>(sc) * mm + (o < mm ? o : mm - 1)];
-    }
-  constexpr int NM = 4;                       // maxima per thread in the first pass
-  float am[NM], bm[NM];
-#pragma unroll
-  for (int q = 0; q < NM; ++q) {
-    const int i = static_cast<int>(threadIdx.x) + kDecideThreads * q;
-    am[q] = pa.maxpart[i < pa.nA ? i : pa.nA - 1];
-    bm[q] = pa.maxpart[pa.nA + (i < pa.nB ? i : pa.nB - 1)];
-  }
+  // the first slice's partials and the first share of the maxima are loaded together; only
+  // outputs and maxima that exist are loaded
   double v[NQ];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
-    double acc = 0.0;
-#pragma unroll
-    for (int sl = 0; sl < kMaxXSlices; ++sl) acc += sl < pa.xns ? x[sl][q] : 0.0;
-    v[q] = acc;
+    const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
+    v[q] = o < mm ? pa.xpart[o] : 0.0;
   }
-  float amax = am[0], bmax = bm[0];
+  const int t = threadIdx.x;
+  float amax = t < pa.nA ? pa.maxpart[t] : 0.0f;
+  float bmax = t < pa.nB ? pa.maxpart[pa.nA + t] : 0.0f;
+  for (int sl = 1; sl < pa.xns; ++sl) {
 #pragma unroll
-  for (int q = 1; q < NM; ++q) {
-    amax = fmaxf(amax, am[q]);
-    bmax = fmaxf(bmax, bm[q]);
+    for (int q = 0; q < NQ; ++q) {
+      const int o = t + kDecideThreads * q;
+      if (o < mm) v[q] += pa.xpart[static_cast<int64_t>(sl) * mm + o];
+    }
   }
-  for (int i = threadIdx.x + kDecideThreads * NM; i < pa.nA; i += kDecideThreads) {
+  for (int i = t + kDecideThreads; i < pa.nA; i += kDecideThreads) {
     amax = fmaxf(amax, pa.maxpart[i]);
   }
-  for (int i = threadIdx.x + kDecideThreads * NM; i < pa.nB; i += kDecideThreads) {
+  for (int i = t + kDecideThreads; i < pa.nB; i += kDecideThreads) {
     bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
   }
   double lsum = 0.0, lmax = 0.0, lbad = 0.0;
