@@ -190,15 +190,17 @@ fpsketch_status fpsketch_recheck(fpsketch_ctx* ctx, const void* A, const void* B
                                  const int64_t* coords, int32_t n, double* gamma, double* abssum,
                                  void* stream);
 
-/* Probe timing.  With timing enabled, every fpsketch_probe also records three hipEvents on its
- * stream: before the streaming kernel (A, B, C pass), between it and the product/decision
- * kernel, and after that.  No work is skipped or reordered.  Enabling resets the record.
- * Events are created on demand (so this mode allocates; leave it off in capture or serving). */
+/* Probe timing.  With timing enabled, every fpsketch_probe launches its kernels with four
+ * hipEvents that the dispatches time-stamp themselves (no extra queue packets): start and end
+ * of the streaming kernel (A, B, C pass), and start of the first product dispatch and end of
+ * the last (product and decision).  No work is skipped or reordered.  Enabling resets the
+ * record.  Events are created on demand (so this mode allocates; leave it off in capture or
+ * serving). */
 fpsketch_status fpsketch_timing(fpsketch_ctx* ctx, int32_t enable);
 
 /* Waits for the last recorded probe and returns the summed durations (ms) of the streaming
- * kernel and of the product/decision kernel over the probes recorded since timing was enabled
- * or last read, and their number; then clears the record. */
+ * kernel and of the product/decision dispatches over the probes recorded since timing was
+ * enabled or last read, and their number; then clears the record. */
 fpsketch_status fpsketch_timing_read(fpsketch_ctx* ctx, double* stream_ms, double* product_ms,
                                      int64_t* calls);
 

@@ -549,7 +549,7 @@ struct fpsketch_ctx {
       patch_val, rc_coords, rc_gamma, rc_abs, rc_c;
   fpsketch_plan_info last_plan{};
 
-  // optional per-probe event triples around the stream and product kernels
+  // optional per-probe events: start and end of the stream kernel, of the product dispatches
   bool timing = false;
   std::vector<hipEvent_t> events;
   size_t events_used = 0;
@@ -674,12 +674,11 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
     a.xns = d.xns;
     a.xpart = as<double>(W.xpart);
   }
-  if (ev) FPSK_HIP(hipEventRecord(ev[0], st));
+  // with ev: the dispatches themselves time-stamp ev[0..1] (stream kernel) and ev[2..3]
+  // (first product dispatch start to last dispatch end)
   FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.ng,
-                               d.lds_stream, st));
-  if (ev) FPSK_HIP(hipEventRecord(ev[1], st));
-  FPSK_HIP(fpsk::launch_product(a, d.ts, mom, st));
-  if (ev) FPSK_HIP(hipEventRecord(ev[2], st));
+                               d.lds_stream, st, ev ? ev[0] : nullptr, ev ? ev[1] : nullptr));
+  FPSK_HIP(fpsk::launch_product(a, d.ts, mom, st, ev ? ev[2] : nullptr, ev ? ev[3] : nullptr));
   return FPSK_OK;
 }
 
@@ -1012,13 +1011,13 @@ fpsketch_status fpsketch_probe(fpsketch_ctx* c, const void* A, const void* B, co
   const hipStream_t st = static_cast<hipStream_t>(stream);
   hipEvent_t* ev = nullptr;
   if (c->timing) {
-    while (c->events.size() < c->events_used + 3) {
+    while (c->events.size() < c->events_used + 4) {
       hipEvent_t e;
       FPSK_HIP(hipEventCreate(&e));
       c->events.push_back(e);
     }
     ev = c->events.data() + c->events_used;
-    c->events_used += 3;
+    c->events_used += 4;
   }
   return run_pass(c, c->probe_round, c->probe_ws, A, B, static_cast<const float*>(C), false, 1,
                   d_dirty, nullptr, nullptr, nullptr, st, ev);
@@ -1038,12 +1037,12 @@ fpsketch_status fpsketch_timing_read(fpsketch_ctx* c, double* stream_ms, double*
   }
   FPSK_TRY(set_device(c));
   double s1 = 0.0, s2 = 0.0;
-  const size_t n = c->events_used / 3;
-  if (n > 0) FPSK_HIP(hipEventSynchronize(c->events[3 * n - 1]));
+  const size_t n = c->events_used / 4;
+  if (n > 0) FPSK_HIP(hipEventSynchronize(c->events[4 * n - 1]));
   for (size_t k = 0; k < n; ++k) {
     float a = 0.0f, b = 0.0f;
-    FPSK_HIP(hipEventElapsedTime(&a, c->events[3 * k], c->events[3 * k + 1]));
-    FPSK_HIP(hipEventElapsedTime(&b, c->events[3 * k + 1], c->events[3 * k + 2]));
+    FPSK_HIP(hipEventElapsedTime(&a, c->events[4 * k], c->events[4 * k + 1]));
+    FPSK_HIP(hipEventElapsedTime(&b, c->events[4 * k + 2], c->events[4 * k + 3]));
     s1 += a;
     s2 += b;
   }

@@ -97,9 +97,13 @@ struct ProductArgs {
   double* xpart;
 };
 
+// e0 / e1 (may be null): events that the first / last dispatch of the call records its
+// start / end time in.
 hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g, int ng,
-                         size_t lds_bytes, hipStream_t st);
-hipError_t launch_product(const ProductArgs& a, int ts, bool moments, hipStream_t st);
+                         size_t lds_bytes, hipStream_t st, hipEvent_t e0 = nullptr,
+                         hipEvent_t e1 = nullptr);
+hipError_t launch_product(const ProductArgs& a, int ts, bool moments, hipStream_t st,
+                          hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_scan_count(const float* C, int64_t n1, int64_t n3, int32_t* counts,
                              hipStream_t st);
 hipError_t launch_scan_extract(const float* C, int64_t n3, const int32_t* rows,

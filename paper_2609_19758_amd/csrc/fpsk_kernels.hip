@@ -14,6 +14,8 @@
 //           recomputation of candidates (Sec. III-D).
 #include "fpsk_internal.h"
 
+#include <hip/hip_ext.h>
+
 namespace fpsk {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -1462,20 +1464,33 @@ __global__ __launch_bounds__(kThreads) void copy_kernel(const u32x4* src, u32x4*
 // ----------------------------------------------------------------------------------------
 // Launchers.
 
+// A launch whose dispatch packet, when e0 / e1 are given, records its own start / end time in
+// them (no extra queue packets, so the events bracket exactly the kernel).
+template <typename K, typename... Args>
+static void launch_k(K kernel, dim3 grid, dim3 block, size_t shmem, hipStream_t st, hipEvent_t e0,
+                     hipEvent_t e1, Args... args) {
+  if (e0 != nullptr || e1 != nullptr) {
+    hipExtLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(shmem), st, e0, e1, 0u,
+                          args...);
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, shmem, st, args...);
+  }
+}
+
 template <int DT, bool MOM>
 static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, int ng, size_t lds,
-                                  hipStream_t st) {
+                                  hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   const int grid = s.nA + s.nB + s.nC;
   if (grid <= 0) return hipSuccess;
   const bool vec = s.vec_a && s.vec_b && s.vec_c;
 #define FPSK_STREAM_CASE(RB_, G_, NG_)                                                        \
   if (rb == RB_ && g == G_ && ng == NG_) {                                                    \
     if (vec) {                                                                                \
-      hipLaunchKernelGGL((stream_kernel<DT, MOM, RB_, G_, NG_, true>), dim3(grid),            \
-                         dim3(kThreads), lds, st, s);                                         \
+      launch_k(stream_kernel<DT, MOM, RB_, G_, NG_, true>, dim3(grid), dim3(kThreads), lds,   \
+               st, e0, e1, s);                                                                \
     } else {                                                                                  \
-      hipLaunchKernelGGL((stream_kernel<DT, MOM, RB_, G_, NG_, false>), dim3(grid),           \
-                         dim3(kThreads), lds, st, s);                                         \
+      launch_k(stream_kernel<DT, MOM, RB_, G_, NG_, false>, dim3(grid), dim3(kThreads), lds,  \
+               st, e0, e1, s);                                                                \
     }                                                                                         \
     return hipGetLastError();                                                                 \
   }
@@ -1491,45 +1506,42 @@ static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, int ng, si
 }
 
 hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g, int ng,
-                         size_t lds_bytes, hipStream_t st) {
+                         size_t lds_bytes, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   if (dt == 1) {
-    return moments ? stream_dispatch<1, true>(s, rb, g, ng, lds_bytes, st)
-                   : stream_dispatch<1, false>(s, rb, g, ng, lds_bytes, st);
+    return moments ? stream_dispatch<1, true>(s, rb, g, ng, lds_bytes, st, e0, e1)
+                   : stream_dispatch<1, false>(s, rb, g, ng, lds_bytes, st, e0, e1);
   }
-  return moments ? stream_dispatch<0, true>(s, rb, g, ng, lds_bytes, st)
-                 : stream_dispatch<0, false>(s, rb, g, ng, lds_bytes, st);
+  return moments ? stream_dispatch<0, true>(s, rb, g, ng, lds_bytes, st, e0, e1)
+                 : stream_dispatch<0, false>(s, rb, g, ng, lds_bytes, st, e0, e1);
 }
 
-hipError_t launch_product(const ProductArgs& a0, int ts, bool moments, hipStream_t st) {
+hipError_t launch_product(const ProductArgs& a0, int ts, bool moments, hipStream_t st,
+                          hipEvent_t e0, hipEvent_t e1) {
   ProductArgs a = a0;
   if (a.mode == 1 && !moments && a.nX > 0) {
+    const dim3 g(a.nX), b(kThreads);
     switch (a.xb) {
-      case 1:
-        hipLaunchKernelGGL(block_product_kernel<1>, dim3(a.nX), dim3(kThreads), 0, st, a);
-        break;
-      case 2:
-        hipLaunchKernelGGL(block_product_kernel<2>, dim3(a.nX), dim3(kThreads), 0, st, a);
-        break;
-      case 3:
-        hipLaunchKernelGGL(block_product_kernel<3>, dim3(a.nX), dim3(kThreads), 0, st, a);
-        break;
-      default:
-        hipLaunchKernelGGL(block_product_kernel<4>, dim3(a.nX), dim3(kThreads), 0, st, a);
-        break;
+      case 1: launch_k(block_product_kernel<1>, g, b, 0, st, e0, nullptr, a); break;
+      case 2: launch_k(block_product_kernel<2>, g, b, 0, st, e0, nullptr, a); break;
+      case 3: launch_k(block_product_kernel<3>, g, b, 0, st, e0, nullptr, a); break;
+      default: launch_k(block_product_kernel<4>, g, b, 0, st, e0, nullptr, a); break;
     }
-    hipLaunchKernelGGL(block_decide_kernel, dim3(1), dim3(kDecideThreads), 0, st, a);
+    launch_k(block_decide_kernel, dim3(1), dim3(kDecideThreads), 0, st, nullptr, e1, a);
     return hipGetLastError();
   }
   const dim3 grid(a.nt * a.nt, a.NS);
   const dim3 rgrid(a.nt * a.nt);
-#define FPSK_PRODUCT_CASE(TS_, MOM_)                                                       \
-  if (ts == TS_ && moments == MOM_) {                                                      \
-    hipLaunchKernelGGL((product_kernel<TS_, MOM_>), grid, dim3(kThreads), 0, st, a);       \
-    if (a.NS > 1) {                                                                        \
-      hipLaunchKernelGGL((reduce_kernel<TS_, MOM_>), rgrid, dim3(kThreads), 0, st, a);     \
-    }                                                                                      \
-    if (a.mode == 1) hipLaunchKernelGGL(decide_kernel, dim3(1), dim3(kThreads), 0, st, a); \
-    return hipGetLastError();                                                              \
+  const bool red = a.NS > 1, dec = a.mode == 1;
+#define FPSK_PRODUCT_CASE(TS_, MOM_)                                                        \
+  if (ts == TS_ && moments == MOM_) {                                                       \
+    launch_k(product_kernel<TS_, MOM_>, grid, dim3(kThreads), 0, st, e0,                    \
+             (red || dec) ? nullptr : e1, a);                                               \
+    if (red) {                                                                              \
+      launch_k(reduce_kernel<TS_, MOM_>, rgrid, dim3(kThreads), 0, st, nullptr,             \
+               dec ? nullptr : e1, a);                                                      \
+    }                                                                                       \
+    if (dec) launch_k(decide_kernel, dim3(1), dim3(kThreads), 0, st, nullptr, e1, a);       \
+    return hipGetLastError();                                                               \
   }
   FPSK_PRODUCT_CASE(16, false)
   FPSK_PRODUCT_CASE(16, true)
