@@ -133,6 +133,68 @@ def summarize_db(db_path: str) -> int:
     return 0
 
 
+def _counter_means(db_path: str, counter: str) -> dict:
+    import sqlite3
+    import statistics
+    con = sqlite3.connect(db_path)
+    per = {}
+    for n, cn, d, v in con.execute("select kernel_name, counter_name, dispatch_id, value "
+                                   "from counters_collection"):
+        if cn == counter:
+            per.setdefault(n, {}).setdefault(d, 0.0)
+            per[n][d] += v
+    return {n: (statistics.mean(dv.values()), len(dv)) for n, dv in per.items()}
+
+
+def write_pmc_summary(workload: str, fetch_db: str, write_db: str) -> int:
+    """HBM bytes per launch of the probe's stream kernel: FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch) scaled by what they read for the plain copy kernel of known size."""
+    from paper_2609_19758_amd import workloads as wl
+    w = wl.workload(workload)
+    fetch, write = _counter_means(fetch_db, "FETCH_SIZE"), _counter_means(write_db, "WRITE_SIZE")
+    stream = [n for n in fetch if "stream_kernel<" in n and ", false," in n]
+    copy = [n for n in fetch if "copy_kernel" in n]
+    if len(stream) != 1 or len(copy) != 1:
+        print(f"expected one probe stream kernel and one copy kernel, got {stream} {copy}",
+              file=sys.stderr)
+        return 1
+    sk, ck = stream[0], copy[0]
+    copy_kib = 256 * 1024                  # --copy-calibration 256: 256 MiB read and written
+    fs, ws = copy_kib / fetch[ck][0], copy_kib / write[ck][0]
+    traffic = (fetch[sk][0] * fs + write[sk][0] * ws) * 1024.0
+    lines = [
+        f"# HBM traffic of the FP-Sketch probe's stream kernel, {workload}",
+        "# commands (from /tmp, repo at $R), one counter per run:",
+        "#   rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/fetch -o run -- python3 $R/bench.py "
+        "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --copy-calibration 256",
+        "#   rocprofv3 --pmc WRITE_SIZE -d $R/gpurun_out/write -o run -- python3 $R/bench.py "
+        "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --copy-calibration 256",
+        "#   python3 bench.py --write-pmc-summary gpurun_out/fetch/run_results.db "
+        "gpurun_out/write/run_results.db",
+        "# scale: the copy kernel moves 262144 KiB in and 262144 KiB out per dispatch",
+        f"workload={workload}",
+        f"kernel={sk}",
+        f"kernel_source_sha256_16={kernel_source_hash()}",
+        f"stream_dispatches={fetch[sk][1]}",
+        f"fetch_size_kib_per_dispatch={fetch[sk][0]:.1f}",
+        f"write_size_kib_per_dispatch={write[sk][0]:.1f}",
+        f"copy_fetch_kib_per_dispatch={fetch[ck][0]:.1f}",
+        f"copy_write_kib_per_dispatch={write[ck][0]:.1f}",
+        f"fetch_scale={fs:.4f}",
+        f"write_scale={ws:.4f}",
+        f"read_bytes_per_launch={fetch[sk][0] * fs * 1024.0:.0f}",
+        f"written_bytes_per_launch={write[sk][0] * ws * 1024.0:.0f}",
+        f"traffic_bytes_per_launch={traffic:.0f}",
+        f"algorithmic_bytes_per_launch={w.bytes_abc}",
+        f"traffic_over_algorithmic={traffic / w.bytes_abc:.4f}",
+    ]
+    os.makedirs(os.path.dirname(PMC_SUMMARY), exist_ok=True)
+    with open(PMC_SUMMARY, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -146,9 +208,15 @@ def main() -> int:
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run the library's plain copy kernel over MIB MiB (counter scale)")
     ap.add_argument("--summarize", metavar="DB", help="summarize a rocprofv3 database and exit")
+    ap.add_argument("--write-pmc-summary", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
+                    help="write the HBM traffic summary of the probe's stream kernel from two "
+                         "rocprofv3 --pmc databases (FETCH_SIZE, WRITE_SIZE) of a run with "
+                         "--copy-calibration, and exit")
     args = ap.parse_args()
     if args.summarize:
         return summarize_db(args.summarize)
+    if args.write_pmc_summary:
+        return write_pmc_summary(args.workload, *args.write_pmc_summary)
     if args.gpus != 1:
         print(f"bench.py: this verifier runs on one GPU; --gpus {args.gpus} is not supported "
               "(no sharded path is built)", file=sys.stderr)
