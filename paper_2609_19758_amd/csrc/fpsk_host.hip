@@ -130,9 +130,17 @@ int64_t m_mem(int64_t n2) {
 
 bool positive_finite(double x) { return std::isfinite(x) && x > 0.0; }
 
-int32_t radius_rule(double B) {
+// ceil(x) for x >= 0 as an integer, saturated at hi (x may be huge or +inf: a probe estimate
+// taken on a C with out-of-range entries can be of the order of those entries).
+int64_t ceil_sat(double x, int64_t hi) {
+  const double c = std::ceil(x);
+  return c < static_cast<double>(hi) ? static_cast<int64_t>(c) : hi;
+}
+
+// r_B of Sec. III-G, saturated far above any radius the plan can use.
+int64_t radius_rule(double B) {
   if (B <= 0.05) return 0;
-  return std::max(2, static_cast<int32_t>(std::ceil(2.5 * B)));
+  return std::max<int64_t>(2, ceil_sat(2.5 * B, int64_t{1} << 40));
 }
 
 struct PlanOut {
@@ -147,20 +155,22 @@ PlanOut plan_localize(int64_t n1, int64_t n2, int64_t n3, fpsketch_dtype dt, int
   o.fallback = !(positive_finite(sigma) && positive_finite(rms));
   o.B = o.fallback ? mx * law_sigma_over_rms(n1, n2, n3, m, dt) / p.rho_min
                    : mx * sigma / (p.rho_min * rms);
-  const int32_t rb = radius_rule(o.B);
+  const int64_t rb = radius_rule(o.B);
   if (rb <= p.r_star) {
     o.m_loc = m;
-    o.r = rb;
+    o.r = static_cast<int32_t>(rb);
     return o;
   }
-  const int64_t need = static_cast<int64_t>(
-      std::ceil(static_cast<double>(m) * static_cast<double>(rb) / static_cast<double>(p.r_star)));
+  const int64_t cap = std::min(m_max(n1, n3), m_mem(n2));
+  const int64_t need = ceil_sat(static_cast<double>(m) * static_cast<double>(rb) /
+                                    static_cast<double>(p.r_star), cap + 16);
   const int64_t grown = 16 * ((need + 15) / 16);
-  const int64_t mloc = std::max<int64_t>(m, std::min({grown, m_max(n1, n3), m_mem(n2)}));
+  const int64_t mloc = std::max<int64_t>(m, std::min(grown, cap));
   o.m_loc = static_cast<int32_t>(mloc);
   const double b2 = o.B * static_cast<double>(m) / static_cast<double>(mloc);
   o.r = b2 <= 0.05 ? 0
-                   : std::min(p.r_max, std::max(2, static_cast<int32_t>(std::ceil(2.5 * b2))));
+                   : static_cast<int32_t>(std::min<int64_t>(
+                         p.r_max, std::max<int64_t>(2, ceil_sat(2.5 * b2, p.r_max))));
   return o;
 }
 
@@ -170,7 +180,7 @@ void recalibrate(int64_t n1, int64_t n3, int32_t m, double sigma_bar, double rms
   *rebuild = 0;
   if (!(positive_finite(sigma_bar) && positive_finite(rms))) return;
   const double b1 = static_cast<double>(std::max(n1, n3)) * sigma_bar / rms;
-  const int64_t want = static_cast<int64_t>(std::ceil(static_cast<double>(m) * b1 / p.b_star));
+  const int64_t want = ceil_sat(static_cast<double>(m) * b1 / p.b_star, m_max(n1, n3));
   const int64_t mp = std::max<int64_t>({m_comb(p), 16, std::min(want, m_max(n1, n3))});
   if (static_cast<double>(mp) < m / 1.25 || static_cast<double>(mp) > 1.25 * m) {
     *m_new = static_cast<int32_t>(mp);

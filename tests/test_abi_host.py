@@ -85,6 +85,20 @@ def test_plan_matches_oracle():
         assert got[:2] == (ref.m_loc, ref.r) and got[3] and ref.fallback
 
 
+def test_plan_with_huge_noise_estimate_matches_oracle():
+    """A probe estimate taken on a C that holds entries near fp32max is itself of that order;
+    the radius rule then asks for far more than any integer radius, and the plan must saturate
+    at the largest m_loc and r_max (Sec. III-G), as the oracle's unbounded integers do."""
+    for sigma in (1e9, 1e20, 1e35, 1e300):
+        for (n1, n2, n3) in ((4096, 11008, 4096), (16384, 16384, 16384), (2048, 4096, 4096)):
+            ref = o.plan_localize(n1, n2, n3, "bf16", 48, sigma, 2.0, P)
+            got = fk.plan_host(n1, n2, n3, "bf16", 48, sigma, 2.0)
+            assert got[:2] == (ref.m_loc, ref.r), (sigma, n1, n2, n3, got, ref)
+            assert ref.r == P.r_max and ref.m_loc == min(o.m_max(n1, n3), o.m_mem(n2))
+    ref = o.recalibrate_m(4096, 4096, 48, 1e300, 2.0, P)
+    assert fk.recalibrate_host(4096, 4096, 48, 1e300, 2.0) == (ref[0], ref[1])
+
+
 def test_recalibration_matches_oracle():
     rng = np.random.Generator(np.random.PCG64(3))
     for _ in range(500):
