@@ -81,11 +81,14 @@ def gen_operands(n1: int, n2: int, n3: int, fmt: str, dist_a, dist_b, seed: int,
     ``seed`` drives A; B uses ``seed_b`` (defaults to ``seed``), so a fixed weight matrix can be
     paired with rotating activations.
     """
-    rng_a = np.random.Generator(np.random.PCG64([int(seed), 0xA]))
-    rng_b = np.random.Generator(np.random.PCG64([int(seed if seed_b is None else seed_b), 0xB]))
-    a = round_to_half(_draw(rng_a, (n1, n2), dist_a), fmt)
-    b = round_to_half(_draw(rng_b, (n2, n3), dist_b), fmt)
-    return a, b
+    return (gen_side(n1, n2, fmt, dist_a, seed, 0xA),
+            gen_side(n2, n3, fmt, dist_b, seed if seed_b is None else seed_b, 0xB))
+
+
+def gen_side(rows: int, cols: int, fmt: str, dist, seed: int, side: int) -> np.ndarray:
+    """One operand of ``gen_operands`` (side 0xA for A, 0xB for B) as uint16 half bits."""
+    rng = np.random.Generator(np.random.PCG64([int(seed), int(side)]))
+    return round_to_half(_draw(rng, (rows, cols), dist), fmt)
 
 
 def cpu_gemm_f32(a_bits: np.ndarray, b_bits: np.ndarray, fmt: str) -> np.ndarray:
@@ -165,6 +168,39 @@ def bitflip_plan(count: int, seed: int) -> list[int]:
     bits 23..30, one flipped bit per fault."""
     rng = np.random.Generator(np.random.PCG64([int(seed), 0xE]))
     return [int(b) for b in rng.integers(13, 31, size=count)]
+
+
+def call_faults(w: "Workload", n1: int, n3: int, unit: float, seed: int):
+    """Faults of one dirty call of workload ``w``: (sites, deltas, masks).
+
+    ``w.faults`` distinct sites (for "mixed" workloads a seeded count in 0..faults); additive and
+    mixed workloads carry signed deltas of U(lo, hi)·unit (log-uniform when ``w.log_uniform``),
+    bit-flip workloads one mask per site from ``bitflip_plan``.  The unused one of deltas /
+    masks is None."""
+    count = w.faults
+    if w.fault_kind == "mixed":
+        rng = np.random.Generator(np.random.PCG64([int(seed), 0xC]))
+        count = int(rng.integers(0, w.faults + 1))
+    sites = fault_sites(n1, n3, count, seed)
+    if w.fault_kind == "bitflip":
+        return sites, None, [1 << b for b in bitflip_plan(count, seed + 1)]
+    deltas = fault_magnitudes(count, w.fault_lo, w.fault_hi, unit, seed + 1,
+                              log_uniform=w.log_uniform)
+    return sites, deltas, None
+
+
+def apply_faults(values: np.ndarray, deltas, masks) -> np.ndarray:
+    """FP32 values at the fault sites after the faults are written (values in site order):
+    fl32(value + delta), or the bit pattern XOR mask."""
+    v = np.array(values, dtype=np.float32, copy=True).ravel()
+    if masks is not None:
+        u = v.view(np.uint32)
+        for t, mk in enumerate(masks):
+            u[t] ^= np.uint32(mk)
+        return v
+    for t, d in enumerate(deltas):
+        v[t] = np.float32(np.float64(v[t]) + float(d))
+    return v
 
 
 # ---------------------------------------------------------------------------------------------
