@@ -240,9 +240,11 @@ int64_t table_stride(int m, int64_t W) {
   return (s + 7) / 8 * 8;
 }
 
-// Staged LDS slot of column offset cc in a B chunk of W columns (W: the zero sentinel slot);
-// groups of 8 columns are XOR-swizzled so that neighbouring groups start on different banks.
-int64_t b_slot(int64_t cc, int64_t W) { return cc < W ? (cc ^ ((cc >> 3) & 7)) : W; }
+// Staged LDS slot of column offset cc in a B chunk of W columns (W: the zero sentinel slot):
+// column-block major, slot (cc mod 8) (W / 8) + cc / 8, so the thread that loads columns
+// 8g .. 8g + 7 stores them at one base address plus constant offsets, and the 64 lanes of a wave
+// store to consecutive slots.
+int64_t b_slot(int64_t cc, int64_t W) { return cc < W ? (cc & 7) * (W / 8) + (cc >> 3) : W; }
 
 // Column tiles of width W sorted by bucket (stable in column order); segment starts per tile,
 // segments padded with the sentinel W.  Entry format: 0 = offset | (v2 < 0) << 15 (C tiles),

@@ -262,13 +262,15 @@ __device__ __forceinline__ uint32_t pick_half(uint32_t wa, uint32_t wb, int odd)
   return odd ? ((wa >> 16) | (wb & 0xffff0000u)) : ((wa & 0xffffu) | (wb << 16));
 }
 
-// Write the 8 columns held by one thread (RB rows x 8 columns) column-major into LDS.  Column e
-// of the group goes to slot e ^ sw: neighbouring groups start on different banks.
+// Write the 8 columns held by one thread (RB rows x 8 columns) column-major into LDS.  Column
+// 8 g8 + e goes to slot e (W / 8) + g8 of a chunk of W = kBChunkHalfs / RB columns: one base
+// address (dst = slot g8) plus the constant offset e * kBChunkHalfs / 8 halfs per column, and
+// the lanes of a wave write consecutive slots.
 template <int RB>
-__device__ __forceinline__ void store_cols(uint16_t* dst, const u32x4* v, int sw) {
+__device__ __forceinline__ void store_cols(uint16_t* dst, const u32x4* v) {
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    uint16_t* d = dst + (e ^ sw) * RB;
+    uint16_t* d = dst + e * (kBChunkHalfs / 8);
     if constexpr (RB == 1) {
       d[0] = static_cast<uint16_t>(v[0][e >> 1] >> (16 * (e & 1)));
     } else if constexpr (RB == 2) {
@@ -290,7 +292,7 @@ __device__ __forceinline__ void store_cols(uint16_t* dst, const u32x4* v, int sw
 // Staged slot of column cc of a chunk of CW columns (CW itself is the zero sentinel slot).
 template <int CW>
 __device__ __forceinline__ int col_slot(int cc) {
-  return cc < CW ? (cc ^ ((cc >> 3) & 7)) : CW;
+  return cc < CW ? (cc & 7) * (CW / 8) + (cc >> 3) : CW;
 }
 
 // RBG consecutive halfs of one staged column.
@@ -432,7 +434,7 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
         for (int h = 0; h < 4; ++h) mx = absmax2(mx, ch.v[it * RB + r][h]);
         ch.v[it * RB + r] ^= smask;
       }
-      store_cols<RB>(L + static_cast<int64_t>(g8) * 8 * RB, ch.v + it * RB, g8 & 7);
+      store_cols<RB>(L + static_cast<int64_t>(g8) * RB, ch.v + it * RB);
     }
 #pragma unroll
     for (int it = 0; it < NT; ++it) {
@@ -450,6 +452,10 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
       const int32_t* boffL = reinterpret_cast<const int32_t*>(tabL + stride);
       const int ngroups = boffL[m] >> 3;
       float part[2][8];
+      // FP16: x * one + part converts and adds in one instruction (v_fma_mix_f32) without a
+      // temporary; `one` is opaque so the multiply by 1 is not folded away (exact either way)
+      float one = 1.0f;
+      asm volatile("" : "+v"(one));
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int grp = threadIdx.x + kThreads * h;
@@ -472,8 +478,14 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
           for (int z = 0; z < 4; ++z)
 #pragma unroll
             for (int w2 = 0; w2 < 4; ++w2) {
-              part[h][2 * w2] += lo_half<DT>(cv[z][w2]);
-              part[h][2 * w2 + 1] += hi_half<DT>(cv[z][w2]);
+              if constexpr (DT == 0) {
+                part[h][2 * w2] = __builtin_fmaf(lo_half<DT>(cv[z][w2]), one, part[h][2 * w2]);
+                part[h][2 * w2 + 1] =
+                    __builtin_fmaf(hi_half<DT>(cv[z][w2]), one, part[h][2 * w2 + 1]);
+              } else {
+                part[h][2 * w2] += lo_half<DT>(cv[z][w2]);
+                part[h][2 * w2 + 1] += hi_half<DT>(cv[z][w2]);
+              }
             }
         }
       }
