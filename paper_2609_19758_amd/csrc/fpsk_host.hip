@@ -376,11 +376,14 @@ struct Decomp {
   int rb = 8, g = 1, ng = 1, cwb = 2048, TB = 0, nB = 0;
   int TC = 0, npc = 1, tg = 1, nC = 0;
   int ctab_stride = 0, btab_stride = 0, tab_off = 0;
-  int ts = 16, nt = 1, NS = 1, ksl = 0;
+  int ts = 32, nt = 1, NS = 1, ksl = 0;
+  bool kw = false;             // product tiles whose k-range the 4 waves split
   size_t lds_stream = 0;
-  int ldp = 0;                 // row length of the factors: n2 rounded up to a multiple of 4
+  int kact = 0;                // k-range of the factors: n2 rounded up to a multiple of 4
+  int ldp = 0;                 // row stride of the factors (kact padded; see decompose)
   // probe block product (nX > 0): work-groups of xb x xb outputs over xns k-slices
   int xb = 0, xnb = 0, xns = 0, nX = 0;
+  int xsr = 1, xsc = 1, xnstc = 1, xslots = 0;   // supertiles of blocks (XCD-local sets)
 };
 
 Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
@@ -413,16 +416,27 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
   d.tg = (d.TC + npc - 1) / npc;
   d.npc = (d.TC + d.tg - 1) / d.tg;
   d.nC = m * d.npc;
-  d.ts = m <= 128 ? 16 : (m <= 512 ? 32 : 64);
+  // Bucket-space product on the matrix cores, tiles of ts x ts outputs over NS k-slices.
+  // Without moments: 16 x 16 tiles whose k-range the 4 waves split, while there are fewer than
+  // 256 of them (slices for about 2048 waves); else 64 x 64 tiles of four 32 x 32 wave quadrants.
+  // With moments: four 16 x 16 quadrants (32 x 32 tiles) up to m = 128, then 64 x 64.  Without
+  // the split, slices for about 1024 work-groups.  A wave takes k in steps of 16; at most 32
+  // slices.
+  if (!mom) {
+    const int t16 = (m + 15) / 16;
+    d.kw = t16 * t16 < 256;
+    d.ts = d.kw ? 16 : 64;
+  } else {
+    d.kw = false;
+    d.ts = m <= 128 ? 32 : 64;
+  }
   d.nt = (m + d.ts - 1) / d.ts;
   const int tiles = d.nt * d.nt;
-  // k per staged chunk of the product kernel (16 KiB of FP32 per factor); a slice is a whole
-  // number of chunks, and about 256 (tile, slice) work-groups are formed
-  const int kch = (mom ? 2048 : 4096) / d.ts;
-  int ns = (256 + tiles - 1) / tiles;
-  ns = std::max(1, std::min<int>(ns, static_cast<int>(std::max<int64_t>(1, n2 / kch))));
+  const int kstep = d.kw ? 64 : 16;
+  int ns = ((d.kw ? 512 : 1024) + tiles - 1) / tiles;
+  ns = std::max(1, std::min<int>({ns, 32, static_cast<int>((n2 + kstep - 1) / kstep)}));
   int64_t ksl = (n2 + ns - 1) / ns;
-  ksl = (ksl + kch - 1) / kch * kch;
+  ksl = (ksl + kstep - 1) / kstep * kstep;
   d.ksl = static_cast<int>(ksl);
   d.NS = static_cast<int>((n2 + ksl - 1) / ksl);
   // dynamic LDS of the stream kernel: a data area (A/C combine and column sums, or the staged
@@ -438,16 +452,29 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
   d.lds_stream = data + static_cast<size_t>(std::max(d.ctab_stride, d.btab_stride)) *
                             sizeof(uint16_t) +
                  (static_cast<size_t>(m) + 1) * sizeof(int32_t);
-  d.ldp = static_cast<int>((n2 + 3) / 4 * 4);
+  d.kact = static_cast<int>((n2 + 3) / 4 * 4);
+  // Factor rows sit 64 floats past a multiple of 1024 apart (an odd multiple of 256 bytes), so
+  // that the 16 rows one matrix-core load instruction touches at the same k fall on 16
+  // different L2 channels rather than one.
+  d.ldp = static_cast<int>((n2 + 1023) / 1024 * 1024 + 64);
   // The probe's product for m <= 64 (at most a 16 x 16 grid of output blocks) and
   // n2 <= kMaxXSlices * kXSlice: block products over whole k-slices, then one deciding
   // work-group.
-  const int xns = static_cast<int>((d.ldp + fpsk::kXSlice - 1) / fpsk::kXSlice);
+  const int xns = static_cast<int>((d.kact + fpsk::kXSlice - 1) / fpsk::kXSlice);
   if (!mom && m <= 64 && xns <= fpsk::kMaxXSlices) {
     d.xb = (m + 15) / 16;
     d.xnb = (m + d.xb - 1) / d.xb;
     d.xns = xns;
-    d.nX = d.xnb * d.xnb * d.xns;
+    // The 8 XCDs take launch indices round-robin, and the kernel maps index i to slot
+    // (i mod 8) nX / 8 + i / 8: each XCD runs a contiguous range of slots.  Slots run over
+    // supertiles of xsr x xsc output blocks within a slice, so one XCD's blocks form a compact
+    // rectangle that shares factor rows in that XCD's L2.
+    d.xsc = std::min(8, d.xnb);
+    const int per = (d.xnb * d.xnb + 7) / 8;
+    d.xsr = std::max(1, std::min(d.xnb, (per + d.xsc - 1) / d.xsc));
+    d.xnstc = (d.xnb + d.xsc - 1) / d.xsc;
+    d.xslots = ((d.xnb + d.xsr - 1) / d.xsr) * d.xsr * d.xnstc * d.xsc;
+    d.nX = (d.xns * d.xslots + 7) / 8 * 8;
   }
   return d;
 }
@@ -663,6 +690,7 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   a.m = d.m;
   a.n2 = static_cast<int>(c->n2);
   a.ldp = d.ldp;
+  a.kact = d.kact;
   a.nt = d.nt;
   a.NS = d.NS;
   a.ksl = d.ksl;
@@ -684,13 +712,18 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
     a.xb = d.xb;
     a.xnb = d.xnb;
     a.xns = d.xns;
+    a.xsr = d.xsr;
+    a.xsc = d.xsc;
+    a.xnstc = d.xnstc;
+    a.xslots = d.xslots;
     a.xpart = as<double>(W.xpart);
   }
   // with ev: the dispatches themselves time-stamp ev[0..1] (stream kernel) and ev[2..3]
   // (first product dispatch start to last dispatch end)
   FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.ng,
                                d.lds_stream, st, ev ? ev[0] : nullptr, ev ? ev[1] : nullptr));
-  FPSK_HIP(fpsk::launch_product(a, d.ts, mom, st, ev ? ev[2] : nullptr, ev ? ev[3] : nullptr));
+  FPSK_HIP(fpsk::launch_product(a, d.ts, d.kw, mom, st, ev ? ev[2] : nullptr,
+                                ev ? ev[3] : nullptr));
   return FPSK_OK;
 }
 

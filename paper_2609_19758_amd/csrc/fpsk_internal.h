@@ -43,7 +43,7 @@ struct StreamArgs {
   int ctab_stride, btab_stride;
   int tab_off;                // byte offset of the staged column list in dynamic LDS
   // outputs
-  // factors, row length ldp (n2 rounded up to a multiple of 4, the padding kept at zero)
+  // factors, row stride ldp >= n2 (a multiple of 4; entries past n2 are kept at zero)
   float* P;        // m x ldp      H1 A
   float* Pw;       // m x ldp      H1 W1 A            (moments only)
   float* Q;        // m x ldp      (B H2^T)^T: row b holds column b of B H2^T
@@ -79,10 +79,11 @@ struct ProductArgs {
   double* S;
   double* R;
   double* T;
-  double* scratch;      // NS x tiles x ts^2 (x 3 with moments) slice partials
+  double* scratch;      // NS x tiles x ts^2 (x 3 with moments) slice partials, row-major tiles
   double* tilestat;     // tiles x 4: sum|S|, max|S|, non-finite count
   int m, n2, nt, NS, ksl, npc;
-  int ldp;              // row length of the factors
+  int ldp;              // row stride of the factors
+  int kact;             // k-range the products cover: n2 rounded up to a multiple of 4
   int mode;             // 0: sketch only; 1: probe decision
   const float* maxpart;
   int nA, nB;
@@ -94,6 +95,9 @@ struct ProductArgs {
   // probe with m <= 64 (nX > 0): nX = xnb^2 xns block-product work-groups of xb x xb outputs
   // over k-slices of kXSlice, their partials in xpart (xns x m x m, slice 0 minus the C grid)
   int nX, xb, xnb, xns;
+  // launch index i -> slot (i mod 8) nX / 8 + i / 8; xslots slots per slice, in supertiles of
+  // xsr x xsc blocks, xnstc supertiles per row of blocks (slots past the grid are idle)
+  int xsr, xsc, xnstc, xslots;
   double* xpart;
 };
 
@@ -102,7 +106,8 @@ struct ProductArgs {
 hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g, int ng,
                          size_t lds_bytes, hipStream_t st, hipEvent_t e0 = nullptr,
                          hipEvent_t e1 = nullptr);
-hipError_t launch_product(const ProductArgs& a, int ts, bool moments, hipStream_t st,
+// ts, kw: product tile edge and whether its k-range is split over the 4 waves
+hipError_t launch_product(const ProductArgs& a, int ts, bool kw, bool moments, hipStream_t st,
                           hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_scan_count(const float* C, int64_t n1, int64_t n3, int32_t* counts,
                              hipStream_t st);

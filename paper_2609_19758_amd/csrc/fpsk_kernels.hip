@@ -770,33 +770,6 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
 // ----------------------------------------------------------------------------------------
 // Reductions and the probe decision shared by the fused and separate product paths.
 
-// Block reductions: fixed butterfly within each wave, then the wave results in order.
-template <int NW>
-__device__ double block_sum_d(double v, double* red) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  double r = 0.0;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) r += red[w];
-  __syncthreads();
-  return r;
-}
-
-template <int NW>
-__device__ double block_max_d(double v, double* red) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  double r = red[0];
-#pragma unroll
-  for (int w = 1; w < NW; ++w) r = fmax(r, red[w]);
-  __syncthreads();
-  return r;
-}
-
 // Fixed-order work-group reduction of NV values per thread through LDS (cross-lane shuffles
 // of doubles cost tens of cycles each).  Levels of 16: at a level over N entries, thread
 // g < N / 16 of value i combines entries g, g + N / 16, ..., g + 15 N / 16 (consecutive threads
@@ -861,7 +834,7 @@ __device__ void lds_reduce(double (&v)[NV], double* buf, uint32_t max_mask) {
 // The probe's decision from the reduced statistics (Sec. III-B): clipped-mean noise estimate,
 // validity bound from max|A| and max|B|, threshold and verdict.
 __device__ void decide_tail(const ProductArgs& pa, double sum_abs, double max_abs, double nbad,
-                            double clipped, double maxA, double maxB) {
+                            double clipped, double maxA, double maxB, double acc0, double acc1) {
   const double mm = static_cast<double>(pa.m) * pa.m;
   const double sigma = 1.2533 * (clipped / mm);
   const double tau = pa.c_valid * static_cast<double>(pa.n2) * 0x1p-23 * maxA * maxB;
@@ -879,8 +852,8 @@ __device__ void decide_tail(const ProductArgs& pa, double sum_abs, double max_ab
   pa.stats[6] = maxA;
   pa.stats[7] = maxB;
   if (clean) {
-    pa.sigma_acc[0] += sigma;
-    pa.sigma_acc[1] += 1.0;
+    pa.sigma_acc[0] = acc0 + sigma;
+    pa.sigma_acc[1] = acc1 + 1.0;
   } else if (pa.d_dirty != nullptr) {
     *pa.d_dirty = 1;
   }
@@ -926,10 +899,16 @@ __global__ __launch_bounds__(kThreads) void block_product_kernel(ProductArgs pa)
   __shared__ double red[NV * (kThreads + 2 * kThreads / 16 + 1)];
   const int m = pa.m;
   const int64_t mm = static_cast<int64_t>(m) * m;
-  const int x = blockIdx.x;
-  const int nb2 = pa.xnb * pa.xnb;
-  const int slice = x / nb2, blk = x - slice * nb2;
-  const int rbk = blk / pa.xnb, cbk = blk - rbk * pa.xnb;
+  // XCD-local slot of this launch index, then its slice and output block
+  const int per = gridDim.x / 8;
+  const int slot = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+  const int slice = slot / pa.xslots;
+  if (slice >= pa.xns) return;
+  const int q = slot - slice * pa.xslots;
+  const int st = q / (pa.xsr * pa.xsc), within = q - st * (pa.xsr * pa.xsc);
+  const int rbk = (st / pa.xnstc) * pa.xsr + within / pa.xsc;
+  const int cbk = (st % pa.xnstc) * pa.xsc + within % pa.xsc;
+  if (rbk >= pa.xnb || cbk >= pa.xnb) return;
   const int a0 = rbk * XB, b0 = cbk * XB;
   // uniform row bases (rows past m repeat row m - 1; their results are dropped)
   const float* prow[XB];
@@ -959,7 +938,7 @@ __global__ __launch_bounds__(kThreads) void block_product_kernel(ProductArgs pa)
 #pragma unroll
   for (int j = 0; j < JH; ++j) {
     const int k = kb + 4 * (static_cast<int>(threadIdx.x) + kThreads * (h * JH + j));
-    const bool kok = k < pa.ldp;
+    const bool kok = k < pa.kact;
     const int kk = kok ? k : 0;
 #pragma unroll
     for (int i = 0; i < XB; ++i) {
@@ -1027,6 +1006,12 @@ __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArg
     v[q] = o < mm ? pa.xpart[o] : 0.0;
   }
   const int t = threadIdx.x;
+  // the running noise sum, read now so that the verdict does not wait on it
+  double acc0 = 0.0, acc1 = 0.0;
+  if (t == 0) {
+    acc0 = pa.sigma_acc[0];
+    acc1 = pa.sigma_acc[1];
+  }
   float amax = t < pa.nA ? pa.maxpart[t] : 0.0f;
   float bmax = t < pa.nB ? pa.maxpart[pa.nA + t] : 0.0f;
   for (int sl = 1; sl < pa.xns; ++sl) {
@@ -1073,7 +1058,7 @@ __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArg
   }
   double r1[1] = {c2};
   lds_reduce<kDecideThreads, 1>(r1, red, 0u);
-  if (threadIdx.x == 0) decide_tail(pa, sum_abs, max_abs, nbad, r1[0], r5[3], r5[4]);
+  if (threadIdx.x == 0) decide_tail(pa, sum_abs, max_abs, nbad, r1[0], r5[3], r5[4], acc0, acc1);
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
@@ -1084,12 +1069,12 @@ __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArg
 // ----------------------------------------------------------------------------------------
 // Product and decision, ordered by kernel boundaries only (no cross-work-group
 // synchronization inside a kernel):
-//   product_kernel  (tile, slice): partial P Q over one k-slab, FP64 accumulation of the FP32
-//                   factors; slice 0 also subtracts the C grid (the sum of its column-group
-//                   partials).  With a single slice it finishes the tile.
+//   mfma_product_kernel (tile, slice): partial P Q over one k-slab on the FP64 matrix cores;
+//                   slice 0 also subtracts the C grid (the sum of its column-group partials).
+//                   With a single slice it finishes the tile.
 //   reduce_kernel   (tile): sums the slices in slice order, stores S (R, T) and, for the probe,
 //                   the tile's sum |S|, max |S| and non-finite count;
-//   decide_kernel   (one work-group): clipped-mean noise, threshold and verdict.
+//   tile_decide_kernel (one work-group): clipped-mean noise, threshold and verdict.
 
 // Store S (R, T) of this thread's outputs and, in probe mode, the tile statistics.  acc holds
 // the full P Q - C grid (and Pw Q - R grid, P Qw - T grid).
@@ -1124,180 +1109,220 @@ __device__ void finish_tile(const ProductArgs& pa, int tile,
       }
     }
   if (pa.mode != 1) return;
-  const double tsum = block_sum_d<kThreads / 64>(lsum, red);
-  const double tmax = block_max_d<kThreads / 64>(lmax, red);
-  const double tbad = block_sum_d<kThreads / 64>(lbad, red);
+  double r3[3] = {lsum, lmax, lbad};
+  lds_reduce<kThreads, 3>(r3, red, 0x2u);
   if (threadIdx.x == 0) {
-    pa.tilestat[tile * 4 + 0] = tsum;
-    pa.tilestat[tile * 4 + 1] = tmax;
-    pa.tilestat[tile * 4 + 2] = tbad;
+    pa.tilestat[tile * 4 + 0] = r3[0];
+    pa.tilestat[tile * 4 + 1] = r3[1];
+    pa.tilestat[tile * 4 + 2] = r3[2];
   }
 }
 
-// Product partials.  Each k-chunk of the slab (KCH columns of P and of the transposed Q, 16 KiB
-// of FP32 per factor) is fetched with every thread issuing all of its loads before any is used,
-// so a chunk costs one memory round trip.  Both factors are staged k-contiguous, so the inner
-// loop reads four k at a time with 16-byte LDS reads; the FMAs run in FP64.
-template <int TS, bool MOM>
-__global__ __launch_bounds__(kThreads) void product_kernel(ProductArgs pa) {
-  constexpr int RT = TS / 16;
-  constexpr int NX = MOM ? 3 : 1;
-  constexpr int NF = MOM ? 2 : 1;                 // factors per side
-  constexpr int KCH = (MOM ? 2048 : 4096) / TS;   // k per chunk
-  constexpr int KP = KCH + 4;                     // padded LDS row (floats)
-  constexpr int PER = TS * KCH / kThreads;        // loads per thread per factor
-  __shared__ __align__(16) float Ps[NF][TS][KP];
-  __shared__ __align__(16) float Qt[NF][TS][KP];
-  __shared__ double red[kThreads / 64];
-  const int m = pa.m;
-  const int ntiles = pa.nt * pa.nt;
-  const int tile = blockIdx.x, slice = blockIdx.y;
-  const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
-  const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
-  const int k0 = slice * pa.ksl;
-  const int k1 = (k0 + pa.ksl < pa.n2) ? k0 + pa.ksl : pa.n2;
-  const int64_t mm = static_cast<int64_t>(m) * m;
-  double acc[NX][RT][RT];
-  // slice 0 carries minus the C grid: the sum of the column-group partials of each output
-  double cg[NX][RT][RT];
-#pragma unroll
-  for (int i = 0; i < RT; ++i)
-#pragma unroll
-    for (int j = 0; j < RT; ++j) {
-      const int row = ta * TS + ty + 16 * i, colb = tb * TS + tx + 16 * j;
-      const bool ok = slice == 0 && row < m && colb < m;
-      const int64_t o = ok ? static_cast<int64_t>(row) * m + colb : 0;
-      double cS = 0.0, cR = 0.0, cT = 0.0;
-      if (ok) {
-        for (int g = 0; g < pa.npc; ++g) {
-          cS += pa.partS[g * mm + o];
-          if (MOM) {
-            cR += pa.partR[g * mm + o];
-            cT += pa.partT[g * mm + o];
-          }
-        }
-      }
-      cg[0][i][j] = cS;
-      if (MOM) {
-        cg[1][i][j] = cR;
-        cg[2][i][j] = cT;
-      }
-#pragma unroll
-      for (int x = 0; x < NX; ++x) acc[x][i][j] = 0.0;
-    }
+// Product on the FP64 matrix cores.  A wave owns WB x WB blocks of 16 x 16 outputs, each an
+// accumulator of v_mfma_f64_16x16x4 (lane l holds rows 4 r + l / 16, column l mod 16 of a block,
+// r = 0..3).  Lane l reads row (l mod 16) of the block's factor rows (P, and the transposed Q,
+// both k-contiguous) 16 bytes at k + 4 (l / 16): the four elements feed four consecutive MFMA
+// steps, which applies one permutation of the 16 k of a step to both operands, so each k is
+// taken exactly once.  The FP32 factors are widened to FP64 (their products are exact) and
+// accumulated in FP64.  KW: the 4 waves split the k-range of one (16 WB)^2 tile and are summed in
+// wave order through LDS (the probe, few tiles); otherwise the 4 waves own the quadrants of a
+// (32 WB)^2 tile.  The C grid (minus the column-group partials of S_C, R_C, T_C) is spread over
+// the (slice, wave) pairs: each subtracts the groups assigned to it, all of a group's loads in
+// one round trip.  With one slice the kernel stores S (R, T) and the probe's tile statistics;
+// otherwise the tile partial goes to the scratch, row-major in the tile, for reduce_kernel.
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 
-  for (int kc = k0; kc < k1; kc += KCH) {
-    float pv[NF][PER], qv[NF][PER];
+template <int WB, bool KW, bool MOM>
+__global__ __launch_bounds__(kThreads) void mfma_product_kernel(ProductArgs pa) {
+  static_assert(!(KW && MOM), "the k-split tile serves the probe");
+  constexpr int NX = MOM ? 3 : 1;
+  constexpr int NF = MOM ? 2 : 1;        // factors per side: P (Pw), Q (Qw)
+  constexpr int WT = 16 * WB;            // wave tile edge
+  constexpr int TS = KW ? WT : 2 * WT;   // work-group tile edge
+  __shared__ f64x4 xl[KW ? 3 * WB * WB * 64 : 1];
+  __shared__ double red[3 * (kThreads + 2 * kThreads / 16 + 1)];
+  const int m = pa.m;
+  const int64_t mm = static_cast<int64_t>(m) * m;
+  const int ntiles = pa.nt * pa.nt;
+  // the 8 XCDs take launch indices round-robin: launch index i runs slot (i mod 8) G / 8 + i / 8
+  // of a slice-major order, so each XCD's work-groups share k-slices of the factors in its L2
+  const int per = gridDim.x / 8;
+  const int slot = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
+  if (slot >= ntiles * pa.NS) return;
+  const int slice = slot / ntiles, tile = slot - slice * ntiles;
+  const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int ro = KW ? 0 : (w >> 1) * WT, co = KW ? 0 : (w & 1) * WT;   // wave origin in the tile
+  // the wave's k-range: whole steps of 16 (loads at or past kact read zeros)
+  const int kw = KW ? pa.ksl / 4 : pa.ksl;
+  const int kbeg = slice * pa.ksl + (KW ? w * kw : 0);
+  const int kend = (kbeg + kw < pa.kact) ? kbeg + kw : pa.kact;
+  const int kq = 4 * (lane >> 4);
+  // factor rows of this lane (rows past m repeat row m - 1; their outputs are dropped)
+  const float* pr[NF][WB];
+  const float* qr[NF][WB];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) {
-      const int idx = threadIdx.x + kThreads * e;
-      const int r = idx / KCH, kk = idx - r * KCH;
-      const int k = kc + kk;
-      {
-        const int row = ta * TS + r;
-        const bool ok = row < m && k < k1;
-        const int64_t o = ok ? static_cast<int64_t>(row) * pa.ldp + k : 0;
-        const float x = pa.P[o];
-        pv[0][e] = ok ? x : 0.0f;
-        if (MOM) {
-          const float y = pa.Pw[o];
-          pv[NF - 1][e] = ok ? y : 0.0f;
-        }
-      }
-      {
-        const int colb = tb * TS + r;
-        const bool ok = colb < m && k < k1;
-        const int64_t o = ok ? static_cast<int64_t>(colb) * pa.ldp + k : 0;
-        const float x = pa.Q[o];
-        qv[0][e] = ok ? x : 0.0f;
-        if (MOM) {
-          const float y = pa.Qw[o];
-          qv[NF - 1][e] = ok ? y : 0.0f;
-        }
-      }
+  for (int i = 0; i < WB; ++i) {
+    const int ra = ta * TS + ro + 16 * i + (lane & 15);
+    const int rb = tb * TS + co + 16 * i + (lane & 15);
+    const int64_t oa = static_cast<int64_t>(ra < m ? ra : m - 1) * pa.ldp + kq;
+    const int64_t ob = static_cast<int64_t>(rb < m ? rb : m - 1) * pa.ldp + kq;
+    pr[0][i] = pa.P + oa;
+    qr[0][i] = pa.Q + ob;
+    if (MOM) {
+      pr[NF - 1][i] = pa.Pw + oa;
+      qr[NF - 1][i] = pa.Qw + ob;
     }
-#pragma unroll
-    for (int e = 0; e < PER; ++e) {
-      const int idx = threadIdx.x + kThreads * e;
-      const int r = idx / KCH, kk = idx - r * KCH;
-#pragma unroll
-      for (int f = 0; f < NF; ++f) {
-        Ps[f][r][kk] = pv[f][e];
-        Qt[f][r][kk] = qv[f][e];
-      }
-    }
-    __syncthreads();
-    // entries past k1 were staged as zeros, so whole groups of four can be used
-    const int kn = (k1 - kc < KCH) ? k1 - kc : KCH;
-    const int kn4 = (kn + 3) & ~3;
-#pragma unroll 2
-    for (int kk = 0; kk < kn4; kk += 4) {
-      float4 a[NF][RT], b[NF][RT];
-#pragma unroll
-      for (int f = 0; f < NF; ++f)
-#pragma unroll
-        for (int i = 0; i < RT; ++i) {
-          a[f][i] = *reinterpret_cast<const float4*>(&Ps[f][ty + 16 * i][kk]);
-          b[f][i] = *reinterpret_cast<const float4*>(&Qt[f][tx + 16 * i][kk]);
-        }
-#pragma unroll
-      for (int i = 0; i < RT; ++i)
-#pragma unroll
-        for (int j = 0; j < RT; ++j) {
-          const float4 ai = a[0][i], bj = b[0][j];
-          double s0 = acc[0][i][j];
-          s0 = fma(static_cast<double>(ai.x), static_cast<double>(bj.x), s0);
-          s0 = fma(static_cast<double>(ai.y), static_cast<double>(bj.y), s0);
-          s0 = fma(static_cast<double>(ai.z), static_cast<double>(bj.z), s0);
-          s0 = fma(static_cast<double>(ai.w), static_cast<double>(bj.w), s0);
-          acc[0][i][j] = s0;
-          if (MOM) {
-            const float4 awi = a[NF - 1][i], bwj = b[NF - 1][j];
-            double s1 = acc[NX - 2][i][j];
-            s1 = fma(static_cast<double>(awi.x), static_cast<double>(bj.x), s1);
-            s1 = fma(static_cast<double>(awi.y), static_cast<double>(bj.y), s1);
-            s1 = fma(static_cast<double>(awi.z), static_cast<double>(bj.z), s1);
-            s1 = fma(static_cast<double>(awi.w), static_cast<double>(bj.w), s1);
-            acc[NX - 2][i][j] = s1;
-            double s2 = acc[NX - 1][i][j];
-            s2 = fma(static_cast<double>(ai.x), static_cast<double>(bwj.x), s2);
-            s2 = fma(static_cast<double>(ai.y), static_cast<double>(bwj.y), s2);
-            s2 = fma(static_cast<double>(ai.z), static_cast<double>(bwj.z), s2);
-            s2 = fma(static_cast<double>(ai.w), static_cast<double>(bwj.w), s2);
-            acc[NX - 1][i][j] = s2;
-          }
-        }
-    }
-    __syncthreads();
   }
+  f64x4 acc[NX][WB][WB];
 #pragma unroll
   for (int x = 0; x < NX; ++x)
 #pragma unroll
-    for (int i = 0; i < RT; ++i)
+    for (int i = 0; i < WB; ++i)
 #pragma unroll
-      for (int j = 0; j < RT; ++j) acc[x][i][j] -= cg[x][i][j];
+      for (int j = 0; j < WB; ++j) acc[x][i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
 
-  if (pa.NS > 1) {
+  // every step's loads are issued one step ahead (the last step reloads itself, in bounds)
+  auto load = [&](float4 (&pv)[NF][WB], float4 (&qv)[NF][WB], int k) {
+    const bool ok = k + kq < pa.kact;    // kact is a multiple of 4: a float4 is in or out
+    const int kk = ok ? k : -kq;         // a float4 past the row reads the row's first instead
+    const float4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int x = 0; x < NX; ++x)
+    for (int f = 0; f < NF; ++f)
 #pragma unroll
-      for (int i = 0; i < RT; ++i)
+      for (int i = 0; i < WB; ++i) {
+        const float4 p = *reinterpret_cast<const float4*>(pr[f][i] + kk);
+        const float4 q = *reinterpret_cast<const float4*>(qr[f][i] + kk);
+        pv[f][i] = ok ? p : z;
+        qv[f][i] = ok ? q : z;
+      }
+  };
+  float4 pv[NF][WB], qv[NF][WB];
+  if (kbeg < kend) load(pv, qv, kbeg);
+  for (int k = kbeg; k < kend; k += 16) {
+    float4 pn[NF][WB], qn[NF][WB];
+    load(pn, qn, k + 16 < kend ? k + 16 : k);
 #pragma unroll
-        for (int j = 0; j < RT; ++j) {
-          const int64_t o = ((static_cast<int64_t>(slice) * ntiles + tile) * NX + x) * TS * TS +
-                            (ty + 16 * i) * TS + tx + 16 * j;
-          pa.scratch[o] = acc[x][i][j];
+    for (int e = 0; e < 4; ++e) {
+      double a[NF][WB], b[NF][WB];
+#pragma unroll
+      for (int f = 0; f < NF; ++f)
+#pragma unroll
+        for (int i = 0; i < WB; ++i) {
+          a[f][i] = static_cast<double>(pv[f][i][e]);
+          b[f][i] = static_cast<double>(qv[f][i][e]);
         }
-    return;
+#pragma unroll
+      for (int i = 0; i < WB; ++i)
+#pragma unroll
+        for (int j = 0; j < WB; ++j) {
+          acc[0][i][j] =
+              __builtin_amdgcn_mfma_f64_16x16x4f64(a[0][i], b[0][j], acc[0][i][j], 0, 0, 0);
+          if (MOM) {
+            acc[1][i][j] =
+                __builtin_amdgcn_mfma_f64_16x16x4f64(a[1][i], b[0][j], acc[1][i][j], 0, 0, 0);
+            acc[2][i][j] =
+                __builtin_amdgcn_mfma_f64_16x16x4f64(a[0][i], b[1][j], acc[2][i][j], 0, 0, 0);
+          }
+        }
+    }
+#pragma unroll
+    for (int f = 0; f < NF; ++f)
+#pragma unroll
+      for (int i = 0; i < WB; ++i) {
+        pv[f][i] = pn[f][i];
+        qv[f][i] = qn[f][i];
+      }
   }
-  finish_tile<TS, MOM>(pa, tile, acc, red);
+  // this wave's share of the C grid: groups g = g0, g0 + gs, ...
+  {
+    const double* part[3] = {pa.partS, pa.partR, pa.partT};
+    const int g0 = KW ? slice * 4 + w : slice;
+    const int gs = KW ? 4 * pa.NS : pa.NS;
+    for (int g = g0; g < pa.npc; g += gs) {
+      const int64_t gb = static_cast<int64_t>(g) * mm;
+#pragma unroll
+      for (int x = 0; x < NX; ++x)
+#pragma unroll
+        for (int i = 0; i < WB; ++i)
+#pragma unroll
+          for (int j = 0; j < WB; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int row = ta * TS + ro + 16 * i + 4 * r + (lane >> 4);
+              const int col = tb * TS + co + 16 * j + (lane & 15);
+              if (row < m && col < m) {
+                acc[x][i][j][r] -= part[x][gb + static_cast<int64_t>(row) * m + col];
+              }
+            }
+    }
+  }
+  if constexpr (KW) {
+    // waves 1..3 hand their accumulators to wave 0, which adds them in wave order
+    if (w > 0) {
+#pragma unroll
+      for (int i = 0; i < WB; ++i)
+#pragma unroll
+        for (int j = 0; j < WB; ++j) xl[((w - 1) * WB * WB + i * WB + j) * 64 + lane] = acc[0][i][j];
+    }
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int v = 0; v < 3; ++v)
+#pragma unroll
+        for (int i = 0; i < WB; ++i)
+#pragma unroll
+          for (int j = 0; j < WB; ++j) acc[0][i][j] += xl[(v * WB * WB + i * WB + j) * 64 + lane];
+    }
+  }
+  const bool owner = !KW || w == 0;       // waves that hold finished tile outputs
+  double* outm[3] = {pa.S, pa.R, pa.T};
+  double lsum = 0.0, lmax = 0.0, lbad = 0.0;
+#pragma unroll
+  for (int x = 0; x < NX; ++x)
+#pragma unroll
+    for (int i = 0; i < WB; ++i)
+#pragma unroll
+      for (int j = 0; j < WB; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int rt = ro + 16 * i + 4 * r + (lane >> 4);   // row and column in the tile
+          const int ct = co + 16 * j + (lane & 15);
+          const int row = ta * TS + rt, col = tb * TS + ct;
+          const bool valid = owner && row < m && col < m;
+          const double v = acc[x][i][j][r];
+          if (pa.NS > 1) {
+            if (owner) {
+              pa.scratch[((static_cast<int64_t>(slice) * ntiles + tile) * NX + x) * TS * TS +
+                         rt * TS + ct] = v;
+            }
+          } else if (valid) {
+            outm[x][static_cast<int64_t>(row) * m + col] = v;
+            if (x == 0) {
+              if (__builtin_isfinite(v)) {
+                lsum += fabs(v);
+                lmax = fmax(lmax, fabs(v));
+              } else {
+                lbad += 1.0;
+              }
+            }
+          }
+        }
+  if (pa.NS > 1 || pa.mode != 1) return;
+  double r3[3] = {lsum, lmax, lbad};
+  lds_reduce<kThreads, 3>(r3, red, 0x2u);
+  if (threadIdx.x == 0) {
+    pa.tilestat[tile * 4 + 0] = r3[0];
+    pa.tilestat[tile * 4 + 1] = r3[1];
+    pa.tilestat[tile * 4 + 2] = r3[2];
+  }
 }
 
 template <int TS, bool MOM>
 __global__ __launch_bounds__(kThreads) void reduce_kernel(ProductArgs pa) {
   constexpr int RT = TS / 16;
   constexpr int NX = MOM ? 3 : 1;
-  __shared__ double red[kThreads / 64];
+  __shared__ double red[3 * (kThreads + 2 * kThreads / 16 + 1)];
   const int ntiles = pa.nt * pa.nt;
   const int tile = blockIdx.x;
   const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
@@ -1320,39 +1345,58 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(ProductArgs pa) {
   finish_tile<TS, MOM>(pa, tile, acc, red);
 }
 
-__global__ __launch_bounds__(kThreads) void decide_kernel(ProductArgs pa) {
-  __shared__ double red[kThreads / 64];
-  const int m = pa.m;
-  const int ntiles = pa.nt * pa.nt;
-  double v = 0.0, vmax = 0.0, vbad = 0.0;
-#pragma unroll 4
-  for (int t = threadIdx.x; t < ntiles; t += kThreads) {
-    v += pa.tilestat[t * 4 + 0];
-    vmax = fmax(vmax, pa.tilestat[t * 4 + 1]);
-    vbad += pa.tilestat[t * 4 + 2];
+// The probe's decision after the tile path (one work-group of 1024): the tile statistics and
+// operand maxima in one reduction, then the clipped sum over S, whose first 16 x 1024 entries
+// were loaded with the statistics.
+__global__ __launch_bounds__(kDecideThreads) void tile_decide_kernel(ProductArgs pa) {
+  constexpr int NQ = 16;
+  __shared__ double red[5 * (kDecideThreads + 2 * kDecideThreads / 16 + 1)];
+  const int t = threadIdx.x;
+  // the running noise sum, read now so that the verdict does not wait on it
+  double acc0 = 0.0, acc1 = 0.0;
+  if (t == 0) {
+    acc0 = pa.sigma_acc[0];
+    acc1 = pa.sigma_acc[1];
   }
-  const double mm = static_cast<double>(m) * m;
-  const double sum_abs = block_sum_d<kThreads / 64>(v, red);
-  const double max_abs = block_max_d<kThreads / 64>(vmax, red);
-  const double nbad = block_sum_d<kThreads / 64>(vbad, red);
+  const int64_t mm = static_cast<int64_t>(pa.m) * pa.m;
+  const int ntiles = pa.nt * pa.nt;
+  double v[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int64_t o = t + static_cast<int64_t>(kDecideThreads) * q;
+    v[q] = o < mm ? pa.S[o] : 0.0;
+  }
+  double lsum = 0.0, lmax = 0.0, lbad = 0.0;
+  for (int i = t; i < ntiles; i += kDecideThreads) {
+    lsum += pa.tilestat[i * 4 + 0];
+    lmax = fmax(lmax, pa.tilestat[i * 4 + 1]);
+    lbad += pa.tilestat[i * 4 + 2];
+  }
+  float amax = 0.0f, bmax = 0.0f;
+  for (int i = t; i < pa.nA; i += kDecideThreads) amax = fmaxf(amax, pa.maxpart[i]);
+  for (int i = t; i < pa.nB; i += kDecideThreads) bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
+  // sums: 0, 2; maxima: 1, 3, 4
+  double r5[5] = {lsum, lmax, lbad, static_cast<double>(amax), static_cast<double>(bmax)};
+  lds_reduce<kDecideThreads, 5>(r5, red, 0x1au);
+  const double sum_abs = r5[0], max_abs = r5[1], nbad = r5[2];
   // mean|S| over all buckets (a non-finite bucket makes the mean non-finite)
-  const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / mm;
+  const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / static_cast<double>(mm);
   const double clip = 5.0 * mean_abs;
   double c2 = 0.0;
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int64_t o = t + static_cast<int64_t>(kDecideThreads) * q;
+    const double a = fabs(v[q]);
+    if (o < mm) c2 += a < clip ? a : clip;
+  }
 #pragma unroll 8
-  for (int64_t idx = threadIdx.x; idx < static_cast<int64_t>(mm); idx += kThreads) {
-    const double a = fabs(pa.S[idx]);
+  for (int64_t o = t + static_cast<int64_t>(kDecideThreads) * NQ; o < mm; o += kDecideThreads) {
+    const double a = fabs(pa.S[o]);
     c2 += a < clip ? a : clip;
   }
-  const double clipped = block_sum_d<kThreads / 64>(c2, red);
-  float amax = 0.0f, bmax = 0.0f;
-#pragma unroll 8
-  for (int i = threadIdx.x; i < pa.nA; i += kThreads) amax = fmaxf(amax, pa.maxpart[i]);
-#pragma unroll 8
-  for (int i = threadIdx.x; i < pa.nB; i += kThreads) bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
-  const double maxA = block_max_d<kThreads / 64>(static_cast<double>(amax), red);
-  const double maxB = block_max_d<kThreads / 64>(static_cast<double>(bmax), red);
-  if (threadIdx.x == 0) decide_tail(pa, sum_abs, max_abs, nbad, clipped, maxA, maxB);
+  double r1[1] = {c2};
+  lds_reduce<kDecideThreads, 1>(r1, red, 0u);
+  if (t == 0) decide_tail(pa, sum_abs, max_abs, nbad, r1[0], r5[3], r5[4], acc0, acc1);
 }
 
 // ----------------------------------------------------------------------------------------
@@ -1527,7 +1571,7 @@ hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int 
                  : stream_dispatch<0, false>(s, rb, g, ng, lds_bytes, st, e0, e1);
 }
 
-hipError_t launch_product(const ProductArgs& a0, int ts, bool moments, hipStream_t st,
+hipError_t launch_product(const ProductArgs& a0, int ts, bool kw, bool moments, hipStream_t st,
                           hipEvent_t e0, hipEvent_t e1) {
   ProductArgs a = a0;
   if (a.mode == 1 && !moments && a.nX > 0) {
@@ -1541,26 +1585,24 @@ hipError_t launch_product(const ProductArgs& a0, int ts, bool moments, hipStream
     launch_k(block_decide_kernel, dim3(1), dim3(kDecideThreads), 0, st, nullptr, e1, a);
     return hipGetLastError();
   }
-  const dim3 grid(a.nt * a.nt, a.NS);
+  const dim3 grid((a.nt * a.nt * a.NS + 7) / 8 * 8);     // whole rounds of the 8 XCDs
   const dim3 rgrid(a.nt * a.nt);
   const bool red = a.NS > 1, dec = a.mode == 1;
-#define FPSK_PRODUCT_CASE(TS_, MOM_)                                                        \
-  if (ts == TS_ && moments == MOM_) {                                                       \
-    launch_k(product_kernel<TS_, MOM_>, grid, dim3(kThreads), 0, st, e0,                    \
+#define FPSK_PRODUCT_CASE(TS_, WB_, KW_, MOM_)                                              \
+  if (ts == TS_ && kw == KW_ && moments == MOM_) {                                          \
+    launch_k(mfma_product_kernel<WB_, KW_, MOM_>, grid, dim3(kThreads), 0, st, e0,          \
              (red || dec) ? nullptr : e1, a);                                               \
     if (red) {                                                                              \
       launch_k(reduce_kernel<TS_, MOM_>, rgrid, dim3(kThreads), 0, st, nullptr,             \
                dec ? nullptr : e1, a);                                                      \
     }                                                                                       \
-    if (dec) launch_k(decide_kernel, dim3(1), dim3(kThreads), 0, st, nullptr, e1, a);       \
+    if (dec) launch_k(tile_decide_kernel, dim3(1), dim3(kDecideThreads), 0, st, nullptr, e1, a); \
     return hipGetLastError();                                                               \
   }
-  FPSK_PRODUCT_CASE(16, false)
-  FPSK_PRODUCT_CASE(16, true)
-  FPSK_PRODUCT_CASE(32, false)
-  FPSK_PRODUCT_CASE(32, true)
-  FPSK_PRODUCT_CASE(64, false)
-  FPSK_PRODUCT_CASE(64, true)
+  FPSK_PRODUCT_CASE(16, 1, true, false)
+  FPSK_PRODUCT_CASE(64, 2, false, false)
+  FPSK_PRODUCT_CASE(32, 1, false, true)
+  FPSK_PRODUCT_CASE(64, 2, false, true)
 #undef FPSK_PRODUCT_CASE
   return hipErrorInvalidValue;
 }
