@@ -586,6 +586,8 @@ struct fpsketch_ctx {
   Workspace aux_ws;
   DevBuf scan_counts, scan_rows, scan_base, scan_out, samples, patch_rowptr, patch_col,
       patch_val, rc_coords, rc_gamma, rc_abs, rc_c;
+  // localize rounds on the device: selection state and histogram, peel list, candidates
+  DevBuf sel_state, sel_hist, peel_list, cands, cand_count;
   fpsketch_plan_info last_plan{};
 
   // optional per-probe events: start and end of the stream kernel, of the product dispatches
@@ -865,11 +867,41 @@ fpsketch_status sketch_round(fpsketch_ctx* c, uint64_t seed, int round, int m, b
   return FPSK_OK;
 }
 
-double mad_sigma(const std::vector<double>& S) {
-  const double med = median_of(S);
-  std::vector<double> dev(S.size());
-  for (size_t i = 0; i < S.size(); ++i) dev[i] = std::fabs(S[i] - med);
-  return 1.4826 * median_of(dev);
+// One sketch pass at m whose S (R, T) stay in the auxiliary workspace; max|A|, max|B| to host.
+fpsketch_status sketch_round_device(fpsketch_ctx* c, uint64_t seed, int round, int m, bool mom,
+                                    const void* A, const void* B, const float* C,
+                                    const int32_t* prow, const int32_t* pcol, const float* pval,
+                                    hipStream_t st, HostRound& HR, double* maxA, double* maxB) {
+  const Decomp d = decompose(c->n1, c->n2, c->n3, m, mom);
+  build_round(seed, round, c->n1, c->n3, m, d.cwb, mom, HR);
+  FPSK_TRY(upload_round(HR, d.cwb, c->aux_round, st));
+  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, mom));
+  FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, C, mom, 0, nullptr, prow, pcol, pval, st));
+  std::vector<float> mp(static_cast<size_t>(d.nA + d.nB));
+  FPSK_HIP(hipMemcpyAsync(mp.data(), c->aux_ws.maxpart.p, mp.size() * sizeof(float),
+                          hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  float ma = 0.0f, mb = 0.0f;
+  for (int i = 0; i < d.nA; ++i) ma = std::fmax(ma, mp[i]);
+  for (int i = 0; i < d.nB; ++i) mb = std::fmax(mb, mp[d.nA + i]);
+  *maxA = ma;
+  *maxB = mb;
+  return FPSK_OK;
+}
+
+// sigma_MAD = 1.4826 median(|S - median S|) of the m^2 buckets in the auxiliary workspace,
+// selected exactly on the device (the host rule's values: even counts take the mean of the two
+// middle order statistics).
+fpsketch_status device_mad_sigma(fpsketch_ctx* c, int64_t mm, hipStream_t st, double* sigma) {
+  FPSK_TRY(dev_alloc(c->sel_state, sizeof(fpsk::SelState)));
+  FPSK_TRY(dev_alloc_zero(c->sel_hist, 256 * sizeof(uint32_t)));
+  FPSK_HIP(fpsk::launch_median_mad(as<double>(c->aux_ws.S), mm, as<fpsk::SelState>(c->sel_state),
+                                   as<uint32_t>(c->sel_hist), st));
+  fpsk::SelState h{};
+  FPSK_HIP(hipMemcpyAsync(&h, c->sel_state.p, sizeof(h), hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  *sigma = 1.4826 * h.mad;
+  return FPSK_OK;
 }
 
 struct Found {
@@ -1043,7 +1075,8 @@ void fpsketch_destroy(fpsketch_ctx* c) {
   free_workspace(c->aux_ws);
   for (DevBuf* b : {&c->stats, &c->sigma_acc, &c->zero, &c->scan_counts, &c->scan_rows, &c->scan_base,
                     &c->scan_out, &c->samples, &c->patch_rowptr, &c->patch_col, &c->patch_val,
-                    &c->rc_coords, &c->rc_gamma, &c->rc_abs, &c->rc_c}) {
+                    &c->rc_coords, &c->rc_gamma, &c->rc_abs, &c->rc_c, &c->sel_state,
+                    &c->sel_hist, &c->peel_list, &c->cands, &c->cand_count}) {
     dev_free(*b);
   }
   delete c;
@@ -1277,10 +1310,10 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
     sigma = stt[0];
   } else {
     HostRound HR0;
-    std::vector<double> S0, R0, T0;
-    FPSK_TRY(sketch_round(c, seed, 0, c->m, false, A, B, Cf, prow, pcol, pval, st, HR0, S0, R0,
-                          T0, nullptr, nullptr));
-    sigma = mad_sigma(S0);
+    double ma0 = 0.0, mb0 = 0.0;
+    FPSK_TRY(sketch_round_device(c, seed, 0, c->m, false, A, B, Cf, prow, pcol, pval, st, HR0,
+                                 &ma0, &mb0));
+    FPSK_TRY(device_mad_sigma(c, static_cast<int64_t>(c->m) * c->m, st, &sigma));
   }
   const PlanOut plan = plan_localize(c->n1, c->n2, c->n3, c->dt, c->m, sigma, rms, c->p);
   if (plan.m_loc > fpsk::kMaxM) return fail(FPSK_ESHAPE, "m_loc beyond 4096");
@@ -1308,40 +1341,76 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
   const double L1 = static_cast<double>(c->L1), L3 = static_cast<double>(c->L3);
   for (int t = 1; t <= c->p.rounds; ++t) {
     HostRound HR;
-    std::vector<double> S, Rm, T;
     double maxA = 0, maxB = 0;
-    FPSK_TRY(sketch_round(c, seed, t, m, true, A, B, Cf, prow, pcol, pval, st, HR, S, Rm, T,
-                          &maxA, &maxB));
+    FPSK_TRY(sketch_round_device(c, seed, t, m, true, A, B, Cf, prow, pcol, pval, st, HR, &maxA,
+                                 &maxB));
     tau = c->p.c_valid * static_cast<double>(c->n2) * std::ldexp(1.0, -23) * maxA * maxB;
-    // peel every finite fault confirmed so far (Sec. III-H)
+    const int64_t mm = static_cast<int64_t>(m) * m;
+    double* dS = as<double>(c->aux_ws.S);
+    double* dR = as<double>(c->aux_ws.R);
+    double* dT = as<double>(c->aux_ws.T);
+    // peel every finite fault confirmed so far (Sec. III-H), in order, on the device
+    std::vector<fpsk::PeelEntry> peel;
     for (const Found& f : F) {
       if (f.absolute) continue;
-      const size_t o = static_cast<size_t>(HR.h1[f.i]) * m + HR.h2[f.j];
+      const int64_t o = static_cast<int64_t>(HR.h1[f.i]) * m + HR.h2[f.j];
       const double sv = static_cast<double>(HR.v1[f.i]) * HR.v2[f.j] * f.delta;
-      S[o] -= sv;
-      Rm[o] -= sv * static_cast<double>(f.i + 1) / L1;
-      T[o] -= sv * static_cast<double>(f.j + 1) / L3;
+      peel.push_back({o, sv, sv * static_cast<double>(f.i + 1) / L1,
+                      sv * static_cast<double>(f.j + 1) / L3});
     }
-    const double sig = mad_sigma(S);
+    if (!peel.empty()) {
+      FPSK_TRY(dev_alloc(c->peel_list, peel.size() * sizeof(fpsk::PeelEntry)));
+      FPSK_HIP(hipMemcpyAsync(c->peel_list.p, peel.data(), peel.size() * sizeof(fpsk::PeelEntry),
+                              hipMemcpyHostToDevice, st));
+      FPSK_HIP(fpsk::launch_peel(dS, dR, dT, as<fpsk::PeelEntry>(c->peel_list),
+                                 static_cast<int>(peel.size()), st));
+    }
+    double sig = 0.0;
+    FPSK_TRY(device_mad_sigma(c, mm, st, &sig));
     const double tau_c = std::min(tau, 2.0 * sig);
     const double tau_d = static_cast<double>(std::max(c->n1, c->n3)) * sig /
                          std::max(static_cast<double>(r), 0.5);
     const double cut = std::max(tau_c, tau_d);
-    std::vector<int64_t> above;
-    for (size_t o = 0; o < S.size(); ++o)
-      if (std::fabs(S[o]) > cut) above.push_back(static_cast<int64_t>(o));
-    std::sort(above.begin(), above.end(), [&S](int64_t x, int64_t y) {
-      const double ax = std::fabs(S[x]), ay = std::fabs(S[y]);
+    // buckets with |S| > cut, with their sketches; by |S| descending, then bucket index
+    constexpr uint32_t kCandCap = 1u << 20;
+    FPSK_TRY(dev_alloc(c->cands, static_cast<size_t>(kCandCap) * sizeof(fpsk::Cand)));
+    FPSK_TRY(dev_alloc(c->cand_count, sizeof(uint32_t)));
+    FPSK_HIP(hipMemsetAsync(c->cand_count.p, 0, sizeof(uint32_t), st));
+    FPSK_HIP(fpsk::launch_above(dS, dR, dT, mm, cut, as<fpsk::Cand>(c->cands), kCandCap,
+                                as<uint32_t>(c->cand_count), st));
+    uint32_t ncand = 0;
+    FPSK_HIP(hipMemcpyAsync(&ncand, c->cand_count.p, sizeof(ncand), hipMemcpyDeviceToHost, st));
+    FPSK_HIP(hipStreamSynchronize(st));
+    std::vector<fpsk::Cand> above;
+    if (ncand <= kCandCap) {
+      above.resize(ncand);
+      if (ncand > 0) {
+        FPSK_HIP(hipMemcpyAsync(above.data(), c->cands.p, ncand * sizeof(fpsk::Cand),
+                                hipMemcpyDeviceToHost, st));
+        FPSK_HIP(hipStreamSynchronize(st));
+      }
+    } else {
+      // more candidates than the buffer holds: scan the whole grid on the host
+      std::vector<double> S(mm), Rm(mm), T(mm);
+      FPSK_HIP(hipMemcpyAsync(S.data(), dS, mm * sizeof(double), hipMemcpyDeviceToHost, st));
+      FPSK_HIP(hipMemcpyAsync(Rm.data(), dR, mm * sizeof(double), hipMemcpyDeviceToHost, st));
+      FPSK_HIP(hipMemcpyAsync(T.data(), dT, mm * sizeof(double), hipMemcpyDeviceToHost, st));
+      FPSK_HIP(hipStreamSynchronize(st));
+      for (int64_t o = 0; o < mm; ++o)
+        if (std::fabs(S[o]) > cut) above.push_back({o, S[o], Rm[o], T[o]});
+    }
+    std::sort(above.begin(), above.end(), [](const fpsk::Cand& x, const fpsk::Cand& y) {
+      const double ax = std::fabs(x.s), ay = std::fabs(y.s);
       if (ax != ay) return ax > ay;
-      return x < y;
+      return x.o < y.o;
     });
     if (static_cast<int64_t>(above.size()) > K) above.resize(K);
-    struct Cand {
+    struct Center {
       int64_t ci, cj;
     };
-    std::vector<Cand> live;
-    for (int64_t o : above) {
-      const double s = S[o], rr = Rm[o], tt = T[o];
+    std::vector<Center> live;
+    for (const fpsk::Cand& cd : above) {
+      const double s = cd.s, rr = cd.r, tt = cd.t;
       if (!(s != 0.0 && std::isfinite(s) && std::isfinite(rr) && std::isfinite(tt))) continue;
       const double ri = L1 * rr / s, rj = L3 * tt / s;
       if (!std::isfinite(ri) || !std::isfinite(rj) || std::fabs(ri) > 0x1p40 ||
@@ -1356,7 +1425,7 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
     // then replay Algorithm 1's offset-major loop sequentially.
     std::vector<int64_t> coords;
     std::unordered_map<int64_t, int32_t> slot;
-    for (const Cand& cd : live) {
+    for (const Center& cd : live) {
       for (const auto& od : offs) {
         const int64_t i = cd.ci + od.first, j = cd.cj + od.second;
         if (i < 0 || i >= c->n1 || j < 0 || j >= c->n3) continue;

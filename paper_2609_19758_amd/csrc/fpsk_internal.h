@@ -120,6 +120,38 @@ hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, const float* C, 
                           int64_t n3, int dt, const int64_t* coords, int n, double* gamma,
                           double* abssum, float* cval, hipStream_t st);
 
+// Order statistics of a bucket grid on the device (the MAD and candidate scan of a localize
+// round).  The selection state lives in device memory.
+struct SelState {
+  uint64_t prefix;     // key bits fixed so far
+  uint64_t k;          // rank sought among the keys that match the prefix
+  uint64_t next;       // smallest key above the selected one
+  uint32_t count_eq;   // keys equal to the selected one (after the last digit)
+  int32_t pass;        // digits fixed so far
+  double med;          // median of S
+  double mad;          // median of |S - med|
+};
+struct PeelEntry {     // S[o] -= ds, R[o] -= dr, T[o] -= dt
+  int64_t o;
+  double ds, dr, dt;
+};
+struct Cand {          // a bucket above the cut with its three sketches
+  int64_t o;
+  double s, r, t;
+};
+// Applies the peel list in order (one thread), so the result equals sequential subtraction.
+hipError_t launch_peel(double* S, double* R, double* T, const PeelEntry* list, int n,
+                       hipStream_t st);
+// st->med = median of S[0 .. n), then st->mad = median of |S - med| (even counts: the mean of
+// the two middle order statistics; NaN orders above +inf).  hist: 256 words of scratch, zero
+// on entry and on return.
+hipError_t launch_median_mad(const double* S, int64_t n, SelState* st, uint32_t* hist,
+                             hipStream_t st_);
+// Appends (o, S, R, T) of every bucket with |S[o]| > cut to out (at most cap; *count receives
+// the number found, which may exceed cap); the order of the entries is unspecified.
+hipError_t launch_above(const double* S, const double* R, const double* T, int64_t n,
+                        double cut, Cand* out, uint32_t cap, uint32_t* count, hipStream_t st);
+
 hipError_t launch_read(const void* src, int64_t bytes, uint32_t* out, int grid, hipStream_t st);
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int grid, hipStream_t st);
 

@@ -1454,6 +1454,144 @@ __global__ __launch_bounds__(kThreads) void scan_extract_kernel(const float* C, 
   }
 }
 
+// ----------------------------------------------------------------------------------------
+// Order statistics of the bucket grid (the MAD of Sec. III-E and the candidate scan of
+// Algorithm 1) by radix selection over order-preserving 64-bit keys: eight passes of 8-bit
+// digits, each a histogram of the keys that match the digits fixed so far, then one work-group
+// that fixes the next digit.  Exact: the selected key is the k-th smallest.
+
+// Key order equals the order of the doubles (-0 just below +0); NaN sorts above +inf.
+__device__ __forceinline__ uint64_t order_key(double x) {
+  if (__builtin_isnan(x)) return ~0ull;
+  const uint64_t u = __builtin_bit_cast(uint64_t, x);
+  return (u >> 63) ? ~u : (u | (1ull << 63));
+}
+
+__device__ __forceinline__ double key_value(uint64_t k) {
+  const uint64_t u = (k >> 63) ? (k & ~(1ull << 63)) : ~k;
+  return __builtin_bit_cast(double, u);
+}
+
+// MODE 0: keys of S; MODE 1: keys of |S - st->med|
+template <int MODE>
+__device__ __forceinline__ uint64_t sel_key(const double* S, int64_t i, double med) {
+  const double x = MODE == 0 ? S[i] : fabs(S[i] - med);
+  return order_key(x);
+}
+
+__global__ __launch_bounds__(kThreads) void sel_init_kernel(SelState* st, uint64_t k) {
+  st->prefix = 0;
+  st->k = k;
+  st->next = ~0ull;
+  st->count_eq = 0;
+  st->pass = 0;
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kThreads) void sel_hist_kernel(const double* S, int64_t n,
+                                                            const SelState* st, uint32_t* hist) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int shift = 56 - 8 * st->pass;
+  const uint64_t hmask = shift == 56 ? 0ull : (~0ull << (shift + 8));
+  const uint64_t pref = st->prefix;
+  const double med = st->med;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kThreads) {
+    const uint64_t key = sel_key<MODE>(S, i, med);
+    if ((key & hmask) == pref) atomicAdd(&h[(key >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  if (h[threadIdx.x] != 0) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
+}
+
+// One work-group of 256: the digit whose cumulative count passes k; clears the histogram.
+__global__ __launch_bounds__(kThreads) void sel_step_kernel(SelState* st, uint32_t* hist) {
+  __shared__ uint32_t h[256];
+  h[threadIdx.x] = hist[threadIdx.x];
+  __syncthreads();
+  hist[threadIdx.x] = 0;
+  if (threadIdx.x == 0) {
+    const int shift = 56 - 8 * st->pass;
+    uint64_t below = 0;
+    int b = 0;
+    for (; b < 255; ++b) {
+      if (st->k < below + h[b]) break;
+      below += h[b];
+    }
+    st->prefix |= static_cast<uint64_t>(b) << shift;
+    st->k -= below;
+    st->count_eq = h[b];
+    st->pass += 1;
+  }
+}
+
+// Smallest key above the selected one (the upper middle element when it differs).
+template <int MODE>
+__global__ __launch_bounds__(kThreads) void sel_next_kernel(const double* S, int64_t n,
+                                                            SelState* st) {
+  __shared__ uint64_t red[kThreads];
+  const uint64_t sel = st->prefix;
+  const double med = st->med;
+  uint64_t best = ~0ull;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kThreads) {
+    const uint64_t key = sel_key<MODE>(S, i, med);
+    if (key > sel && key < best) best = key;
+  }
+  red[threadIdx.x] = best;
+  __syncthreads();
+  for (int w = kThreads / 2; w > 0; w >>= 1) {
+    if (static_cast<int>(threadIdx.x) < w && red[threadIdx.x + w] < red[threadIdx.x]) {
+      red[threadIdx.x] = red[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && red[0] != ~0ull) atomicMin(reinterpret_cast<unsigned long long*>(&st->next), static_cast<unsigned long long>(red[0]));
+}
+
+// The median from the selected order statistic(s): x_(n/2) for odd n, else the mean of
+// x_(n/2 - 1) (selected) and x_(n/2) (the same key while equal keys remain, else the next).
+template <int MODE>
+__global__ __launch_bounds__(kThreads) void sel_final_kernel(SelState* st, int64_t n) {
+  const double lo = key_value(st->prefix);
+  double v = lo;
+  if (n % 2 == 0) {
+    const double hi = (st->k + 1 < st->count_eq) ? lo : key_value(st->next);
+    v = 0.5 * (lo + hi);
+  }
+  if (MODE == 0) {
+    st->med = v;
+  } else {
+    st->mad = v;
+  }
+}
+
+__global__ __launch_bounds__(1) void peel_kernel(double* S, double* R, double* T,
+                                                 const PeelEntry* list, int n) {
+  for (int q = 0; q < n; ++q) {
+    const PeelEntry e = list[q];
+    S[e.o] -= e.ds;
+    R[e.o] -= e.dr;
+    T[e.o] -= e.dt;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void above_kernel(const double* S, const double* R,
+                                                         const double* T, int64_t n, double cut,
+                                                         Cand* out, uint32_t cap,
+                                                         uint32_t* count) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kThreads) {
+    const double s = S[i];
+    if (fabs(s) > cut) {
+      const uint32_t p = atomicAdd(count, 1u);
+      if (p < cap) out[p] = Cand{i, s, R[i], T[i]};
+    }
+  }
+}
+
 __global__ __launch_bounds__(kThreads) void sample_kernel(const float* C, int64_t stride,
                                                           int64_t count, float* out) {
   const int64_t t = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
@@ -1628,6 +1766,48 @@ hipError_t launch_sample(const float* C, int64_t stride, int64_t count, float* o
   if (count <= 0) return hipSuccess;
   const unsigned grid = static_cast<unsigned>((count + kThreads - 1) / kThreads);
   hipLaunchKernelGGL(sample_kernel, dim3(grid), dim3(kThreads), 0, st, C, stride, count, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_peel(double* S, double* R, double* T, const PeelEntry* list, int n,
+                       hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(peel_kernel, dim3(1), dim3(1), 0, st, S, R, T, list, n);
+  return hipGetLastError();
+}
+
+namespace {
+unsigned grid_for(int64_t n) {
+  const int64_t g = (n + 8 * kThreads - 1) / (8 * kThreads);
+  return static_cast<unsigned>(g < 1 ? 1 : (g > 1024 ? 1024 : g));
+}
+
+template <int MODE>
+void select_median(const double* S, int64_t n, SelState* st, uint32_t* hist, hipStream_t s) {
+  const unsigned g = grid_for(n);
+  hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(1), 0, s, st,
+                     static_cast<uint64_t>(n % 2 ? n / 2 : n / 2 - 1));
+  for (int p = 0; p < 8; ++p) {
+    hipLaunchKernelGGL(sel_hist_kernel<MODE>, dim3(g), dim3(kThreads), 0, s, S, n, st, hist);
+    hipLaunchKernelGGL(sel_step_kernel, dim3(1), dim3(kThreads), 0, s, st, hist);
+  }
+  if (n % 2 == 0) hipLaunchKernelGGL(sel_next_kernel<MODE>, dim3(g), dim3(kThreads), 0, s, S, n, st);
+  hipLaunchKernelGGL(sel_final_kernel<MODE>, dim3(1), dim3(1), 0, s, st, n);
+}
+}  // namespace
+
+hipError_t launch_median_mad(const double* S, int64_t n, SelState* st, uint32_t* hist,
+                             hipStream_t s) {
+  if (n <= 0) return hipErrorInvalidValue;
+  select_median<0>(S, n, st, hist, s);
+  select_median<1>(S, n, st, hist, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_above(const double* S, const double* R, const double* T, int64_t n,
+                        double cut, Cand* out, uint32_t cap, uint32_t* count, hipStream_t st) {
+  hipLaunchKernelGGL(above_kernel, dim3(grid_for(n)), dim3(kThreads), 0, st, S, R, T, n, cut,
+                     out, cap, count);
   return hipGetLastError();
 }
 
