@@ -71,14 +71,19 @@ def cpu_baseline(w, a_bits, b_bits, c, m: int, seed: int, budget_s: float) -> di
                       f"({elapsed:.1f} s, {per_call:.2f} s/call)"}
 
 
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_19758_amd", "csrc", "fpsk_kernels.hip")
+# the sources the probe's stream kernel is built from (its counters stay valid while these do)
+KERNEL_SRC = [os.path.join(ROOT, "paper_2609_19758_amd", "csrc", f)
+              for f in ("fpsk_stream.hip", "fpsk_device.h", "fpsk_internal.h")]
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "stream_kernel_square4096_bf16_pmc.txt")
 
 
 def kernel_source_hash() -> str:
     import hashlib
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SRC:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_from_summary(workload: str):
@@ -165,12 +170,12 @@ def write_pmc_summary(workload: str, fetch_db: str, write_db: str) -> int:
     lines = [
         f"# HBM traffic of the FP-Sketch probe's stream kernel, {workload}",
         "# commands (from /tmp, repo at $R), one counter per run:",
-        "#   rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/fetch -o run -- python3 $R/bench.py "
+        "#   rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/fetch21 -o run -- python3 $R/bench.py "
         "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --copy-calibration 256",
-        "#   rocprofv3 --pmc WRITE_SIZE -d $R/gpurun_out/write -o run -- python3 $R/bench.py "
+        "#   rocprofv3 --pmc WRITE_SIZE -d $R/gpurun_out/write21 -o run -- python3 $R/bench.py "
         "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --copy-calibration 256",
-        "#   python3 bench.py --write-pmc-summary gpurun_out/fetch/run_results.db "
-        "gpurun_out/write/run_results.db",
+        "#   python3 bench.py --write-pmc-summary gpurun_out/fetch21/run_results.db "
+        "gpurun_out/write21/run_results.db",
         "# scale: the copy kernel moves 262144 KiB in and 262144 KiB out per dispatch",
         f"workload={workload}",
         f"kernel={sk}",

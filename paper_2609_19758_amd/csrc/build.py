@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 OUT = os.path.join(PKG, "libfpsketch.so")
-SOURCES = ["fpsk_kernels.hip", "fpsk_host.hip"]
+SOURCES = ["fpsk_stream.hip", "fpsk_kernels.hip", "fpsk_host.hip"]
 
 # gfx950 only; packed FP32 instructions disabled (hipcc forms them from plain float code).
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

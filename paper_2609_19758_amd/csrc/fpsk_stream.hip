@@ -1,0 +1,697 @@
+// gfx950 stream kernel of the FP-Sketch post hoc verifier: one pass over A, B and C forming
+// the factors of Eq. 1 without forming AB: P = H1 A (row-bucket segmented reduction),
+// Q = B H2^T (column-bucket fold of each row of B) and the bucket grid of C (row-bucket
+// accumulation, then a column-bucket fold once per row bucket and tile); with moments, the
+// weighted forms that give the first-moment sketches R and T (paper, Sec. III-B).  No atomics:
+// every sum has a fixed order, so sketches are bit-reproducible.  Streaming sums accumulate in
+// FP64.
+#include "fpsk_device.h"
+
+namespace fpsk {
+
+// ----------------------------------------------------------------------------------------
+// Row-bucket passes (A and C work-groups).  Wave w of a work-group takes rows w, w + 4, ... of
+// the bucket's sorted row list.  The row entries of up to 64 of its rows arrive with one vector
+// load and are broadcast with readlane, so a group of row loads issues back to back instead of
+// waiting on an index load per row.
+
+// Row entry (row | negative-sign bit) of this wave's r-th row in the current batch.
+__device__ __forceinline__ int32_t row_entry(int32_t pe, int r) {
+  return __builtin_amdgcn_readlane(pe, r);
+}
+
+// A work-group: bucket a, column tile t of A.  P[a, tile] = sum over the bucket's rows of
+// v1(i) A[i, tile] (and Pw with w_i).  Groups of 8 rows are summed in FP32 (their partial sums
+// stay within a few units of the last place of the stored FP32 factor), groups in FP64; the 4
+// waves are combined in fixed wave order.
+template <int DT, bool MOM, bool VEC>
+__device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) {
+  constexpr int U = 8;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int a = u / s.TA, t = u - a * s.TA;
+  const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
+  const bool lane_ok = col < s.n2;
+  const int32_t* prow = s.perm + static_cast<int64_t>(a) * s.cap;
+  double acc[8], accw[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    acc[k] = 0.0;
+    accw[k] = 0.0;
+  }
+  uint32_t mx = 0;
+  for (int base = w; base < s.cap; base += 4 * 64) {
+    const int32_t pe = base + 4 * lane < s.cap ? prow[base + 4 * lane] : -1;
+    const int nr = __popcll(__ballot(pe != -1));   // valid entries are a prefix of the lanes
+    if (nr == 0) break;
+    for (int r0 = 0; r0 < nr; r0 += U) {
+      u32x4 v[U];
+      float sg[U], sw[U];
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+        const bool ok = r0 + q < nr;
+        const int32_t e = row_entry(pe, ok ? r0 + q : 0);
+        const int64_t row = e & 0x7fffffff;
+        sg[q] = ok ? (e < 0 ? -1.0f : 1.0f) : 0.0f;
+        sw[q] = MOM ? static_cast<float>(sg[q] * static_cast<double>(row + 1) * s.inv_l1) : 0.0f;
+        if (VEC) {
+          v[q] = load8h_sel(s.A + row * s.n2 + col, ok && lane_ok, s.zero);
+        } else {
+          v[q] = ok ? load8h(s.A + row * s.n2, col, s.n2, false) : u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+      float g32[8], gw32[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        g32[k] = 0.0f;
+        gw32[k] = 0.0f;
+      }
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const uint32_t wd = v[q][h];
+          mx = absmax2(mx, wd);
+          const float x0 = lo_half<DT>(wd), x1 = hi_half<DT>(wd);
+          g32[2 * h] = fmaf(sg[q], x0, g32[2 * h]);
+          g32[2 * h + 1] = fmaf(sg[q], x1, g32[2 * h + 1]);
+          if (MOM) {
+            gw32[2 * h] = fmaf(sw[q], x0, gw32[2 * h]);
+            gw32[2 * h + 1] = fmaf(sw[q], x1, gw32[2 * h + 1]);
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        acc[k] += static_cast<double>(g32[k]);
+        if (MOM) accw[k] += static_cast<double>(gw32[k]);
+      }
+    }
+  }
+  // Combine the 4 waves: layout [wave][k][lane].
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    lds[(w * 8 + k) * 64 + lane] = acc[k];
+    if (MOM) lds[2048 + (w * 8 + k) * 64 + lane] = accw[k];
+  }
+  const float amax = block_absmax_half<DT>(mx, ldsu);   // contains __syncthreads
+  for (int c = threadIdx.x; c < kColTile; c += kThreads) {
+    const int ln = c >> 3, k = c & 7;
+    const int64_t gc = static_cast<int64_t>(t) * kColTile + c;
+    if (gc < s.n2) {
+      double v = lds[k * 64 + ln] + lds[(8 + k) * 64 + ln];
+      v += lds[(16 + k) * 64 + ln];
+      v += lds[(24 + k) * 64 + ln];
+      s.P[static_cast<int64_t>(a) * s.ldp + gc] = static_cast<float>(v);
+      if (MOM) {
+        double vw = lds[2048 + k * 64 + ln] + lds[2048 + (8 + k) * 64 + ln];
+        vw += lds[2048 + (16 + k) * 64 + ln];
+        vw += lds[2048 + (24 + k) * 64 + ln];
+        s.Pw[static_cast<int64_t>(a) * s.ldp + gc] = static_cast<float>(vw);
+      }
+    }
+  }
+  if (threadIdx.x == 0) s.maxpart[u] = amax;
+}
+
+// ----------------------------------------------------------------------------------------
+// B work-group: RB consecutive rows of B, all columns, in chunks of CW = kBChunkHalfs / RB
+// columns.  Per chunk, every thread issues its 8 x 16-byte loads of B and its share of the
+// chunk's bucket-sorted column list at once; B is then staged column-major ([column][RB rows])
+// in LDS and thread (row group rg, bucket b) folds the chunk's columns of bucket b for its
+// RB / NG rows: Q[k, b] = sum v2(j) B[k, j].
+
+template <int RB>
+__device__ __forceinline__ uint32_t pick_half(uint32_t wa, uint32_t wb, int odd) {
+  return odd ? ((wa >> 16) | (wb & 0xffff0000u)) : ((wa & 0xffffu) | (wb << 16));
+}
+
+// Write the 8 columns held by one thread (RB rows x 8 columns) column-major into LDS.  Column
+// 8 g8 + e goes to slot e (W / 8) + g8 of a chunk of W = kBChunkHalfs / RB columns: one base
+// address (dst = slot g8) plus the constant offset e * kBChunkHalfs / 8 halfs per column, and
+// the lanes of a wave write consecutive slots.
+template <int RB>
+__device__ __forceinline__ void store_cols(uint16_t* dst, const u32x4* v) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    uint16_t* d = dst + e * (kBChunkHalfs / 8);
+    if constexpr (RB == 1) {
+      d[0] = static_cast<uint16_t>(v[0][e >> 1] >> (16 * (e & 1)));
+    } else if constexpr (RB == 2) {
+      *reinterpret_cast<uint32_t*>(d) = pick_half<RB>(v[0][e >> 1], v[1][e >> 1], e & 1);
+    } else if constexpr (RB == 4) {
+      u32x2 o;
+      o[0] = pick_half<RB>(v[0][e >> 1], v[1][e >> 1], e & 1);
+      o[1] = pick_half<RB>(v[2][e >> 1], v[3][e >> 1], e & 1);
+      *reinterpret_cast<u32x2*>(d) = o;
+    } else {
+      u32x4 o;
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) o[rr] = pick_half<RB>(v[2 * rr][e >> 1], v[2 * rr + 1][e >> 1], e & 1);
+      *reinterpret_cast<u32x4*>(d) = o;
+    }
+  }
+}
+
+// Staged slot of column cc of a chunk of CW columns (CW itself is the zero sentinel slot).
+template <int CW>
+__device__ __forceinline__ int col_slot(int cc) {
+  return cc < CW ? (cc & 7) * (CW / 8) + (cc >> 3) : CW;
+}
+
+// RBG consecutive halfs of one staged column.
+template <int DT, int RBG>
+__device__ __forceinline__ void load_col(const uint16_t* src, float* x) {
+  if constexpr (RBG == 1) {
+    x[0] = half_bits_to_float<DT>(*src);
+  } else if constexpr (RBG == 2) {
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(src);
+    x[0] = lo_half<DT>(w);
+    x[1] = hi_half<DT>(w);
+  } else if constexpr (RBG == 4) {
+    const u32x2 w = *reinterpret_cast<const u32x2*>(src);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      x[2 * h] = lo_half<DT>(w[h]);
+      x[2 * h + 1] = hi_half<DT>(w[h]);
+    }
+  } else {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(src);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      x[2 * h] = lo_half<DT>(w[h]);
+      x[2 * h + 1] = hi_half<DT>(w[h]);
+    }
+  }
+}
+
+// Loads of one B chunk in flight: 8 x 16 bytes of B, the sign bits of the thread's columns,
+// the chunk's staged column list and this thread's segment bounds.
+template <int RB, int G, int NT>
+struct BChunk {
+  static constexpr int NV = kBChunkHalfs / 8 / kThreads;
+  static constexpr int NI = NV / RB;
+  u32x4 v[NV];
+  u32x4 tv[NT];
+  uint32_t sb[NI];
+  int qb[G], qe[G];
+};
+
+template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
+__device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, uint32_t* ldsu) {
+  constexpr int CW = kBChunkHalfs / RB;      // columns per chunk
+  constexpr int RBG = RB / NG;               // rows per fold group
+  constexpr int SLOTS = kThreads / NG;       // bucket slots per fold group
+  constexpr int PADG = (RB == 8 && G == 1) ? 8 : 1; // bucket segments padded to this multiple
+  constexpr int NT = PADG == 8 ? 2 : (CW / 8 / kThreads > 0 ? CW / 8 / kThreads : 1);
+  // Group fold (probe, 8 rows, m <= 256): thread t sums the 8 columns of entry groups t and
+  // t + 256 of the chunk's sorted list (each group lies in one bucket, as segments are padded
+  // to whole groups) over all 8 rows with one 16-byte LDS read per column; thread (b, r) then
+  // adds the group partials of bucket b, row r in FP64.
+  constexpr bool GF = !MOM && PADG == 8;
+  constexpr int GFP = 8 / NG;                // (bucket, row) pairs per thread: 8 m <= 2048 / NG
+  double qacc[GF ? GFP : 1];
+#pragma unroll
+  for (int i = 0; i < (GF ? GFP : 1); ++i) qacc[i] = 0.0;
+  using Chunk = BChunk<RB, G, NT>;
+  constexpr int NI = Chunk::NI;
+  static_assert(Chunk::NV == 8, "each thread stages 64 halfs of B per chunk");
+  const int m = s.m;
+  const int stride = s.btab_stride;
+  const int rg = threadIdx.x / SLOTS, bslot = threadIdx.x - rg * SLOTS;
+  const int64_t k0 = static_cast<int64_t>(u) * RB;
+  double acc[G][RBG], accw[G][RBG];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+#pragma unroll
+    for (int r = 0; r < RBG; ++r) {
+      acc[g][r] = 0.0;
+      accw[g][r] = 0.0;
+    }
+  }
+  if (threadIdx.x < RB) L[CW * RB + threadIdx.x] = 0;   // zero sentinel column
+  uint32_t mx = 0;
+
+  // Every load of chunk c, unconditionally (a chunk past the end reads the zero buffer).
+  auto issue = [&](Chunk& ch, int c) {
+    const bool live = c < s.TB;
+    const int64_t cbase = static_cast<int64_t>(c) * CW;
+#pragma unroll
+    for (int it = 0; it < NI; ++it) {
+      const int g8 = threadIdx.x + kThreads * it;
+      const int64_t col = cbase + static_cast<int64_t>(g8) * 8;
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const bool ok = live && k0 + r < s.n2 && col < s.n3;
+        if (VEC) {
+          ch.v[it * RB + r] = load8h_sel(s.B + (k0 + r) * s.n3 + col, ok, s.zero);
+        } else {
+          ch.v[it * RB + r] = ok ? load8h(s.B + (k0 + r) * s.n3, col, s.n3, false)
+                                 : u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+      const uint8_t* sp = live ? s.bsign + cbase / 8 + g8 : static_cast<const uint8_t*>(s.zero);
+      ch.sb[it] = *sp;
+    }
+    const uint16_t* btab = s.btab + static_cast<int64_t>(live ? c : 0) * stride;
+#pragma unroll
+    for (int it = 0; it < NT; ++it) {
+      const int o = (threadIdx.x + kThreads * it) * 8;
+      const u32x4* tp = (live && o < stride) ? reinterpret_cast<const u32x4*>(btab + o)
+                                             : static_cast<const u32x4*>(s.zero);
+      ch.tv[it] = *tp;
+    }
+    const int32_t* boff = s.boff + static_cast<int64_t>(live ? c : 0) * (m + 1);
+    if constexpr (GF) {
+      // segment starts m + 1 <= 257: entries t and t + 256, staged in LDS after the list
+      const int t = threadIdx.x;
+      const int32_t* p0 = (live && t <= m) ? boff + t : static_cast<const int32_t*>(s.zero);
+      const int32_t* p1 = (live && t + kThreads <= m) ? boff + t + kThreads
+                                                      : static_cast<const int32_t*>(s.zero);
+      ch.qb[0] = *p0;
+      ch.qe[0] = *p1;
+    } else {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int b = bslot + SLOTS * g;
+        const int32_t* bp = (live && b < m) ? boff + b : static_cast<const int32_t*>(s.zero);
+        ch.qb[g] = bp[0];
+        ch.qe[g] = bp[1];
+      }
+    }
+  };
+
+  // Stage chunk c (signs v2(j) applied to the halves) and fold it.
+  auto process = [&](Chunk& ch, int c) {
+    const int64_t cbase = static_cast<int64_t>(c) * CW;
+#pragma unroll
+    for (int it = 0; it < NI; ++it) {
+      const int g8 = threadIdx.x + kThreads * it;
+      u32x4 smask;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        smask[h] = (((ch.sb[it] >> (2 * h)) & 1u) << 15) | (((ch.sb[it] >> (2 * h + 1)) & 1u) << 31);
+      }
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) mx = absmax2(mx, ch.v[it * RB + r][h]);
+        ch.v[it * RB + r] ^= smask;
+      }
+      store_cols<RB>(L + static_cast<int64_t>(g8) * RB, ch.v + it * RB);
+    }
+#pragma unroll
+    for (int it = 0; it < NT; ++it) {
+      const int o = (threadIdx.x + kThreads * it) * 8;
+      if (o < stride) *reinterpret_cast<u32x4*>(tabL + o) = ch.tv[it];
+    }
+    if constexpr (GF) {
+      int32_t* boffL = reinterpret_cast<int32_t*>(tabL + stride);
+      const int t = threadIdx.x;
+      if (t <= m) boffL[t] = ch.qb[0];
+      if (t + kThreads <= m) boffL[t + kThreads] = ch.qe[0];
+    }
+    __syncthreads();
+    if constexpr (GF) {
+      const int32_t* boffL = reinterpret_cast<const int32_t*>(tabL + stride);
+      const int ngroups = boffL[m] >> 3;
+      float part[2][8];
+      // FP16: x * one + part converts and adds in one instruction (v_fma_mix_f32) without a
+      // temporary; `one` is opaque so the multiply by 1 is not folded away (exact either way)
+      float one = 1.0f;
+      asm volatile("" : "+v"(one));
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int grp = threadIdx.x + kThreads * h;
+        const bool gok = grp < ngroups;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) part[h][r] = 0.0f;
+        if (h == 1 && ngroups <= kThreads) break;   // uniform: no second groups
+        // a missing group reads the zero sentinel column
+        const u32x4 tw = *reinterpret_cast<const u32x4*>(tabL + 8 * (gok ? grp : 0));
+#pragma unroll
+        for (int z0 = 0; z0 < 8; z0 += 4) {
+          u32x4 cv[4];
+#pragma unroll
+          for (int z = 0; z < 4; ++z) {
+            const int zz = z0 + z;
+            const int e = gok ? static_cast<int>((tw[zz >> 1] >> (16 * (zz & 1))) & 0xffffu) : CW;
+            cv[z] = *reinterpret_cast<const u32x4*>(L + e * RB);
+          }
+#pragma unroll
+          for (int z = 0; z < 4; ++z)
+#pragma unroll
+            for (int w2 = 0; w2 < 4; ++w2) {
+              if constexpr (DT == 0) {
+                part[h][2 * w2] = __builtin_fmaf(lo_half<DT>(cv[z][w2]), one, part[h][2 * w2]);
+                part[h][2 * w2 + 1] =
+                    __builtin_fmaf(hi_half<DT>(cv[z][w2]), one, part[h][2 * w2 + 1]);
+              } else {
+                part[h][2 * w2] += lo_half<DT>(cv[z][w2]);
+                part[h][2 * w2 + 1] += hi_half<DT>(cv[z][w2]);
+              }
+            }
+        }
+      }
+      __syncthreads();
+      // group partials [group][row] over the staged data (the zero column lies beyond them)
+      float* PL = reinterpret_cast<float*>(L);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int grp = threadIdx.x + kThreads * h;
+        if (grp < ngroups) {
+          *reinterpret_cast<f32x4*>(PL + grp * 8) =
+              f32x4{part[h][0], part[h][1], part[h][2], part[h][3]};
+          *reinterpret_cast<f32x4*>(PL + grp * 8 + 4) =
+              f32x4{part[h][4], part[h][5], part[h][6], part[h][7]};
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < GFP; ++i) {
+        const int p = threadIdx.x + kThreads * i;
+        if (p < 8 * m) {
+          const int b = p >> 3, r = p & 7;
+          const int g1 = boffL[b + 1] >> 3;
+          double sum = 0.0;
+          for (int g = boffL[b] >> 3; g < g1; ++g) sum += static_cast<double>(PL[g * 8 + r]);
+          qacc[i] += sum;
+        }
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < (GF ? 0 : G); ++g) {
+      if constexpr (PADG == 8) {
+        // segments are whole multiples of 8 entries (sentinels read the zero slot): 8 list
+        // entries with one LDS read, their 8 columns summed in FP32, then added in FP64
+        for (int q = ch.qb[g]; q < ch.qe[g]; q += 8) {
+          const u32x4 tw = *reinterpret_cast<const u32x4*>(tabL + q);
+          float part[RBG], partw[RBG];
+#pragma unroll
+          for (int r = 0; r < RBG; ++r) {
+            part[r] = 0.0f;
+            partw[r] = 0.0f;
+          }
+#pragma unroll
+          for (int z = 0; z < 8; ++z) {
+            const int e = static_cast<int>((tw[z >> 1] >> (16 * (z & 1))) & 0xffffu);
+            float x[RBG];
+            if (MOM) {
+              // MOM tables hold column offsets: slot swizzle and weight w_j per column
+              load_col<DT, RBG>(L + col_slot<CW>(e) * RB + rg * RBG, x);
+              const float wj = static_cast<float>(static_cast<double>(cbase + e + 1) * s.inv_l3);
+#pragma unroll
+              for (int r = 0; r < RBG; ++r) partw[r] = fmaf(wj, x[r], partw[r]);
+            } else {
+              load_col<DT, RBG>(L + e * RB + rg * RBG, x);   // pre-swizzled slot
+            }
+#pragma unroll
+            for (int r = 0; r < RBG; ++r) part[r] += x[r];
+          }
+#pragma unroll
+          for (int r = 0; r < RBG; ++r) {
+            acc[g][r] += static_cast<double>(part[r]);
+            if (MOM) accw[g][r] += static_cast<double>(partw[r]);
+          }
+        }
+      } else {
+        for (int q = ch.qb[g]; q < ch.qe[g]; ++q) {
+          const int e = tabL[q];
+          float x[RBG];
+          load_col<DT, RBG>(L + (MOM ? col_slot<CW>(e) : e) * RB + rg * RBG, x);
+          const double wj = MOM ? static_cast<double>(cbase + e + 1) * s.inv_l3 : 0.0;
+#pragma unroll
+          for (int r = 0; r < RBG; ++r) {
+            const double d = static_cast<double>(x[r]);
+            acc[g][r] += d;
+            if (MOM) accw[g][r] = fma(d, wj, accw[g][r]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  };
+
+  for (int c = 0; c < s.TB; ++c) {
+    Chunk ch;
+    issue(ch, c);
+    process(ch, c);
+  }
+  if constexpr (GF) {
+#pragma unroll
+    for (int i = 0; i < GFP; ++i) {
+      const int p = threadIdx.x + kThreads * i;
+      const int64_t k = k0 + (p & 7);
+      if (p < 8 * m && k < s.n2) {
+        s.Q[static_cast<int64_t>(p >> 3) * s.ldp + k] = static_cast<float>(qacc[i]);
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < (GF ? 0 : G); ++g) {
+    const int b = bslot + SLOTS * g;
+    if (b < m) {
+#pragma unroll
+      for (int r = 0; r < RBG; ++r) {
+        const int64_t k = k0 + rg * RBG + r;
+        if (k < s.n2) {
+          s.Q[static_cast<int64_t>(b) * s.ldp + k] = static_cast<float>(acc[g][r]);
+          if (MOM) s.Qw[static_cast<int64_t>(b) * s.ldp + k] = static_cast<float>(accw[g][r]);
+        }
+      }
+    }
+  }
+  const float bmax = block_absmax_half<DT>(mx, ldsu);
+  if (threadIdx.x == 0) s.maxpart[s.nA + u] = bmax;
+}
+
+// ----------------------------------------------------------------------------------------
+// C work-group: row bucket a, a group of tg column tiles.  Per tile, the 4 waves accumulate
+// v1(i) C[i, tile] (and w_i v1(i) C) over the bucket's rows in FP64, combine in fixed order,
+// and thread b folds the tile's columns of bucket b from the tile's bucket-sorted column list
+// (staged in LDS with the row loads): S_C[a, b] += sum v2(j) colsum[j] (T_C with w_j, R_C from
+// the row-weighted sums).  One partial per tile group.
+
+template <bool MOM, int G, bool VEC>
+__device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) {
+  constexpr int U = 8;
+  constexpr int PADG = G == 1 ? 8 : 1;       // bucket segments padded to this multiple
+  const int m = s.m;
+  const int a = u / s.npc, gi = u - a * s.npc;
+  const int t0 = gi * s.tg;
+  const int t1 = (t0 + s.tg < s.TC) ? t0 + s.tg : s.TC;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int32_t* prow = s.perm + static_cast<int64_t>(a) * s.cap;
+  const bool patched = s.patch_rowptr != nullptr;
+  double* comb = lds;                          // [2][4][8][64]
+  double* cs = lds + (MOM ? 4096 : 2048);      // column sums [513] (+ weighted at 520)
+  double fS[G], fR[G], fT[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    fS[g] = 0.0;
+    fR[g] = 0.0;
+    fT[g] = 0.0;
+  }
+  for (int t = t0; t < t1; ++t) {
+    const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
+    const bool lane_ok = col < s.n3;
+    // fold tables of this tile, loaded with the first rows
+    const int stride = s.ctab_stride;
+    const uint16_t* ctab = s.ctab + static_cast<int64_t>(t) * stride;
+    u32x4 tv[2];
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int o = (threadIdx.x + kThreads * it) * 8;
+      tv[it] = o < stride ? *reinterpret_cast<const u32x4*>(ctab + o) : u32x4{0u, 0u, 0u, 0u};
+    }
+    const int32_t* coff = s.coff + static_cast<int64_t>(t) * (m + 1);
+    int qb[G], qe[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int b = threadIdx.x + kThreads * g;
+      qb[g] = b < m ? coff[b] : 0;
+      qe[g] = b < m ? coff[b + 1] : 0;
+    }
+    double acc[8], accw[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      acc[k] = 0.0;
+      accw[k] = 0.0;
+    }
+    for (int base = w; base < s.cap; base += 4 * 64) {
+      const int32_t pe = base + 4 * lane < s.cap ? prow[base + 4 * lane] : -1;
+      const int nr = __popcll(__ballot(pe != -1));
+      if (nr == 0) break;
+      for (int r0 = 0; r0 < nr; r0 += U) {
+        f32x4 v0[U], v1[U];
+        double sg[U], sw[U];
+        int64_t rows[U];
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+          const bool ok = r0 + q < nr;
+          const int32_t e = row_entry(pe, ok ? r0 + q : 0);
+          const int64_t row = e & 0x7fffffff;
+          rows[q] = row;
+          sg[q] = ok ? (e < 0 ? -1.0 : 1.0) : 0.0;
+          sw[q] = MOM ? sg[q] * static_cast<double>(row + 1) * s.inv_l1 : 0.0;
+          if (VEC) {
+            load8f_sel(s.C + row * s.n3 + col, ok && lane_ok, s.zero, v0[q], v1[q]);
+          } else if (ok) {
+            load8f(s.C + row * s.n3, col, s.n3, false, v0[q], v1[q]);
+          } else {
+            v0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+            v1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
+        if (patched) {
+#pragma unroll
+          for (int q = 0; q < U; ++q) {
+            if (r0 + q < nr) apply_patches(s, rows[q], col, v0[q], v1[q]);
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const double x = static_cast<double>(e < 4 ? v0[q][e] : v1[q][e - 4]);
+            acc[e] = fma(x, sg[q], acc[e]);
+            if (MOM) accw[e] = fma(x, sw[q], accw[e]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int o = (threadIdx.x + kThreads * it) * 8;
+      if (o < stride) *reinterpret_cast<u32x4*>(tabL + o) = tv[it];
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      comb[(w * 8 + k) * 64 + lane] = acc[k];
+      if (MOM) comb[2048 + (w * 8 + k) * 64 + lane] = accw[k];
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < kColTile; c += kThreads) {
+      const int ln = c >> 3, k = c & 7;
+      double v = comb[k * 64 + ln] + comb[(8 + k) * 64 + ln];
+      v += comb[(16 + k) * 64 + ln];
+      v += comb[(24 + k) * 64 + ln];
+      cs[c] = v;
+      if (MOM) {
+        double vw = comb[2048 + k * 64 + ln] + comb[2048 + (8 + k) * 64 + ln];
+        vw += comb[2048 + (16 + k) * 64 + ln];
+        vw += comb[2048 + (24 + k) * 64 + ln];
+        cs[520 + c] = vw;
+      }
+    }
+    if (threadIdx.x == 0) {
+      cs[kColTile] = 0.0;            // zero sentinel column
+      if (MOM) cs[520 + kColTile] = 0.0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      for (int q = qb[g]; q < qe[g]; q += PADG) {
+        uint32_t ez[PADG];
+        if constexpr (PADG == 8) {
+          const u32x4 tw = *reinterpret_cast<const u32x4*>(tabL + q);
+#pragma unroll
+          for (int z = 0; z < 8; ++z) ez[z] = (tw[z >> 1] >> (16 * (z & 1))) & 0xffffu;
+        } else {
+          ez[0] = tabL[q];
+        }
+#pragma unroll
+        for (int z = 0; z < PADG; ++z) {
+          const int cc = ez[z] & 0x7fff;
+          const double sgd = (ez[z] & 0x8000u) ? -1.0 : 1.0;
+          const double x = sgd * cs[cc];
+          fS[g] += x;
+          if (MOM) {
+            const double wj =
+                static_cast<double>(static_cast<int64_t>(t) * kColTile + cc + 1) * s.inv_l3;
+            fT[g] = fma(x, wj, fT[g]);
+            fR[g] += sgd * cs[520 + cc];
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int b = threadIdx.x + kThreads * g;
+    if (b < m) {
+      const int64_t o = (static_cast<int64_t>(gi) * m + a) * m + b;
+      s.partS[o] = fS[g];
+      if (MOM) {
+        s.partR[o] = fR[g];
+        s.partT[o] = fT[g];
+      }
+    }
+  }
+}
+
+// LDS layout of the stream kernel (dynamic): the A/C combine area or the staged B chunk first,
+// then the sorted column list of the current B chunk or C tile.
+template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
+__global__ __launch_bounds__(kThreads, MOM ? 2 : 4) void stream_kernel(StreamArgs s) {
+  extern __shared__ double lds_dyn[];
+  __shared__ uint32_t ldsu[kThreads / 64];
+  // the sorted column list of the current B chunk or C tile follows the data area
+  uint16_t* tabL = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(lds_dyn) + s.tab_off);
+  // Work-groups are dispatched in index order: the C work-groups (the largest) come first, then
+  // B, then A, so the short A work-groups fill the tail.
+  int u = blockIdx.x;
+  if (u < s.nC) {
+    c_unit<MOM, G, VEC>(s, u, lds_dyn, tabL);
+    return;
+  }
+  u -= s.nC;
+  if (u < s.nB) {
+    b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
+    return;
+  }
+  a_unit<DT, MOM, VEC>(s, u - s.nB, lds_dyn, ldsu);
+}
+
+// ----------------------------------------------------------------------------------------
+// Launcher.
+
+template <int DT, bool MOM>
+static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, int ng, size_t lds,
+                                  hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  const int grid = s.nA + s.nB + s.nC;
+  if (grid <= 0) return hipSuccess;
+  const bool vec = s.vec_a && s.vec_b && s.vec_c;
+#define FPSK_STREAM_CASE(RB_, G_, NG_)                                                        \
+  if (rb == RB_ && g == G_ && ng == NG_) {                                                    \
+    if (vec) {                                                                                \
+      launch_k(stream_kernel<DT, MOM, RB_, G_, NG_, true>, dim3(grid), dim3(kThreads), lds,   \
+               st, e0, e1, s);                                                                \
+    } else {                                                                                  \
+      launch_k(stream_kernel<DT, MOM, RB_, G_, NG_, false>, dim3(grid), dim3(kThreads), lds,  \
+               st, e0, e1, s);                                                                \
+    }                                                                                         \
+    return hipGetLastError();                                                                 \
+  }
+  FPSK_STREAM_CASE(8, 1, 4)
+  FPSK_STREAM_CASE(8, 1, 2)
+  FPSK_STREAM_CASE(8, 1, 1)
+  FPSK_STREAM_CASE(8, 2, 1)
+  FPSK_STREAM_CASE(4, 4, 1)
+  FPSK_STREAM_CASE(2, 8, 1)
+  FPSK_STREAM_CASE(1, 16, 1)
+#undef FPSK_STREAM_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g, int ng,
+                         size_t lds_bytes, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  if (dt == 1) {
+    return moments ? stream_dispatch<1, true>(s, rb, g, ng, lds_bytes, st, e0, e1)
+                   : stream_dispatch<1, false>(s, rb, g, ng, lds_bytes, st, e0, e1);
+  }
+  return moments ? stream_dispatch<0, true>(s, rb, g, ng, lds_bytes, st, e0, e1)
+                 : stream_dispatch<0, false>(s, rb, g, ng, lds_bytes, st, e0, e1);
+}
+
+}  // namespace fpsk
