@@ -571,3 +571,30 @@ def localize(a64, b64, c32, fmt: str, m: int, seed: int, p: Params,
         hr = make_round(seed, t, n1, n3, plan.m_loc)
         localize_round(a64, b64, E, hr, plan.r, tau, F, p, t, trace)
     return LocalizeResult(F, plan, sig, rms, tau, trace)
+
+
+# ---------------------------------------------------------------------------------------------
+# Apply (Algorithm 2, last part).
+
+
+def apply_records(c32: np.ndarray, F) -> np.ndarray:
+    """A repaired copy of C: each record written in order, C_ij := delta for an absolute entry
+    (its recomputed value), else C_ij := C_ij + delta, the sum formed in FP64 and rounded to
+    FP32 (C is delivered in FP32).  The input is not modified."""
+    out = np.array(c32, dtype=np.float32, copy=True)
+    for f in F:
+        if f.absolute:
+            out[f.i, f.j] = np.float32(f.delta)
+        else:
+            out[f.i, f.j] = np.float32(np.float64(out[f.i, f.j]) + float(f.delta))
+    return out
+
+
+def apply_and_reprobe(a64, b64, c32, F, seed: int, m: int, p: Params):
+    """Algorithm 2's apply step: write the records, then probe the repaired C once more with a
+    fresh hash round (round 0 of `seed`) at the probe's m.  Returns (repaired C, probe result);
+    when the probe fires the caller recomputes C = AB at FP32 (the GEMM is the caller's)."""
+    c2 = apply_records(c32, F)
+    n1, n3 = c2.shape
+    res = probe(a64, b64, c2, make_round(seed, 0, n1, n3, m), p)
+    return c2, res
