@@ -150,6 +150,20 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* ctx, const void* A, const void* 
                                   fpsketch_dtype c_dtype, uint64_t seed, int32_t sigma_from_probe,
                                   fpsketch_fault* out, int32_t cap, int32_t* n_out, void* stream);
 
+/* Algorithm 2, apply step: writes the n records `recs` (a HOST array, as fpsketch_localize
+ * returns them) into the device product C (n1 x n3 FP32, row-major), then probes the repaired
+ * C once more with a fresh hash round.  Record (i, j, delta, absolute): C_ij <- delta when
+ * absolute is 1 (the recomputed value of a non-finite or out-of-range entry), else
+ * C_ij <- C_ij + delta, the sum formed in FP64 and rounded once to FP32.  The re-probe uses hash
+ * round 0 of `seed` at the probe's m (pass a seed not used for this C before); it leaves the
+ * context's probe statistics and noise average untouched.  *still_dirty = 1 when the re-probe
+ * fires: the paper then recomputes C = AB at FP32, which is the caller's GEMM.  Synchronous on
+ * `stream`.  C is modified.  FPSK_EINVAL for null pointers, n < 0, a coordinate outside C or a
+ * coordinate listed twice; FPSK_EDTYPE unless c_dtype is FPSK_F32. */
+fpsketch_status fpsketch_apply(fpsketch_ctx* ctx, const void* A, const void* B, void* C,
+                               fpsketch_dtype c_dtype, const fpsketch_fault* recs, int32_t n,
+                               uint64_t seed, int32_t* still_dirty, void* stream);
+
 /* Probe recalibration (Sec. III-G).  Synchronous.  sigma_bar = mean sigma_hat over the clean
  * probes since the last rebuild; B1 = max(n1, n3) sigma_bar / rms-hat(C);
  * m' = max(m_comb, 16, min(ceil(m B1 / B*), m_max)).  If m' lies outside [m/1.25, 1.25 m] the

@@ -588,6 +588,8 @@ struct fpsketch_ctx {
       patch_val, rc_coords, rc_gamma, rc_abs, rc_c;
   // localize rounds on the device: selection state and histogram, peel list, candidates
   DevBuf sel_state, sel_hist, peel_list, cands, cand_count;
+  // apply step: the record list and the re-probe's statistics and scratch noise sum
+  DevBuf apply_list, reprobe_stats, reprobe_acc;
   fpsketch_plan_info last_plan{};
 
   // optional per-probe events: start and end of the stream kernel, of the product dispatches
@@ -622,7 +624,8 @@ fpsketch_status set_device(const fpsketch_ctx* c) {
 fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const void* A,
                          const void* B, const float* Cm, bool mom, int mode, int32_t* d_dirty,
                          const int32_t* prow, const int32_t* pcol, const float* pval,
-                         hipStream_t st, hipEvent_t* ev = nullptr) {
+                         hipStream_t st, hipEvent_t* ev = nullptr,
+                         double* stats_out = nullptr, double* sigma_acc_out = nullptr) {
   const Decomp& d = W.d;
   fpsk::StreamArgs s{};
   s.A = static_cast<const uint16_t*>(A);
@@ -701,9 +704,10 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   a.maxpart = s.maxpart;
   a.nA = d.nA;
   a.nB = s.nB;
-  a.stats = as<double>(c->stats);
+  // the decision's outputs: the context's probe statistics and noise average unless redirected
+  a.stats = stats_out != nullptr ? stats_out : as<double>(c->stats);
   a.d_dirty = d_dirty;
-  a.sigma_acc = as<double>(c->sigma_acc);
+  a.sigma_acc = sigma_acc_out != nullptr ? sigma_acc_out : as<double>(c->sigma_acc);
   a.mu = c->p.mu;
   a.c_valid = c->p.c_valid;
   const double mmd = static_cast<double>(d.m) * d.m;
@@ -1076,7 +1080,8 @@ void fpsketch_destroy(fpsketch_ctx* c) {
   for (DevBuf* b : {&c->stats, &c->sigma_acc, &c->zero, &c->scan_counts, &c->scan_rows, &c->scan_base,
                     &c->scan_out, &c->samples, &c->patch_rowptr, &c->patch_col, &c->patch_val,
                     &c->rc_coords, &c->rc_gamma, &c->rc_abs, &c->rc_c, &c->sel_state,
-                    &c->sel_hist, &c->peel_list, &c->cands, &c->cand_count}) {
+                    &c->sel_hist, &c->peel_list, &c->cands, &c->cand_count, &c->apply_list,
+                    &c->reprobe_stats, &c->reprobe_acc}) {
     dev_free(*b);
   }
   delete c;
@@ -1212,6 +1217,52 @@ fpsketch_status fpsketch_recheck(fpsketch_ctx* c, const void* A, const void* B,
   FPSK_HIP(hipMemcpyAsync(gamma, c->rc_gamma.p, nn * sizeof(double), hipMemcpyDeviceToHost, st));
   FPSK_HIP(hipMemcpyAsync(abssum, c->rc_abs.p, nn * sizeof(double), hipMemcpyDeviceToHost, st));
   FPSK_HIP(hipStreamSynchronize(st));
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_apply(fpsketch_ctx* c, const void* A, const void* B, void* C,
+                               fpsketch_dtype c_dtype, const fpsketch_fault* recs, int32_t n,
+                               uint64_t seed, int32_t* still_dirty, void* stream) {
+  FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
+  if (still_dirty == nullptr || n < 0 || (n > 0 && recs == nullptr)) {
+    return fail(FPSK_EINVAL, "null argument or negative record count");
+  }
+  std::vector<fpsk::ApplyEntry> list(static_cast<size_t>(n));
+  std::unordered_set<int64_t> seen;
+  for (int32_t t = 0; t < n; ++t) {
+    const fpsketch_fault& f = recs[t];
+    if (f.i < 0 || f.i >= c->n1 || f.j < 0 || f.j >= c->n3) {
+      return fail(FPSK_EINVAL, "record outside C");
+    }
+    const int64_t o = f.i * c->n3 + f.j;
+    if (!seen.insert(o).second) return fail(FPSK_EINVAL, "record coordinate listed twice");
+    list[t] = {o, f.delta, f.absolute ? 1 : 0, 0};
+  }
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  float* Cm = static_cast<float*>(C);
+  if (n > 0) {
+    FPSK_TRY(dev_alloc(c->apply_list, list.size() * sizeof(fpsk::ApplyEntry)));
+    FPSK_HIP(hipMemcpyAsync(c->apply_list.p, list.data(), list.size() * sizeof(fpsk::ApplyEntry),
+                            hipMemcpyHostToDevice, st));
+    FPSK_HIP(fpsk::launch_apply(Cm, as<fpsk::ApplyEntry>(c->apply_list), n, st));
+  }
+  // re-probe with a fresh round at the probe's m; its statistics go to buffers of their own
+  const int m = c->m;
+  const Decomp d = decompose(c->n1, c->n2, c->n3, m, false);
+  HostRound HR;
+  build_round(seed, 0, c->n1, c->n3, m, d.cwb, false, HR, true);
+  FPSK_TRY(upload_round(HR, d.cwb, c->aux_round, st));
+  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, false));
+  FPSK_TRY(dev_alloc(c->reprobe_stats, 8 * sizeof(double)));
+  FPSK_TRY(dev_alloc(c->reprobe_acc, 2 * sizeof(double)));
+  FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, Cm, false, 1, nullptr, nullptr, nullptr,
+                    nullptr, st, nullptr, as<double>(c->reprobe_stats),
+                    as<double>(c->reprobe_acc)));
+  double stt[8];
+  FPSK_HIP(hipMemcpyAsync(stt, c->reprobe_stats.p, sizeof(stt), hipMemcpyDeviceToHost, st));
+  FPSK_HIP(hipStreamSynchronize(st));
+  *still_dirty = stt[5] != 0.0 ? 1 : 0;
   return FPSK_OK;
 }
 

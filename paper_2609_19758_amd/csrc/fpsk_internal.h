@@ -135,6 +135,13 @@ struct PeelEntry {     // S[o] -= ds, R[o] -= dr, T[o] -= dt
   int64_t o;
   double ds, dr, dt;
 };
+struct ApplyEntry {    // one record of the apply step: C[o] <- d, or C[o] + d
+  int64_t o;
+  double d;
+  int32_t absolute;
+  int32_t pad;
+};
+hipError_t launch_apply(float* C, const ApplyEntry* list, int n, hipStream_t st);
 struct Cand {          // a bucket above the cut with its three sketches
   int64_t o;
   double s, r, t;

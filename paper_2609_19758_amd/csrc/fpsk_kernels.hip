@@ -800,6 +800,16 @@ __global__ __launch_bounds__(1) void peel_kernel(double* S, double* R, double* T
   }
 }
 
+// Apply step of Algorithm 2: one thread per record (the coordinates are distinct).
+__global__ __launch_bounds__(kThreads) void apply_kernel(float* C, const ApplyEntry* list,
+                                                         int n) {
+  const int t = static_cast<int>(blockIdx.x) * kThreads + static_cast<int>(threadIdx.x);
+  if (t >= n) return;
+  const ApplyEntry e = list[t];
+  C[e.o] = e.absolute ? static_cast<float>(e.d)
+                      : static_cast<float>(static_cast<double>(C[e.o]) + e.d);
+}
+
 __global__ __launch_bounds__(kThreads) void above_kernel(const double* S, const double* R,
                                                          const double* T, int64_t n, double cut,
                                                          Cand* out, uint32_t cap,
@@ -972,6 +982,13 @@ hipError_t launch_median_mad(const double* S, int64_t n, SelState* st, uint32_t*
   if (n <= 0) return hipErrorInvalidValue;
   select_median<0>(S, n, st, hist, s);
   select_median<1>(S, n, st, hist, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_apply(float* C, const ApplyEntry* list, int n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(apply_kernel, dim3((n + kThreads - 1) / kThreads), dim3(kThreads), 0, st, C,
+                     list, n);
   return hipGetLastError();
 }
 

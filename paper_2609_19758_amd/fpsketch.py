@@ -63,6 +63,8 @@ _SIGS = {
     "fpsketch_probe": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_localize": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _U64, _I32,
                                          ctypes.POINTER(Fault), _I32, ctypes.POINTER(_I32), _P]),
+    "fpsketch_apply": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, ctypes.POINTER(Fault), _I32,
+                                      _U64, ctypes.POINTER(_I32), _P]),
     "fpsketch_calibrate_noise": (ctypes.c_int, [_P, _P, ctypes.c_int, _P, ctypes.POINTER(_I32),
                                                 ctypes.POINTER(_D), ctypes.POINTER(_I32)]),
     "fpsketch_get_plan": (ctypes.c_int, [_P, ctypes.POINTER(PlanInfo)]),
@@ -277,6 +279,26 @@ class Verifier:
         recs = [(buf[t].i, buf[t].j, buf[t].delta, bool(buf[t].absolute), buf[t].round)
                 for t in range(min(n.value, cap))]
         return recs, n.value, st
+
+    def apply_status(self, A, B, C, recs, seed: int, stream=None, c_dtype=None):
+        """Raw status and still-dirty flag of fpsketch_apply (records as localize returns them:
+        (i, j, delta, absolute, round) tuples)."""
+        n = len(recs)
+        buf = (Fault * max(n, 1))()
+        for t, (i, j, d, ab, rnd) in enumerate(recs):
+            buf[t].i, buf[t].j, buf[t].delta = int(i), int(j), float(d)
+            buf[t].absolute, buf[t].round = int(bool(ab)), int(rnd)
+        dirty = _I32()
+        st = self.lib.fpsketch_apply(self.handle, _ptr(A), _ptr(B), _ptr(C), _c_dtype(C, c_dtype),
+                                     buf, n, seed, ctypes.byref(dirty), _stream(stream))
+        return st, bool(dirty.value)
+
+    def apply(self, A, B, C, recs, seed: int, stream=None, c_dtype=None) -> bool:
+        """Writes the records into C and re-probes with hash round 0 of `seed`; True when the
+        re-probe still fires (the caller then recomputes C)."""
+        st, dirty = self.apply_status(A, B, C, recs, seed, stream, c_dtype)
+        _check(st, "fpsketch_apply")
+        return dirty
 
     def timing(self, enable: bool):
         _check(self.lib.fpsketch_timing(self.handle, int(enable)), "fpsketch_timing")
