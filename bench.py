@@ -299,6 +299,8 @@ def main() -> int:
     # recovery on dirty calls
     injected = recovered = false_pos = above = 0
     loc_us = []
+    apply_us = []
+    reprobe_clean = recomputed = delivered_ok = 0
     for r in range(args.recovery_calls):
         A, B, C = sets[r % args.sets]
         unit = float(C.abs().double().mean().item())        # mean |C_ij| of the clean product
@@ -333,9 +335,32 @@ def main() -> int:
         false_pos += len(got - {tuple(s) for s in sites.tolist()})
         if truth:
             assert int(flag.item()) == 1
-    recovery = recovered / above if above else float("nan")
-    log(f"recovery {recovered}/{above} above floor ({injected} injected), false positives "
-        f"{false_pos}, localize {np.median(loc_us) / 1e3:.2f} ms median")
+        # apply the records and re-probe with a fresh round; a firing re-probe falls back to
+        # recomputing the product (the caller's GEMM)
+        torch.cuda.synchronize()
+        ta = time.perf_counter()
+        still = v.apply(A, B, Cf, recs, seed=4000 + r)
+        apply_us.append((time.perf_counter() - ta) * 1e6)
+        if still:
+            recomputed += 1
+            Cf = gemm_f32(A, B)
+        else:
+            reprobe_clean += 1
+        # delivered correct: every injected site within its validation bound of the recomputed
+        # entry (the bound a clean GEMM entry satisfies)
+        g2, ab2 = v.recheck(A, B, sites)
+        vals2 = Cf[torch.from_numpy(sites[:, 0].copy()).cuda(),
+                   torch.from_numpy(sites[:, 1].copy()).cuda()].cpu().numpy() if len(sites) \
+            else np.zeros(0, dtype=np.float32)
+        ok = all(math.isfinite(float(x)) and abs(gi - float(x)) <= 100 * 2.0 ** -23 * abi
+                 for gi, abi, x in zip(g2, ab2, vals2))
+        delivered_ok += int(ok)
+    recovery = recovered / above if above else None
+    if loc_us:
+        log(f"recovery {recovered}/{above} above floor ({injected} injected), false positives "
+            f"{false_pos}, localize {np.median(loc_us) / 1e3:.2f} ms median; apply + re-probe "
+            f"{np.median(apply_us) / 1e3:.2f} ms median, re-probe clean {reprobe_clean}, "
+            f"recomputed {recomputed}, delivered correct {delivered_ok}/{len(apply_us)}")
 
     if args.copy_calibration > 0:
         # a plain copy of known size, for scaling the HBM byte counters of the same run
@@ -368,7 +393,12 @@ def main() -> int:
         "gemm_us": round(gemm_us, 2),
         "recovery": {"rate": recovery, "recovered": recovered, "above_floor": above,
                      "injected": injected, "false_positives": false_pos,
-                     "localize_ms_median": round(float(np.median(loc_us)) / 1e3, 3)},
+                     "localize_ms_median": round(float(np.median(loc_us)) / 1e3, 3) if loc_us
+                     else None,
+                     "apply": {"calls": len(apply_us), "reprobe_clean": reprobe_clean,
+                               "recomputed": recomputed, "delivered_correct": delivered_ok,
+                               "apply_ms_median": round(float(np.median(apply_us)) / 1e3, 3)
+                               if apply_us else None}},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic_from_summary(w.name)},
