@@ -150,6 +150,20 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* ctx, const void* A, const void* 
                                   fpsketch_dtype c_dtype, uint64_t seed, int32_t sigma_from_probe,
                                   fpsketch_fault* out, int32_t cap, int32_t* n_out, void* stream);
 
+/* The B-side cache of the probe (Sec. III-C; Algorithm 2's probe keeps BH2^T of a weight):
+ * forms Q = B H2^T for the probe's current hash round and m, and max |B|, from the device weight
+ * B (n2 x n3, the context's half format, row-major) and keeps them in the context.  Enqueue only
+ * on `stream`; B is not referenced afterwards.  A rebuild at a new m (fpsketch_calibrate_noise)
+ * drops the cache.  FPSK_EINVAL for null arguments. */
+fpsketch_status fpsketch_cache_b(fpsketch_ctx* ctx, const void* B, void* stream);
+
+/* fpsketch_probe with the cached B side: streams A and C only and decides exactly as
+ * fpsketch_probe does on the B the cache was formed from (same statistics, bit for bit).
+ * Enqueue only.  FPSK_EINVAL when nothing is cached for the probe's current m; FPSK_EDTYPE
+ * unless c_dtype is FPSK_F32. */
+fpsketch_status fpsketch_probe_cached(fpsketch_ctx* ctx, const void* A, const void* C,
+                                      fpsketch_dtype c_dtype, int32_t* d_dirty, void* stream);
+
 /* Algorithm 2, apply step: writes the n records `recs` (a HOST array, as fpsketch_localize
  * returns them) into the device product C (n1 x n3 FP32, row-major), then probes the repaired
  * C once more with a fresh hash round.  Record (i, j, delta, absolute): C_ij <- delta when

@@ -590,6 +590,10 @@ struct fpsketch_ctx {
   DevBuf sel_state, sel_hist, peel_list, cands, cand_count;
   // apply step: the record list and the re-probe's statistics and scratch noise sum
   DevBuf apply_list, reprobe_stats, reprobe_acc;
+  // the B-side cache of the probe: Q = (B H2^T)^T for the probe's round at m = qcache_m
+  // (0: nothing cached) and the per-work-group max |B|
+  DevBuf qcache, maxb_cache;
+  int qcache_m = 0;
   fpsketch_plan_info last_plan{};
 
   // optional per-probe events: start and end of the stream kernel, of the product dispatches
@@ -620,12 +624,17 @@ fpsketch_status set_device(const fpsketch_ctx* c) {
   return FPSK_OK;
 }
 
+// How a pass treats the B side: streamed, only filled into the context's cache (no product),
+// or taken from that cache (A and C streamed).
+enum class BSide { kStream, kFillCache, kUseCache };
+
 // One sketch pass (stream + product) on `st`.
 fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const void* A,
                          const void* B, const float* Cm, bool mom, int mode, int32_t* d_dirty,
                          const int32_t* prow, const int32_t* pcol, const float* pval,
                          hipStream_t st, hipEvent_t* ev = nullptr,
-                         double* stats_out = nullptr, double* sigma_acc_out = nullptr) {
+                         double* stats_out = nullptr, double* sigma_acc_out = nullptr,
+                         BSide bside = BSide::kStream) {
   const Decomp& d = W.d;
   fpsk::StreamArgs s{};
   s.A = static_cast<const uint16_t*>(A);
@@ -678,6 +687,17 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
     return fail(FPSK_EINVAL, "internal: tables do not match the pass");
   }
   s.ldp = d.ldp;
+  if (bside == BSide::kFillCache) {
+    // B work-groups only, into the cache (Q and the per-work-group max |B|)
+    s.nA = 0;
+    s.nC = 0;
+    s.Q = as<float>(c->qcache);
+    s.maxpart = as<float>(c->maxb_cache);
+    FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, false, d.rb, d.g, d.ng,
+                                 d.lds_stream, st));
+    return FPSK_OK;
+  }
+  if (bside == BSide::kUseCache) s.nB = 0;
 
   fpsk::ProductArgs a{};
   a.P = s.P;
@@ -703,7 +723,11 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   a.mode = mode;
   a.maxpart = s.maxpart;
   a.nA = d.nA;
-  a.nB = s.nB;
+  a.nB = d.nB;
+  if (bside == BSide::kUseCache) {
+    a.Q = as<float>(c->qcache);
+    a.maxpart_b = as<float>(c->maxb_cache);
+  }
   // the decision's outputs: the context's probe statistics and noise average unless redirected
   a.stats = stats_out != nullptr ? stats_out : as<double>(c->stats);
   a.d_dirty = d_dirty;
@@ -740,6 +764,7 @@ fpsketch_status build_probe(fpsketch_ctx* c, int m, hipStream_t st) {
   FPSK_TRY(upload_round(R, d.cwb, c->probe_round, st));
   FPSK_TRY(ensure_workspace(c->probe_ws, c->n1, c->n2, c->n3, m, false));
   c->m = m;
+  c->qcache_m = 0;      // a cached B side belongs to the previous round
   return FPSK_OK;
 }
 
@@ -1081,7 +1106,7 @@ void fpsketch_destroy(fpsketch_ctx* c) {
                     &c->scan_out, &c->samples, &c->patch_rowptr, &c->patch_col, &c->patch_val,
                     &c->rc_coords, &c->rc_gamma, &c->rc_abs, &c->rc_c, &c->sel_state,
                     &c->sel_hist, &c->peel_list, &c->cands, &c->cand_count, &c->apply_list,
-                    &c->reprobe_stats, &c->reprobe_acc}) {
+                    &c->reprobe_stats, &c->reprobe_acc, &c->qcache, &c->maxb_cache}) {
     dev_free(*b);
   }
   delete c;
@@ -1104,6 +1129,45 @@ fpsketch_status fpsketch_probe(fpsketch_ctx* c, const void* A, const void* B, co
   }
   return run_pass(c, c->probe_round, c->probe_ws, A, B, static_cast<const float*>(C), false, 1,
                   d_dirty, nullptr, nullptr, nullptr, st, ev);
+}
+
+fpsketch_status fpsketch_cache_b(fpsketch_ctx* c, const void* B, void* stream) {
+  if (c == nullptr || B == nullptr) return fail(FPSK_EINVAL, "null argument");
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const Decomp& d = c->probe_ws.d;
+  const size_t fm = static_cast<size_t>(c->m) * static_cast<size_t>(d.ldp) * sizeof(float);
+  FPSK_TRY(dev_alloc_zero(c->qcache, fm));
+  FPSK_TRY(dev_alloc(c->maxb_cache, static_cast<size_t>(d.nB) * sizeof(float)));
+  FPSK_TRY(run_pass(c, c->probe_round, c->probe_ws, c->zero.p, B, nullptr, false, 1, nullptr,
+                    nullptr, nullptr, nullptr, st, nullptr, nullptr, nullptr,
+                    BSide::kFillCache));
+  c->qcache_m = c->m;
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_probe_cached(fpsketch_ctx* c, const void* A, const void* C,
+                                      fpsketch_dtype c_dtype, int32_t* d_dirty, void* stream) {
+  if (c == nullptr) return fail(FPSK_EINVAL, "null context");
+  FPSK_TRY(check_matrices(c, A, c->zero.p, C, c_dtype));
+  if (c->qcache_m != c->m) {
+    return fail(FPSK_EINVAL, "no B side cached for the probe's current m (call fpsketch_cache_b)");
+  }
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  hipEvent_t* ev = nullptr;
+  if (c->timing) {
+    while (c->events.size() < c->events_used + 4) {
+      hipEvent_t e;
+      FPSK_HIP(hipEventCreate(&e));
+      c->events.push_back(e);
+    }
+    ev = c->events.data() + c->events_used;
+    c->events_used += 4;
+  }
+  return run_pass(c, c->probe_round, c->probe_ws, A, c->zero.p, static_cast<const float*>(C),
+                  false, 1, d_dirty, nullptr, nullptr, nullptr, st, ev, nullptr, nullptr,
+                  BSide::kUseCache);
 }
 
 fpsketch_status fpsketch_timing(fpsketch_ctx* c, int32_t enable) {

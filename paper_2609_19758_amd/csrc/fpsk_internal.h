@@ -87,6 +87,7 @@ struct ProductArgs {
   int mode;             // 0: sketch only; 1: probe decision
   const float* maxpart;
   int nA, nB;
+  const float* maxpart_b; // max |B| per B work-group when the B side is cached, else null
   double* stats;        // [8] sigma_hat, thr, tau, max|S|, finite, dirty, max|A|, max|B|
   int32_t* d_dirty;     // caller's flag (may be null)
   double* sigma_acc;    // [2] running sum of clean sigma_hat, count

@@ -234,8 +234,9 @@ __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArg
     acc0 = pa.sigma_acc[0];
     acc1 = pa.sigma_acc[1];
   }
+  const float* mb = pa.maxpart_b != nullptr ? pa.maxpart_b : pa.maxpart + pa.nA;
   float amax = t < pa.nA ? pa.maxpart[t] : 0.0f;
-  float bmax = t < pa.nB ? pa.maxpart[pa.nA + t] : 0.0f;
+  float bmax = t < pa.nB ? mb[t] : 0.0f;
   for (int sl = 1; sl < pa.xns; ++sl) {
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArg
     amax = fmaxf(amax, pa.maxpart[i]);
   }
   for (int i = t + kDecideThreads; i < pa.nB; i += kDecideThreads) {
-    bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
+    bmax = fmaxf(bmax, mb[i]);
   }
   double lsum = 0.0, lmax = 0.0, lbad = 0.0;
 #pragma unroll
@@ -596,7 +597,8 @@ __global__ __launch_bounds__(kDecideThreads) void tile_decide_kernel(ProductArgs
   }
   float amax = 0.0f, bmax = 0.0f;
   for (int i = t; i < pa.nA; i += kDecideThreads) amax = fmaxf(amax, pa.maxpart[i]);
-  for (int i = t; i < pa.nB; i += kDecideThreads) bmax = fmaxf(bmax, pa.maxpart[pa.nA + i]);
+  const float* mb = pa.maxpart_b != nullptr ? pa.maxpart_b : pa.maxpart + pa.nA;
+  for (int i = t; i < pa.nB; i += kDecideThreads) bmax = fmaxf(bmax, mb[i]);
   // sums: 0, 2; maxima: 1, 3, 4
   double r5[5] = {lsum, lmax, lbad, static_cast<double>(amax), static_cast<double>(bmax)};
   lds_reduce<kDecideThreads, 5>(r5, red, 0x1au);

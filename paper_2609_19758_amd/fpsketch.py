@@ -63,6 +63,8 @@ _SIGS = {
     "fpsketch_probe": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_localize": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _U64, _I32,
                                          ctypes.POINTER(Fault), _I32, ctypes.POINTER(_I32), _P]),
+    "fpsketch_cache_b": (ctypes.c_int, [_P, _P, _P]),
+    "fpsketch_probe_cached": (ctypes.c_int, [_P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_apply": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, ctypes.POINTER(Fault), _I32,
                                       _U64, ctypes.POINTER(_I32), _P]),
     "fpsketch_calibrate_noise": (ctypes.c_int, [_P, _P, ctypes.c_int, _P, ctypes.POINTER(_I32),
@@ -259,6 +261,18 @@ class Verifier:
 
     def probe(self, A, B, C, d_dirty=None, stream=None, c_dtype=None):
         _check(self.probe_status(A, B, C, d_dirty, stream, c_dtype), "fpsketch_probe")
+
+    def cache_b(self, B, stream=None):
+        """Forms and keeps the probe's B side (B H2^T and max|B|) for the current m."""
+        _check(self.lib.fpsketch_cache_b(self.handle, _ptr(B), _stream(stream)), "fpsketch_cache_b")
+
+    def probe_cached_status(self, A, C, d_dirty=None, stream=None, c_dtype=None) -> int:
+        return self.lib.fpsketch_probe_cached(self.handle, _ptr(A), _ptr(C), _c_dtype(C, c_dtype),
+                                              _ptr(d_dirty), _stream(stream))
+
+    def probe_cached(self, A, C, d_dirty=None, stream=None, c_dtype=None):
+        """fpsketch_probe with the cached B side (A and C streamed)."""
+        _check(self.probe_cached_status(A, C, d_dirty, stream, c_dtype), "fpsketch_probe_cached")
 
     def probe_stats(self, stream=None) -> dict:
         out = (_D * 8)()
