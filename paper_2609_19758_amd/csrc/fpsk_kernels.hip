@@ -112,8 +112,8 @@ __device__ void decide_tail(const ProductArgs& pa, double sum_abs, double max_ab
 //     k-contiguous, read with 16-byte loads that the work-groups of an XCD share through its L2);
 //     the 4 waves are combined in fixed order.  Slice 0 subtracts the C grid (the sum of the
 //     column-group partials).
-//   block_decide_kernel (one work-group): S = sum of the slice partials in slice order, the
-//     probe statistics and the verdict.
+//   block_decide_kernel (one work-group): S = sum of the slice partials in slice order (kept
+//     in registers, not stored), the probe statistics and the verdict.
 
 template <int XB>
 __global__ __launch_bounds__(kThreads) void block_product_kernel(ProductArgs pa) {
@@ -270,23 +270,24 @@ __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArg
   const double sum_abs = r5[0], max_abs = r5[1], nbad = r5[2];
   const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / static_cast<double>(mm);
   const double clip = 5.0 * mean_abs;
-  double c2 = 0.0;
+  // When no bucket reaches the clip (the usual clean case) the clipped sum is sum|S| itself:
+  // the same terms in the same order through the same reduction tree.  Otherwise a second pass.
+  double clipped = sum_abs;
+  if (!(nbad == 0.0 && max_abs <= clip)) {
+    double c2 = 0.0;
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
-    if (o < mm) {
-      const double a = fabs(v[q]);
-      c2 += a < clip ? a : clip;
+    for (int q = 0; q < NQ; ++q) {
+      const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
+      if (o < mm) {
+        const double a = fabs(v[q]);
+        c2 += a < clip ? a : clip;
+      }
     }
+    double r1[1] = {c2};
+    lds_reduce<kDecideThreads, 1>(r1, red, 0u);
+    clipped = r1[0];
   }
-  double r1[1] = {c2};
-  lds_reduce<kDecideThreads, 1>(r1, red, 0u);
-  if (threadIdx.x == 0) decide_tail(pa, sum_abs, max_abs, nbad, r1[0], r5[3], r5[4], acc0, acc1);
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
-    if (o < mm) pa.S[o] = v[q];
-  }
+  if (threadIdx.x == 0) decide_tail(pa, sum_abs, max_abs, nbad, clipped, r5[3], r5[4], acc0, acc1);
 }
 
 // ----------------------------------------------------------------------------------------
