@@ -48,6 +48,41 @@ def test_cached_probe_equals_streamed_probe(fk, n1, n2, n3, m, fmt):
     v.close()
 
 
+@pytest.mark.parametrize("n1,n2,n3,m,fmt", [
+    (512, 1000, 640, 40, "fp16"),     # two A tiles, the second ragged
+    (300, 1537, 200, 64, "bf16"),     # four A tiles, one column in the last; largest block m
+])
+def test_cached_block_probe_matches_oracle(fk, n1, n2, n3, m, fmt):
+    """The cached probe on the block path (m <= 64) across several 512-column A tiles, the last
+    ragged, against the oracle's probe: verdicts, tau and max|A|, max|B| exact, max|S|
+    within the FP32-storage bound of the factors, sigma-hat within the 5 % the streamed probe's
+    parity test allows (both measure noise that the FP32 factors add to)."""
+    import torch
+    a_bits, b_bits = wl.gen_operands(n1, n2, n3, fmt, ("normal", 1.0), ("normal", 0.02), 83)
+    A, B = to_dev_half(a_bits, fmt), to_dev_half(b_bits, fmt)
+    c = gemm_f32(A, B).cpu().numpy()
+    a64, b64 = o.decode(a_bits, fmt), o.decode(b_bits, fmt)
+    v = fk.Verifier(n1, n2, n3, fmt, m=m)
+    v.cache_b(B)
+    hr = o.make_round(v.params.seed, 0, n1, n3, m)
+    P = o.Params()
+    sites = wl.fault_sites(n1, n3, 3, 84)
+    dirty_c = wl.inject_additive(c, sites, wl.fault_magnitudes(3, 0.5, 2.0, wl.mean_abs(c), 85))
+    for cc, expect_dirty in ((c, False), (dirty_c, True)):
+        flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+        v.probe_cached(A, to_dev_f32(cc), d_dirty=flag)
+        st = v.probe_stats()
+        ref = o.probe(a64, b64, cc, hr, P)
+        assert bool(st["dirty"]) == ref.dirty == expect_dirty
+        assert int(flag.item()) == int(expect_dirty)
+        assert abs(st["tau"] / ref.tau - 1) < 1e-12
+        assert st["max_a"] == float(np.abs(a64).max()) and st["max_b"] == float(np.abs(b64).max())
+        DS, _, _ = o.abs_contributions(a64, b64, cc.astype(np.float64), hr)
+        assert abs(st["max_abs"] - ref.max_abs) <= 2.0 ** -20 * DS.max()
+        assert abs(st["sigma_hat"] / ref.sigma_hat - 1) < 0.05
+    v.close()
+
+
 def test_cached_weight_with_rotating_activations(fk):
     """One cached weight, several activation matrices: every verdict and statistic equals the
     streamed probe's, clean and dirty."""
