@@ -296,6 +296,31 @@ def main() -> int:
     p_us = prod_ms * 1e3 / ncalls
     log(f"stream kernel {k_us:.2f} us, product+decide {p_us:.2f} us (event-timed)")
 
+    # the same probe calls captured in a HIP graph (the probe only enqueues kernels): one graph of
+    # 5 rounds over the buffer sets, replayed to the same number of calls
+    per_graph = 5 * args.sets
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(stream)
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            for k in range(per_graph):
+                A, B, C = sets[k % args.sets]
+                v.probe(A, B, C, d_dirty=flag)
+    torch.cuda.synchronize()
+    replays = max(1, args.steps // per_graph)
+    g.replay()
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(replays):
+        g.replay()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    graph_us = t0.elapsed_time(t1) * 1e3 / (replays * per_graph)
+    assert int(flag.item()) == 0, "a clean call was reported dirty (graph replay)"
+    log(f"probe in a HIP graph: {graph_us:.2f} us/call ({replays} replays of {per_graph} calls)")
+    del g
+
     # the probe with the B side cached (the paper's probe keeps BH2^T of the weight): one weight,
     # the activations of every buffer set, their products C = A_k B_0; A and C streamed
     B0 = sets[0][1]
@@ -419,6 +444,8 @@ def main() -> int:
         "us_per_call": round(ms_per * 1e3, 3),
         "kernel_us": {"stream": round(k_us, 3), "product_decide": round(p_us, 3)},
         "gemm_us": round(gemm_us, 2),
+        "graph": {"us_per_call": round(graph_us, 3), "calls_per_graph": per_graph,
+                  "replays": replays},
         "b_cached": {"us_per_call": round(cached_us, 3), "bytes_per_call": bytes_ac,
                      "gbs_a_c": round(bytes_ac / cached_us / 1e3, 1),
                      "stream_us": round(cs_ms * 1e3 / cn, 3),
