@@ -59,7 +59,9 @@ typedef struct {
   int32_t s_budget;   /* declared error budget s (16) */
   int32_t delta_rc;   /* errors per row or column Delta (8) */
   int32_t k_cap;      /* candidate cap K per round; 0 = max(64, 8 s) (Sec. III-E) */
-  int32_t reserved;   /* must be 0 */
+  int32_t b_layout;   /* 0: B is n2 x n3 row-major (C = A B); 1: B is passed as W = B^T,
+                         n3 x n2 row-major (a linear layer's weight, C = A W^T); every call
+                         of the context then takes W where it takes B */
   double rho_min;     /* smallest fault magnitude to localize, x rms(C) (0.02, Sec. III-G) */
   double mu;          /* probe margin (4, Sec. III-E) */
   double c_valid;     /* validation constant c (100, Sec. III-D) */

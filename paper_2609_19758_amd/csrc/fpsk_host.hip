@@ -229,6 +229,10 @@ struct HostRound {
   std::vector<int32_t> perm, coff, boff;
   std::vector<uint16_t> ctab, btab;
   std::vector<uint8_t> bsign;
+  // B passed transposed: the column lists of each bucket (j | (v2 < 0) << 31, ascending,
+  // padded to cap2 with -1), natural bucket order (the C grid's column order)
+  int cap2 = 0;
+  std::vector<int32_t> perm2;
 };
 
 // Bucket segments are padded to a multiple of 8 for m <= 256 (the kernels then fold 8 list
@@ -291,7 +295,7 @@ void build_col_tables(const std::vector<int32_t>& h2, const std::vector<int8_t>&
 // The sketch rows then come out in that order; only the probe, whose statistics do not depend
 // on the numbering of the buckets, uses it.
 void build_round(uint64_t seed, int round, int64_t n1, int64_t n3, int m, int64_t cwb, bool mom,
-                 HostRound& R, bool size_order = false) {
+                 bool transb, HostRound& R, bool size_order = false) {
   R.m = m;
   R.mom = mom;
   R.h1.resize(n1);
@@ -321,6 +325,21 @@ void build_round(uint64_t seed, int round, int64_t n1, int64_t n3, int m, int64_
   }
   build_col_tables(R.h2, R.v2, m, kColTile, 0, R.ctab, R.coff);
   build_col_tables(R.h2, R.v2, m, cwb, mom ? 1 : 2, R.btab, R.boff);
+  if (transb) {
+    std::vector<int32_t> c2(static_cast<size_t>(m), 0);
+    for (int64_t j = 0; j < n3; ++j) c2[R.h2[j]]++;
+    R.cap2 = std::max(1, *std::max_element(c2.begin(), c2.end()));
+    R.perm2.assign(static_cast<size_t>(m) * R.cap2, -1);
+    std::fill(c2.begin(), c2.end(), 0);
+    for (int64_t j = 0; j < n3; ++j) {
+      const int b = R.h2[j];
+      R.perm2[static_cast<size_t>(b) * R.cap2 + c2[b]++] =
+          static_cast<int32_t>(static_cast<uint32_t>(j) | (R.v2[j] < 0 ? 0x80000000u : 0u));
+    }
+  } else {
+    R.cap2 = 0;
+    R.perm2.clear();
+  }
   // column signs as bits, padded to whole B chunks
   const int64_t TB = (n3 + cwb - 1) / cwb;
   R.bsign.assign(static_cast<size_t>(TB * cwb / 8), 0);
@@ -386,7 +405,7 @@ struct Decomp {
   int xsr = 1, xsc = 1, xnstc = 1, xslots = 0;   // supertiles of blocks (XCD-local sets)
 };
 
-Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
+Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool transb) {
   (void)n1;
   Decomp d;
   d.m = m;
@@ -410,6 +429,8 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom) {
   d.cwb = fpsk::kBChunkHalfs / d.rb;
   d.TB = static_cast<int>((n3 + d.cwb - 1) / d.cwb);
   d.nB = static_cast<int>((n2 + d.rb - 1) / d.rb);
+  // B passed transposed: row-bucket work-groups over the rows of W = B^T, as many as A's
+  if (transb) d.nB = m * d.TA;
   d.TC = static_cast<int>((n3 + kColTile - 1) / kColTile);
   int npc = static_cast<int>((1024 + m - 1) / m);
   npc = std::max(1, std::min(npc, d.TC));
@@ -484,7 +505,8 @@ struct DevRound {
   int cap = 0;
   bool mom = false;
   int64_t cwb = 0;
-  DevBuf perm, ctab, coff, btab, boff, bsign;
+  int cap2 = 0;
+  DevBuf perm, ctab, coff, btab, boff, bsign, perm2;
 };
 
 fpsketch_status upload_round(const HostRound& R, int64_t cwb, DevRound& D, hipStream_t st) {
@@ -503,6 +525,8 @@ fpsketch_status upload_round(const HostRound& R, int64_t cwb, DevRound& D, hipSt
   FPSK_TRY(up(D.coff, R.coff.data(), R.coff.size() * 4));
   FPSK_TRY(up(D.btab, R.btab.data(), R.btab.size() * 2));
   FPSK_TRY(up(D.boff, R.boff.data(), R.boff.size() * 4));
+  D.cap2 = R.cap2;
+  if (!R.perm2.empty()) FPSK_TRY(up(D.perm2, R.perm2.data(), R.perm2.size() * 4));
   // host vectors must outlive the asynchronous copies
   FPSK_HIP(hipStreamSynchronize(st));
   return FPSK_OK;
@@ -515,6 +539,7 @@ void free_round(DevRound& D) {
   dev_free(D.coff);
   dev_free(D.btab);
   dev_free(D.boff);
+  dev_free(D.perm2);
 }
 
 struct Workspace {
@@ -525,8 +550,8 @@ struct Workspace {
 };
 
 fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n3, int m,
-                                 bool mom) {
-  const Decomp d = decompose(n1, n2, n3, m, mom);
+                                 bool mom, bool transb) {
+  const Decomp d = decompose(n1, n2, n3, m, mom, transb);
   W.d = d;
   W.mom = mom;
   // factor rows are ldp long; the padding past n2 is never written and stays zero
@@ -570,6 +595,7 @@ void free_workspace(Workspace& W) {
 struct fpsketch_ctx {
   int64_t n1 = 0, n2 = 0, n3 = 0;
   fpsketch_dtype dt = FPSK_BF16;
+  bool transb = false;        // B passed as W = B^T (p.b_layout == 1)
   fpsketch_params p{};
   int device = 0;
   int m = 0;
@@ -609,7 +635,7 @@ bool valid_half(fpsketch_dtype d) { return d == FPSK_F16 || d == FPSK_BF16; }
 fpsketch_status check_params(const fpsketch_params& p) {
   if (p.m < 0 || p.rounds < 1 || p.r_star < 0 || p.r_max < 0 || p.s_budget < 1 ||
       p.delta_rc < 1 || p.k_cap < 0 || !(p.rho_min > 0) || !(p.mu > 0) || !(p.c_valid > 0) ||
-      !(p.b_star > 0) || !(p.c_coll > 0)) {
+      !(p.b_star > 0) || !(p.c_coll > 0) || (p.b_layout != 0 && p.b_layout != 1)) {
     return fail(FPSK_EINVAL, "parameter out of range");
   }
   return FPSK_OK;
@@ -646,6 +672,9 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   s.m = d.m;
   s.perm = static_cast<const int32_t*>(R.perm.p);
   s.cap = R.cap;
+  s.transb = c->transb ? 1 : 0;
+  s.perm2 = static_cast<const int32_t*>(R.perm2.p);
+  s.cap2 = R.cap2;
   s.bsign = static_cast<const uint8_t*>(R.bsign.p);
   s.ctab = static_cast<const uint16_t*>(R.ctab.p);
   s.coff = static_cast<const int32_t*>(R.coff.p);
@@ -678,12 +707,13 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   s.inv_l3 = c->inv_l3;
   auto aligned16 = [](const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; };
   s.vec_a = (c->n2 % 8 == 0) && aligned16(A);
-  s.vec_b = (c->n3 % 8 == 0) && aligned16(B);
+  // B as stored: rows of n3; transposed: rows of W, n2 long
+  s.vec_b = ((c->transb ? c->n2 : c->n3) % 8 == 0) && aligned16(B);
   s.vec_c = (c->n3 % 4 == 0) && aligned16(Cm);
   // the vector path loads whole 8-element groups: every row length must be a multiple of 8
   if (c->n2 % 8 != 0 || c->n3 % 8 != 0) s.vec_a = s.vec_b = s.vec_c = 0;
   s.zero = c->zero.p;
-  if (R.cwb != d.cwb || R.m != d.m || R.mom != mom) {
+  if (R.cwb != d.cwb || R.m != d.m || R.mom != mom || (c->transb && R.perm2.p == nullptr)) {
     return fail(FPSK_EINVAL, "internal: tables do not match the pass");
   }
   s.ldp = d.ldp;
@@ -759,10 +789,10 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
 
 fpsketch_status build_probe(fpsketch_ctx* c, int m, hipStream_t st) {
   HostRound R;
-  const Decomp d = decompose(c->n1, c->n2, c->n3, m, false);
-  build_round(c->p.seed, 0, c->n1, c->n3, m, d.cwb, false, R, true);
+  const Decomp d = decompose(c->n1, c->n2, c->n3, m, false, c->transb);
+  build_round(c->p.seed, 0, c->n1, c->n3, m, d.cwb, false, c->transb, R, true);
   FPSK_TRY(upload_round(R, d.cwb, c->probe_round, st));
-  FPSK_TRY(ensure_workspace(c->probe_ws, c->n1, c->n2, c->n3, m, false));
+  FPSK_TRY(ensure_workspace(c->probe_ws, c->n1, c->n2, c->n3, m, false, c->transb));
   c->m = m;
   c->qcache_m = 0;      // a cached B side belongs to the previous round
   return FPSK_OK;
@@ -810,6 +840,7 @@ fpsketch_status recheck_coords(fpsketch_ctx* c, const void* A, const void* B, co
   FPSK_HIP(hipMemcpyAsync(c->rc_coords.p, coords.data(), coords.size() * sizeof(int64_t),
                           hipMemcpyHostToDevice, st));
   FPSK_HIP(fpsk::launch_recheck(static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B),
+                                c->transb ? 1 : c->n3, c->transb ? c->n2 : 1,
                                 C, c->n2, c->n3, c->dt == FPSK_BF16 ? 1 : 0,
                                 as<int64_t>(c->rc_coords), n, as<double>(c->rc_gamma),
                                 as<double>(c->rc_abs), as<float>(c->rc_c), st));
@@ -867,10 +898,10 @@ fpsketch_status sketch_round(fpsketch_ctx* c, uint64_t seed, int round, int m, b
                              const int32_t* pcol, const float* pval, hipStream_t st,
                              HostRound& HR, std::vector<double>& S, std::vector<double>& Rm,
                              std::vector<double>& T, double* maxA, double* maxB) {
-  const Decomp d = decompose(c->n1, c->n2, c->n3, m, mom);
-  build_round(seed, round, c->n1, c->n3, m, d.cwb, mom, HR);
+  const Decomp d = decompose(c->n1, c->n2, c->n3, m, mom, c->transb);
+  build_round(seed, round, c->n1, c->n3, m, d.cwb, mom, c->transb, HR);
   FPSK_TRY(upload_round(HR, d.cwb, c->aux_round, st));
-  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, mom));
+  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, mom, c->transb));
   FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, C, mom, 0, nullptr, prow, pcol, pval, st));
   const size_t mm = static_cast<size_t>(m) * static_cast<size_t>(m);
   S.resize(mm);
@@ -901,10 +932,10 @@ fpsketch_status sketch_round_device(fpsketch_ctx* c, uint64_t seed, int round, i
                                     const void* A, const void* B, const float* C,
                                     const int32_t* prow, const int32_t* pcol, const float* pval,
                                     hipStream_t st, HostRound& HR, double* maxA, double* maxB) {
-  const Decomp d = decompose(c->n1, c->n2, c->n3, m, mom);
-  build_round(seed, round, c->n1, c->n3, m, d.cwb, mom, HR);
+  const Decomp d = decompose(c->n1, c->n2, c->n3, m, mom, c->transb);
+  build_round(seed, round, c->n1, c->n3, m, d.cwb, mom, c->transb, HR);
   FPSK_TRY(upload_round(HR, d.cwb, c->aux_round, st));
-  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, mom));
+  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, mom, c->transb));
   FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, C, mom, 0, nullptr, prow, pcol, pval, st));
   std::vector<float> mp(static_cast<size_t>(d.nA + d.nB));
   FPSK_HIP(hipMemcpyAsync(mp.data(), c->aux_ws.maxpart.p, mp.size() * sizeof(float),
@@ -1069,6 +1100,7 @@ fpsketch_status fpsketch_create(int64_t n1, int64_t n2, int64_t n3, fpsketch_dty
   c->n2 = n2;
   c->n3 = n3;
   c->dt = ab_dtype;
+  c->transb = p.b_layout == 1;
   c->p = p;
   c->device = dev;
   c->L1 = pow2_ceil(n1);
@@ -1275,6 +1307,7 @@ fpsketch_status fpsketch_recheck(fpsketch_ctx* c, const void* A, const void* B,
                           hipMemcpyHostToDevice, st));
   // no C here: the kernel skips the C read when C is null
   FPSK_HIP(fpsk::launch_recheck(static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B),
+                                c->transb ? 1 : c->n3, c->transb ? c->n2 : 1,
                                 nullptr, c->n2, c->n3, c->dt == FPSK_BF16 ? 1 : 0,
                                 as<int64_t>(c->rc_coords), n, as<double>(c->rc_gamma),
                                 as<double>(c->rc_abs), nullptr, st));
@@ -1313,11 +1346,11 @@ fpsketch_status fpsketch_apply(fpsketch_ctx* c, const void* A, const void* B, vo
   }
   // re-probe with a fresh round at the probe's m; its statistics go to buffers of their own
   const int m = c->m;
-  const Decomp d = decompose(c->n1, c->n2, c->n3, m, false);
+  const Decomp d = decompose(c->n1, c->n2, c->n3, m, false, c->transb);
   HostRound HR;
-  build_round(seed, 0, c->n1, c->n3, m, d.cwb, false, HR, true);
+  build_round(seed, 0, c->n1, c->n3, m, d.cwb, false, c->transb, HR, true);
   FPSK_TRY(upload_round(HR, d.cwb, c->aux_round, st));
-  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, false));
+  FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, false, c->transb));
   FPSK_TRY(dev_alloc(c->reprobe_stats, 8 * sizeof(double)));
   FPSK_TRY(dev_alloc(c->reprobe_acc, 2 * sizeof(double)));
   FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, Cm, false, 1, nullptr, nullptr, nullptr,

@@ -20,7 +20,7 @@ constexpr int kMaxXSlices = 4;           // n2 <= kMaxXSlices * kXSlice
 // One pass over A, B and C producing the factors of Eq. 1 (and their weighted forms).
 struct StreamArgs {
   const uint16_t* A;          // n1 x n2 half bits
-  const uint16_t* B;          // n2 x n3 half bits
+  const uint16_t* B;          // n2 x n3 half bits, or with transb its transpose W (n3 x n2)
   const float* C;             // n1 x n3
   int64_t n1, n2, n3;
   int m;
@@ -28,6 +28,12 @@ struct StreamArgs {
   // padded to cap entries with -1
   const int32_t* perm;
   int cap;
+  // transb: B is passed as W = B^T (n3 x n2 row-major) and the nB B work-groups are row-bucket
+  // work-groups over W's rows (m x TA of them, like A's), with the column lists perm2 / cap2
+  // (per bucket b its columns j ascending as j | (v2 < 0) << 31, natural bucket order)
+  int transb;
+  const int32_t* perm2;
+  int cap2;
   // C column tiles of kColTile: per tile (ctab_stride entries), columns sorted by bucket as
   // (offset in tile) | (v2 < 0) << 15, with coff[t * (m + 1) + b] segment starts; for m <= 256
   // each segment is padded to a multiple of 8 with the sentinel offset kColTile (a zero column)
@@ -117,9 +123,10 @@ hipError_t launch_scan_extract(const float* C, int64_t n3, const int32_t* rows,
                                hipStream_t st);
 hipError_t launch_sample(const float* C, int64_t stride, int64_t count, float* out,
                          hipStream_t st);
-hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, const float* C, int64_t n2,
-                          int64_t n3, int dt, const int64_t* coords, int n, double* gamma,
-                          double* abssum, float* cval, hipStream_t st);
+// B[k][j] is read at B + k * bsk + j * bsj (n3, 1 for B as stored; 1, n2 for W = B^T).
+hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, int64_t bsk, int64_t bsj,
+                          const float* C, int64_t n2, int64_t n3, int dt, const int64_t* coords,
+                          int n, double* gamma, double* abssum, float* cval, hipStream_t st);
 
 // Order statistics of a bucket grid on the device (the MAD and candidate scan of a localize
 // round).  The selection state lives in device memory.

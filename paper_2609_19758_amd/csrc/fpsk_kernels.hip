@@ -837,6 +837,7 @@ __global__ __launch_bounds__(kThreads) void sample_kernel(const float* C, int64_
 // accumulated in FP64, reduced across lanes in fixed butterfly order.
 template <int DT>
 __global__ __launch_bounds__(kThreads) void recheck_kernel(const uint16_t* A, const uint16_t* B,
+                                                           int64_t bsk, int64_t bsj,
                                                            const float* C, int64_t n2, int64_t n3,
                                                            const int64_t* coords, int n,
                                                            double* gamma, double* abssum,
@@ -848,7 +849,7 @@ __global__ __launch_bounds__(kThreads) void recheck_kernel(const uint16_t* A, co
   double g = 0.0, ab = 0.0;
   for (int64_t k = lane; k < n2; k += 64) {
     const double a = static_cast<double>(half_bits_to_float<DT>(A[i * n2 + k]));
-    const double b = static_cast<double>(half_bits_to_float<DT>(B[k * n3 + j]));
+    const double b = static_cast<double>(half_bits_to_float<DT>(B[k * bsk + j * bsj]));
     const double p = a * b;
     g += p;
     ab += fabs(p);
@@ -1002,17 +1003,17 @@ hipError_t launch_above(const double* S, const double* R, const double* T, int64
   return hipGetLastError();
 }
 
-hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, const float* C, int64_t n2,
-                          int64_t n3, int dt, const int64_t* coords, int n, double* gamma,
-                          double* abssum, float* cval, hipStream_t st) {
+hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, int64_t bsk, int64_t bsj,
+                          const float* C, int64_t n2, int64_t n3, int dt, const int64_t* coords,
+                          int n, double* gamma, double* abssum, float* cval, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   const unsigned grid = static_cast<unsigned>((n + 3) / 4);
   if (dt == 1) {
-    hipLaunchKernelGGL(recheck_kernel<1>, dim3(grid), dim3(kThreads), 0, st, A, B, C, n2, n3,
-                       coords, n, gamma, abssum, cval);
+    hipLaunchKernelGGL(recheck_kernel<1>, dim3(grid), dim3(kThreads), 0, st, A, B, bsk, bsj, C,
+                       n2, n3, coords, n, gamma, abssum, cval);
   } else {
-    hipLaunchKernelGGL(recheck_kernel<0>, dim3(grid), dim3(kThreads), 0, st, A, B, C, n2, n3,
-                       coords, n, gamma, abssum, cval);
+    hipLaunchKernelGGL(recheck_kernel<0>, dim3(grid), dim3(kThreads), 0, st, A, B, bsk, bsj, C,
+                       n2, n3, coords, n, gamma, abssum, cval);
   }
   return hipGetLastError();
 }

@@ -20,18 +20,40 @@ __device__ __forceinline__ int32_t row_entry(int32_t pe, int r) {
   return __builtin_amdgcn_readlane(pe, r);
 }
 
-// A work-group: bucket a, column tile t of A.  P[a, tile] = sum over the bucket's rows of
-// v1(i) A[i, tile] (and Pw with w_i).  Groups of 8 rows are summed in FP32 (their partial sums
+// A row-bucket side: a matrix with rows of n2 halfs whose rows are hashed into buckets.  The A
+// side (rows i of A, h1, v1, w_i) gives P and Pw; with B passed transposed (W = B^T, n3 x n2),
+// the rows j of W with h2, v2, w_j give Q = (B H2^T)^T and Qw directly, in the same layout.
+struct RowSide {
+  const uint16_t* X;       // rows x n2 half bits
+  const int32_t* perm;     // bucket lists (row | sign << 31), cap entries each
+  int cap;
+  double inv_l;            // 1 / 2^ceil(log2 rows)
+  float* out;              // m x ldp
+  float* outw;             // m x ldp (moments)
+  float* maxslot;          // max |X| per work-group (A: maxpart, W: after the nA A entries)
+};
+
+__device__ __forceinline__ RowSide a_side(const StreamArgs& s) {
+  return RowSide{s.A, s.perm, s.cap, s.inv_l1, s.P, s.Pw, s.maxpart};
+}
+
+__device__ __forceinline__ RowSide w_side(const StreamArgs& s) {
+  return RowSide{s.B, s.perm2, s.cap2, s.inv_l3, s.Q, s.Qw, s.maxpart + s.nA};
+}
+
+// Row-bucket work-group: bucket a, column tile t.  out[a, tile] = sum over the bucket's rows of
+// v(i) X[i, tile] (and outw with w_i).  Groups of 8 rows are summed in FP32 (their partial sums
 // stay within a few units of the last place of the stored FP32 factor), groups in FP64; the 4
 // waves are combined in fixed wave order.
 template <int DT, bool MOM, bool VEC>
-__device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) {
+__device__ void a_unit(const StreamArgs& s, const RowSide& rs, int u, double* lds,
+                       uint32_t* ldsu) {
   constexpr int U = 8;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int a = u / s.TA, t = u - a * s.TA;
   const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
   const bool lane_ok = col < s.n2;
-  const int32_t* prow = s.perm + static_cast<int64_t>(a) * s.cap;
+  const int32_t* prow = rs.perm + static_cast<int64_t>(a) * rs.cap;
   double acc[8], accw[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
@@ -39,8 +61,8 @@ __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) 
     accw[k] = 0.0;
   }
   uint32_t mx = 0;
-  for (int base = w; base < s.cap; base += 4 * 64) {
-    const int32_t pe = base + 4 * lane < s.cap ? prow[base + 4 * lane] : -1;
+  for (int base = w; base < rs.cap; base += 4 * 64) {
+    const int32_t pe = base + 4 * lane < rs.cap ? prow[base + 4 * lane] : -1;
     const int nr = __popcll(__ballot(pe != -1));   // valid entries are a prefix of the lanes
     if (nr == 0) break;
     for (int r0 = 0; r0 < nr; r0 += U) {
@@ -52,11 +74,11 @@ __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) 
         const int32_t e = row_entry(pe, ok ? r0 + q : 0);
         const int64_t row = e & 0x7fffffff;
         sg[q] = ok ? (e < 0 ? -1.0f : 1.0f) : 0.0f;
-        sw[q] = MOM ? static_cast<float>(sg[q] * static_cast<double>(row + 1) * s.inv_l1) : 0.0f;
+        sw[q] = MOM ? static_cast<float>(sg[q] * static_cast<double>(row + 1) * rs.inv_l) : 0.0f;
         if (VEC) {
-          v[q] = load8h_sel(s.A + row * s.n2 + col, ok && lane_ok, s.zero);
+          v[q] = load8h_sel(rs.X + row * s.n2 + col, ok && lane_ok, s.zero);
         } else {
-          v[q] = ok ? load8h(s.A + row * s.n2, col, s.n2, false) : u32x4{0u, 0u, 0u, 0u};
+          v[q] = ok ? load8h(rs.X + row * s.n2, col, s.n2, false) : u32x4{0u, 0u, 0u, 0u};
         }
       }
       float g32[8], gw32[8];
@@ -101,16 +123,16 @@ __device__ void a_unit(const StreamArgs& s, int u, double* lds, uint32_t* ldsu) 
       double v = lds[k * 64 + ln] + lds[(8 + k) * 64 + ln];
       v += lds[(16 + k) * 64 + ln];
       v += lds[(24 + k) * 64 + ln];
-      s.P[static_cast<int64_t>(a) * s.ldp + gc] = static_cast<float>(v);
+      rs.out[static_cast<int64_t>(a) * s.ldp + gc] = static_cast<float>(v);
       if (MOM) {
         double vw = lds[2048 + k * 64 + ln] + lds[2048 + (8 + k) * 64 + ln];
         vw += lds[2048 + (16 + k) * 64 + ln];
         vw += lds[2048 + (24 + k) * 64 + ln];
-        s.Pw[static_cast<int64_t>(a) * s.ldp + gc] = static_cast<float>(vw);
+        rs.outw[static_cast<int64_t>(a) * s.ldp + gc] = static_cast<float>(vw);
       }
     }
   }
-  if (threadIdx.x == 0) s.maxpart[u] = amax;
+  if (threadIdx.x == 0) rs.maxslot[u] = amax;
 }
 
 // ----------------------------------------------------------------------------------------
@@ -647,10 +669,14 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : 4) void stream_kernel(StreamArg
   }
   u -= s.nC;
   if (u < s.nB) {
-    b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
+    if (s.transb) {
+      a_unit<DT, MOM, VEC>(s, w_side(s), u, lds_dyn, ldsu);
+    } else {
+      b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
+    }
     return;
   }
-  a_unit<DT, MOM, VEC>(s, u - s.nB, lds_dyn, ldsu);
+  a_unit<DT, MOM, VEC>(s, a_side(s), u - s.nB, lds_dyn, ldsu);
 }
 
 // ----------------------------------------------------------------------------------------

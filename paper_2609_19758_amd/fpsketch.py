@@ -33,7 +33,7 @@ class Params(ctypes.Structure):
     _fields_ = [("m", ctypes.c_int32), ("rounds", ctypes.c_int32), ("r_star", ctypes.c_int32),
                 ("r_max", ctypes.c_int32), ("s_budget", ctypes.c_int32),
                 ("delta_rc", ctypes.c_int32), ("k_cap", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("rho_min", ctypes.c_double),
+                ("b_layout", ctypes.c_int32), ("rho_min", ctypes.c_double),
                 ("mu", ctypes.c_double), ("c_valid", ctypes.c_double),
                 ("b_star", ctypes.c_double), ("c_coll", ctypes.c_double),
                 ("seed", ctypes.c_uint64)]
@@ -225,7 +225,8 @@ def stream_copy(src, dst, nbytes: int, grid: int = 2048, stream=None):
 
 class Verifier:
     """One verifier context for products A (n1 x n2) x B (n2 x n3) in `fmt` on the current
-    HIP device."""
+    HIP device.  With b_layout=1 every call takes W = B^T (n3 x n2, a linear layer's weight,
+    C = A W^T) where it takes B."""
 
     def __init__(self, n1: int, n2: int, n3: int, fmt: str, params: Optional[Params] = None,
                  **overrides):
