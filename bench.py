@@ -230,6 +230,7 @@ def main() -> int:
     import numpy as np
     import torch
     from paper_2609_19758_amd import fpsketch as fk
+    from paper_2609_19758_amd import noise_law as nl
     from paper_2609_19758_amd import workloads as wl
 
     w = wl.workload(args.workload)
@@ -320,6 +321,32 @@ def main() -> int:
     assert int(flag.item()) == 0, "a clean call was reported dirty (graph replay)"
     log(f"probe in a HIP graph: {graph_us:.2f} us/call ({replays} replays of {per_graph} calls)")
     del g
+
+    # B passed transposed (a linear layer's weight W = B^T, n3 x n2): the same products, a context
+    # with b_layout = 1 at the calibrated m
+    vt = fk.Verifier(w.n1, w.n2, w.n3, w.fmt, m=v.m, rho_min=w.rho_min, s_budget=w.s_budget,
+                     b_layout=1)
+    tsets = [(A, B.t().contiguous(), C) for A, B, C in sets]
+    for k in range(args.warmup):
+        A, Wt, C = tsets[k % args.sets]
+        vt.probe(A, Wt, C, d_dirty=flag)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for k in range(args.steps):
+        A, Wt, C = tsets[k % args.sets]
+        vt.probe(A, Wt, C, d_dirty=flag)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    trans_us = t0.elapsed_time(t1) * 1e3 / args.steps
+    assert int(flag.item()) == 0, "a clean call was reported dirty (B transposed)"
+    vt.timing(True)
+    for k in range(args.steps):
+        A, Wt, C = tsets[k % args.sets]
+        vt.probe(A, Wt, C)
+    ts_ms, tp_ms, tn = vt.timing_read()
+    vt.close()
+    del tsets
+    log(f"B transposed: {trans_us:.2f} us/call, stream kernel {ts_ms * 1e3 / tn:.2f} us")
 
     # the probe with the B side cached (the paper's probe keeps BH2^T of the weight): one weight,
     # the activations of every buffer set, their products C = A_k B_0; A and C streamed
@@ -439,13 +466,19 @@ def main() -> int:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
         "data": "synthetic",
         "config": {"workload": w.name, "n1": w.n1, "n2": w.n2, "n3": w.n3, "operands": w.fmt,
-                   "c": "fp32", "m": v.m, "m_law": m0, "buffer_sets": args.sets,
+                   "c": "fp32", "m": v.m, "m_law": m0,
+                   "m_law_gfx950": fk.m_start(w.n1, w.n2, w.n3, w.fmt, nl.apply_law(
+                       fk.default_params(s_budget=w.s_budget), nl.LAW_GFX950_HIPBLASLT)),
+                   "buffer_sets": args.sets,
                    "bytes_per_call": w.bytes_abc},
         "us_per_call": round(ms_per * 1e3, 3),
         "kernel_us": {"stream": round(k_us, 3), "product_decide": round(p_us, 3)},
         "gemm_us": round(gemm_us, 2),
         "graph": {"us_per_call": round(graph_us, 3), "calls_per_graph": per_graph,
                   "replays": replays},
+        "b_transposed": {"us_per_call": round(trans_us, 3),
+                         "stream_us": round(ts_ms * 1e3 / tn, 3),
+                         "product_decide_us": round(tp_ms * 1e3 / tn, 3)},
         "b_cached": {"us_per_call": round(cached_us, 3), "bytes_per_call": bytes_ac,
                      "gbs_a_c": round(bytes_ac / cached_us / 1e3, 1),
                      "stream_us": round(cs_ms * 1e3 / cn, 3),

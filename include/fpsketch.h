@@ -68,6 +68,13 @@ typedef struct {
   double b_star;      /* index-budget target B* (0.3, Sec. III-F) */
   double c_coll;      /* collision constant c of m_comb (2, Sec. III-F) */
   uint64_t seed;      /* context seed; the probe uses hash round 0 of it */
+  /* Eq. 3's noise law c_f 2^-24 sqrt(n1 n3 n2) (n2/8192)^e rms(C) / m, which starts the bucket
+   * count (Eq. 4-5) and stands in for an unusable noise measurement in the plan (Sec. III-G).
+   * Defaults: the paper's envelope (c_f 0.19 BF16, 0.3344 FP16, e 0.07); the constants belong
+   * to the BLAS that computes C and can be measured for it (c_f > 0, e finite). */
+  double law_cf_bf16;
+  double law_cf_fp16;
+  double law_n2_exp;
 } fpsketch_params;
 
 /* One localized fault (Algorithm 2 "emit record").  When `absolute` is 0, C_ij + delta is the

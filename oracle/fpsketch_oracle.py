@@ -35,7 +35,6 @@ EPS32 = 2.0 ** -23                        # FP32 machine epsilon (Sec. III-D)
 HUGE_LIMIT = FP32_MAX / 16.0              # out-of-range bound of the exact scan (Sec. III-I)
 CLIP_MEAN_CONST = 1.2533                  # sqrt(pi/2), clipped-mean scale (Sec. III-E)
 MAD_CONST = 1.4826                        # MAD-to-sigma scale (Sec. III-E)
-LAW_CF = {"bf16": 0.19, "fp16": 0.19 * 1.76}   # Eq. 3 constants (FP16 = 1.76 x BF16)
 MEM_CAP_BYTES = 2 ** 31                   # 2 GiB sketch-memory cap on m_loc (Sec. III-G)
 
 # splitmix64 (Steele, Lea, Flood 2014; Vigna's reference mixer): golden-gamma increment and the
@@ -59,6 +58,13 @@ class Params:
     s_budget: int = 16         # declared error budget s
     delta_rc: int = 8          # errors per row or column, Delta
     k_cap: int = 0             # K; 0 means max(64, 8 s) (Sec. III-E)
+    # Eq. 3's constants, the paper's envelope: c_f per operand format and the n2 exponent
+    law_cf_bf16: float = 0.19
+    law_cf_fp16: float = 0.19 * 1.76
+    law_n2_exp: float = 0.07
+
+    def law_cf(self, fmt: str) -> float:
+        return self.law_cf_fp16 if fmt == "fp16" else self.law_cf_bf16
 
     @property
     def K(self) -> int:
@@ -274,15 +280,15 @@ def probe(a64, b64, c32, hr: HashRound, p: Params) -> ProbeResult:
 # Noise law and bucket counts (Sec. III-F, Eq. 3-5).
 
 
-def law_sigma_over_rms(n1: int, n2: int, n3: int, m: int, fmt: str) -> float:
-    """Eq. 3 divided by rms(C): c_f 2^-24 sqrt(n1 n3 n2) (n2/8192)^0.07 / m."""
-    return LAW_CF[fmt] * 2.0 ** -24 * math.sqrt(n1 * n3 * n2) * (n2 / 8192.0) ** 0.07 / m
+def law_sigma_over_rms(n1: int, n2: int, n3: int, m: int, fmt: str, p: Params) -> float:
+    """Eq. 3 divided by rms(C): c_f 2^-24 sqrt(n1 n3 n2) (n2/8192)^e / m."""
+    return p.law_cf(fmt) * 2.0 ** -24 * math.sqrt(n1 * n3 * n2) * (n2 / 8192.0) ** p.law_n2_exp / m
 
 
 def m_num(n1: int, n2: int, n3: int, fmt: str, p: Params) -> int:
     """Eq. 4 sized for delta = rms(C) with target B*; rms(C) cancels.  Integer: ceiling."""
-    v = max(n1, n3) / p.b_star * LAW_CF[fmt] * 2.0 ** -24 * math.sqrt(n1 * n3 * n2) * \
-        (n2 / 8192.0) ** 0.07
+    v = max(n1, n3) / p.b_star * p.law_cf(fmt) * 2.0 ** -24 * math.sqrt(n1 * n3 * n2) * \
+        (n2 / 8192.0) ** p.law_n2_exp
     return int(math.ceil(v))
 
 
@@ -367,7 +373,7 @@ def plan_localize(n1: int, n2: int, n3: int, fmt: str, m: int, sigma_hat: float,
     mx = max(n1, n3)
     fallback = not (_ok(sigma_hat) and _ok(rms))
     if fallback:
-        B = mx * law_sigma_over_rms(n1, n2, n3, m, fmt) / p.rho_min
+        B = mx * law_sigma_over_rms(n1, n2, n3, m, fmt, p) / p.rho_min
     else:
         B = mx * sigma_hat / (p.rho_min * rms)
     r_b = radius_rule(B)

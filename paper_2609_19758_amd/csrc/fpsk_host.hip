@@ -81,7 +81,9 @@ int64_t pow2_ceil(int64_t n) {
 // ------------------------------------------------------------------------------------------
 // Bucket-count rules (Sec. III-F, Eq. 3-5) and plan (Sec. III-G).
 
-double law_cf(fpsketch_dtype dt) { return dt == FPSK_F16 ? 0.19 * 1.76 : 0.19; }
+double law_cf(fpsketch_dtype dt, const fpsketch_params& p) {
+  return dt == FPSK_F16 ? p.law_cf_fp16 : p.law_cf_bf16;
+}
 
 int32_t m_comb(const fpsketch_params& p) {
   const double a = 3.0 * p.c_coll * p.delta_rc;
@@ -97,20 +99,21 @@ int64_t m_max(int64_t n1, int64_t n3) {
   return std::max<int64_t>(16, r);
 }
 
-// Eq. 3 noise over rms(C): c_f 2^-24 sqrt(n1 n3 n2) (n2/8192)^0.07 / m.
-double law_sigma_over_rms(int64_t n1, int64_t n2, int64_t n3, int64_t m, fpsketch_dtype dt) {
-  return law_cf(dt) * std::ldexp(1.0, -24) *
+// Eq. 3 noise over rms(C): c_f 2^-24 sqrt(n1 n3 n2) (n2/8192)^e / m.
+double law_sigma_over_rms(int64_t n1, int64_t n2, int64_t n3, int64_t m, fpsketch_dtype dt,
+                          const fpsketch_params& p) {
+  return law_cf(dt, p) * std::ldexp(1.0, -24) *
          std::sqrt(static_cast<double>(n1) * static_cast<double>(n3) * static_cast<double>(n2)) *
-         std::pow(static_cast<double>(n2) / 8192.0, 0.07) / static_cast<double>(m);
+         std::pow(static_cast<double>(n2) / 8192.0, p.law_n2_exp) / static_cast<double>(m);
 }
 
 int64_t m_start(int64_t n1, int64_t n2, int64_t n3, fpsketch_dtype dt, const fpsketch_params& p) {
   // Eq. 4 at delta = rms(C) with target B* (rms(C) cancels), then Eq. 5.
-  const double v = static_cast<double>(std::max(n1, n3)) / p.b_star * law_cf(dt) *
+  const double v = static_cast<double>(std::max(n1, n3)) / p.b_star * law_cf(dt, p) *
                    std::ldexp(1.0, -24) *
                    std::sqrt(static_cast<double>(n1) * static_cast<double>(n3) *
                              static_cast<double>(n2)) *
-                   std::pow(static_cast<double>(n2) / 8192.0, 0.07);
+                   std::pow(static_cast<double>(n2) / 8192.0, p.law_n2_exp);
   const int64_t mnum = static_cast<int64_t>(std::ceil(v));
   const int64_t mc = m_comb(p);
   return std::min(std::max<int64_t>({mc, mnum, 16}), std::max<int64_t>(mc, m_max(n1, n3)));
@@ -153,7 +156,7 @@ PlanOut plan_localize(int64_t n1, int64_t n2, int64_t n3, fpsketch_dtype dt, int
   const double mx = static_cast<double>(std::max(n1, n3));
   PlanOut o{};
   o.fallback = !(positive_finite(sigma) && positive_finite(rms));
-  o.B = o.fallback ? mx * law_sigma_over_rms(n1, n2, n3, m, dt) / p.rho_min
+  o.B = o.fallback ? mx * law_sigma_over_rms(n1, n2, n3, m, dt, p) / p.rho_min
                    : mx * sigma / (p.rho_min * rms);
   const int64_t rb = radius_rule(o.B);
   if (rb <= p.r_star) {
@@ -635,7 +638,9 @@ bool valid_half(fpsketch_dtype d) { return d == FPSK_F16 || d == FPSK_BF16; }
 fpsketch_status check_params(const fpsketch_params& p) {
   if (p.m < 0 || p.rounds < 1 || p.r_star < 0 || p.r_max < 0 || p.s_budget < 1 ||
       p.delta_rc < 1 || p.k_cap < 0 || !(p.rho_min > 0) || !(p.mu > 0) || !(p.c_valid > 0) ||
-      !(p.b_star > 0) || !(p.c_coll > 0) || (p.b_layout != 0 && p.b_layout != 1)) {
+      !(p.b_star > 0) || !(p.c_coll > 0) || (p.b_layout != 0 && p.b_layout != 1) ||
+      !(std::isfinite(p.law_cf_bf16) && p.law_cf_bf16 > 0) ||
+      !(std::isfinite(p.law_cf_fp16) && p.law_cf_fp16 > 0) || !std::isfinite(p.law_n2_exp)) {
     return fail(FPSK_EINVAL, "parameter out of range");
   }
   return FPSK_OK;
@@ -994,6 +999,9 @@ void fpsketch_default_params(fpsketch_params* p) {
   p->b_star = 0.3;
   p->c_coll = 2.0;
   p->seed = 0x5EED5EEDull;
+  p->law_cf_bf16 = 0.19;
+  p->law_cf_fp16 = 0.19 * 1.76;
+  p->law_n2_exp = 0.07;
 }
 
 const char* fpsketch_status_str(fpsketch_status s) {

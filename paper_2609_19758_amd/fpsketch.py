@@ -36,7 +36,8 @@ class Params(ctypes.Structure):
                 ("b_layout", ctypes.c_int32), ("rho_min", ctypes.c_double),
                 ("mu", ctypes.c_double), ("c_valid", ctypes.c_double),
                 ("b_star", ctypes.c_double), ("c_coll", ctypes.c_double),
-                ("seed", ctypes.c_uint64)]
+                ("seed", ctypes.c_uint64), ("law_cf_bf16", ctypes.c_double),
+                ("law_cf_fp16", ctypes.c_double), ("law_n2_exp", ctypes.c_double)]
 
 
 class Fault(ctypes.Structure):

@@ -61,6 +61,38 @@ def test_m_start_matches_oracle_and_table2():
             assert fk.m_start(n1, n2, n3, fmt) == o.m_start(n1, n2, n3, fmt, P)
 
 
+def test_law_constants_are_parameters():
+    """Eq. 3's constants taken from the parameters (as measured for another BLAS): the library's
+    start m and fallback plan equal the oracle's under the same constants, and out-of-range
+    constants are rejected."""
+    rng = np.random.Generator(np.random.PCG64(11))
+    for cf_b, cf_f, e in ((0.05, 0.08, 0.0), (0.31, 0.5, 0.2), (0.11, 0.11, -0.05)):
+        po = o.Params(law_cf_bf16=cf_b, law_cf_fp16=cf_f, law_n2_exp=e)
+        pl = fk.default_params(law_cf_bf16=cf_b, law_cf_fp16=cf_f, law_n2_exp=e)
+        for _ in range(100):
+            n1, n2, n3 = (int(x) for x in rng.integers(1, 70000, size=3))
+            for fmt in ("bf16", "fp16"):
+                assert fk.m_start(n1, n2, n3, fmt, pl) == o.m_start(n1, n2, n3, fmt, po)
+        for fmt in ("bf16", "fp16"):
+            ref = o.plan_localize(4096, 11008, 4096, fmt, 48, float("nan"), 2.0, po)
+            got = fk.plan_host(4096, 11008, 4096, fmt, 48, float("nan"), 2.0, pl)
+            assert got[:2] == (ref.m_loc, ref.r) and got[3] and ref.fallback
+            assert abs(got[2] - ref.B) <= 1e-12 * abs(ref.B)
+    # a smaller c_f lowers the start m; the paper's constants are the defaults
+    assert fk.m_start(2048, 4096, 12288, "bf16", fk.default_params(law_cf_bf16=0.1)) < \
+        fk.m_start(2048, 4096, 12288, "bf16")
+    d = fk.default_params()
+    assert (d.law_cf_bf16, d.law_cf_fp16, d.law_n2_exp) == (P.law_cf_bf16, P.law_cf_fp16,
+                                                            P.law_n2_exp)
+    out = ctypes.c_int32()
+    lib = fk.load()
+    for bad in ({"law_cf_bf16": 0.0}, {"law_cf_fp16": -1.0}, {"law_n2_exp": float("nan")},
+                {"law_cf_bf16": float("inf")}):
+        p = fk.default_params(**bad)
+        assert lib.fpsketch_m_start(4096, 4096, 4096, fk.BF16, ctypes.byref(p),
+                                    ctypes.byref(out)) == fk.EINVAL
+
+
 def test_plan_matches_oracle():
     rng = np.random.Generator(np.random.PCG64(2))
     shapes = [(4096, 4096, 4096), (4096, 11008, 4096), (2048, 13824, 5120),

@@ -278,7 +278,7 @@ def test_plan_growth_and_caps():
 def test_plan_fallback_to_law():
     pl = o.plan_localize(4096, 4096, 4096, "bf16", 48, float("nan"), 64.0, P)
     assert pl.fallback
-    B = 4096 * o.law_sigma_over_rms(4096, 4096, 4096, 48, "bf16") / P.rho_min
+    B = 4096 * o.law_sigma_over_rms(4096, 4096, 4096, 48, "bf16", P) / P.rho_min
     assert abs(pl.B - B) < 1e-12
     assert o.plan_localize(4096, 4096, 4096, "bf16", 48, 0.0, 64.0, P).fallback
     assert o.plan_localize(4096, 4096, 4096, "bf16", 48, 1e-3, float("inf"), P).fallback
