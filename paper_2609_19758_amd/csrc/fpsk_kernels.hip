@@ -143,9 +143,10 @@ __global__ __launch_bounds__(kThreads) void block_product_kernel(ProductArgs pa)
   // every load is issued before the first is used: the slice's factor rows, then the C grid of
   // the block (slice 0; thread (v = t & 15, group t >> 4) takes every 16th column-group partial)
   const int kb = slice * kXSlice;
-  // the slice in 4 / JH round trips of JH 16-byte loads per row (JH = 2 for the largest block
+  // the slice in NJ / JH round trips of JH 16-byte loads per row (JH = 2 for the largest block
   // keeps the loads within the register file)
-  constexpr int JH = XB <= 3 ? 4 : 2;
+  constexpr int NJ = kXSlice / (4 * kThreads);
+  constexpr int JH = (XB <= 3 ? 4 : 2) < NJ ? (XB <= 3 ? 4 : 2) : NJ;
   double acc[NV];
 #pragma unroll
   for (int v = 0; v < NV; ++v) acc[v] = 0.0;
@@ -155,7 +156,7 @@ __global__ __launch_bounds__(kThreads) void block_product_kernel(ProductArgs pa)
   const bool vok = slice == 0 && cv < NV && a0 + ci < m && b0 + cj < m;
   const int64_t co = vok ? static_cast<int64_t>(a0 + ci) * m + b0 + cj : 0;
 #pragma unroll
-  for (int h = 0; h < 4 / JH; ++h) {
+  for (int h = 0; h < NJ / JH; ++h) {
   float4 pv[XB][JH], qv[XB][JH];
 #pragma unroll
   for (int j = 0; j < JH; ++j) {
@@ -237,11 +238,23 @@ __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArg
   const float* mb = pa.maxpart_b != nullptr ? pa.maxpart_b : pa.maxpart + pa.nA;
   float amax = t < pa.nA ? pa.maxpart[t] : 0.0f;
   float bmax = t < pa.nB ? mb[t] : 0.0f;
-  for (int sl = 1; sl < pa.xns; ++sl) {
+  // the other slices in slice order, four slices' loads issued before their sums
+  for (int sl0 = 1; sl0 < pa.xns; sl0 += 4) {
+    double x[4][NQ];
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int o = t + kDecideThreads * q;
-      if (o < mm) v[q] += pa.xpart[static_cast<int64_t>(sl) * mm + o];
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int o = t + kDecideThreads * q;
+        x[j][q] = (sl0 + j < pa.xns && o < mm)
+                      ? pa.xpart[static_cast<int64_t>(sl0 + j) * mm + o] : 0.0;
+      }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (sl0 + j < pa.xns) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) v[q] += x[j][q];
+      }
     }
   }
   for (int i = t + kDecideThreads; i < pa.nA; i += kDecideThreads) {
