@@ -322,6 +322,26 @@ def main() -> int:
     log(f"probe in a HIP graph: {graph_us:.2f} us/call ({replays} replays of {per_graph} calls)")
     del g
 
+    # deferred probes: each call's launch also runs the previous call's block products and the
+    # decision of the one before; the flush after the last call is inside the timed region
+    dflags = torch.zeros(args.steps, dtype=torch.int32, device="cuda")
+    for k in range(args.warmup):
+        A, B, C = sets[k % args.sets]
+        v.probe_deferred(A, B, C, d_dirty=dflags[k % args.steps:k % args.steps + 1])
+    v.probe_flush()
+    dflags.zero_()
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for k in range(args.steps):
+        A, B, C = sets[k % args.sets]
+        v.probe_deferred(A, B, C, d_dirty=dflags[k:k + 1])
+    v.probe_flush()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    deferred_us = t0.elapsed_time(t1) * 1e3 / args.steps
+    assert int(dflags.sum().item()) == 0, "a clean call was reported dirty (deferred)"
+    log(f"deferred probes: {deferred_us:.2f} us/call ({w.bytes_abc / deferred_us / 1e3:.0f} GB/s)")
+
     # B passed transposed (a linear layer's weight W = B^T, n3 x n2): the same products, a context
     # with b_layout = 1 at the calibrated m
     vt = fk.Verifier(w.n1, w.n2, w.n3, w.fmt, m=v.m, rho_min=w.rho_min, s_budget=w.s_budget,
@@ -476,6 +496,8 @@ def main() -> int:
         "gemm_us": round(gemm_us, 2),
         "graph": {"us_per_call": round(graph_us, 3), "calls_per_graph": per_graph,
                   "replays": replays},
+        "deferred": {"us_per_call": round(deferred_us, 3),
+                     "gbs": round(w.bytes_abc / deferred_us / 1e3, 1)},
         "b_transposed": {"us_per_call": round(trans_us, 3),
                          "stream_us": round(ts_ms * 1e3 / tn, 3),
                          "product_decide_us": round(tp_ms * 1e3 / tn, 3)},

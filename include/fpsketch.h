@@ -173,6 +173,25 @@ fpsketch_status fpsketch_cache_b(fpsketch_ctx* ctx, const void* B, void* stream)
 fpsketch_status fpsketch_probe_cached(fpsketch_ctx* ctx, const void* A, const void* C,
                                       fpsketch_dtype c_dtype, int32_t* d_dirty, void* stream);
 
+/* fpsketch_probe without waiting for its own product and decision (Sec. III-C: the verdict is a
+ * device flag the caller reads later).  For the probe's block path up to m = 48 (n2 <= 16384)
+ * each call enqueues ONE launch holding the decision of the call before the previous one, the
+ * block products of the previous call and this call's pass over A, B and C; these run side by side
+ * on three workspace sets in rotation, with the same arithmetic, hence the same bits, as
+ * fpsketch_probe.  A call's verdict (ORed into its d_dirty), its statistics and its share of the
+ * running noise sum are therefore final only after two more deferred calls or
+ * fpsketch_probe_flush.  Every other call on the context flushes first (and waits for the
+ * pending work when it runs on another stream).  A, B and C are read by this call's launch only:
+ * the caller may reuse them as for fpsketch_probe; d_dirty must stay valid until the flush.
+ * Deferred calls and the flush go to one stream (FPSK_EINVAL for another while calls are
+ * pending).  Other shapes run an ordinary probe.  Errors as fpsketch_probe. */
+fpsketch_status fpsketch_probe_deferred(fpsketch_ctx* ctx, const void* A, const void* B,
+                                        const void* C, fpsketch_dtype c_dtype, int32_t* d_dirty,
+                                        void* stream);
+
+/* Enqueues what deferred probes still owe (at most two launches); nothing pending: no-op. */
+fpsketch_status fpsketch_probe_flush(fpsketch_ctx* ctx, void* stream);
+
 /* Algorithm 2, apply step: writes the n records `recs` (a HOST array, as fpsketch_localize
  * returns them) into the device product C (n1 x n3 FP32, row-major), then probes the repaired
  * C once more with a fresh hash round.  Record (i, j, delta, absolute): C_ij <- delta when

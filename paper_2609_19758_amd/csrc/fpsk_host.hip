@@ -623,6 +623,15 @@ struct fpsketch_ctx {
   // (0: nothing cached) and the per-work-group max |B|
   DevBuf qcache, maxb_cache;
   int qcache_m = 0;
+  // deferred probes (m <= 64): three workspace sets in rotation; the previous call, whose block
+  // products are still to run, and the one before it, whose decision is; the stream their
+  // launches go to
+  Workspace pipe_ws[3];
+  int pipe_next = 0;
+  bool pipe_has_prod = false, pipe_has_dec = false;
+  fpsk::ProductArgs pipe_prod{}, pipe_dec{};
+  int pipe_nprod = 0, pipe_xb = 1;
+  hipStream_t pipe_stream = nullptr;
   fpsketch_plan_info last_plan{};
 
   // optional per-probe events: start and end of the stream kernel, of the product dispatches
@@ -659,15 +668,14 @@ fpsketch_status set_device(const fpsketch_ctx* c) {
 // or taken from that cache (A and C streamed).
 enum class BSide { kStream, kFillCache, kUseCache };
 
-// One sketch pass (stream + product) on `st`.
-fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const void* A,
-                         const void* B, const float* Cm, bool mom, int mode, int32_t* d_dirty,
-                         const int32_t* prow, const int32_t* pcol, const float* pval,
-                         hipStream_t st, hipEvent_t* ev = nullptr,
-                         double* stats_out = nullptr, double* sigma_acc_out = nullptr,
-                         BSide bside = BSide::kStream) {
+// Arguments of one sketch pass (stream + product) over workspace W.
+fpsketch_status pass_args(fpsketch_ctx* c, const DevRound& R, Workspace& W, const void* A,
+                          const void* B, const float* Cm, bool mom, int mode, int32_t* d_dirty,
+                          const int32_t* prow, const int32_t* pcol, const float* pval,
+                          double* stats_out, double* sigma_acc_out, BSide bside,
+                          fpsk::StreamArgs& s, fpsk::ProductArgs& a) {
   const Decomp& d = W.d;
-  fpsk::StreamArgs s{};
+  s = fpsk::StreamArgs{};
   s.A = static_cast<const uint16_t*>(A);
   s.B = static_cast<const uint16_t*>(B);
   s.C = Cm;
@@ -728,13 +736,10 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
     s.nC = 0;
     s.Q = as<float>(c->qcache);
     s.maxpart = as<float>(c->maxb_cache);
-    FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, false, d.rb, d.g, d.ng,
-                                 d.lds_stream, st));
-    return FPSK_OK;
   }
   if (bside == BSide::kUseCache) s.nB = 0;
 
-  fpsk::ProductArgs a{};
+  a = fpsk::ProductArgs{};
   a.P = s.P;
   a.Pw = s.Pw;
   a.Q = s.Q;
@@ -783,12 +788,51 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
     a.xslots = d.xslots;
     a.xpart = as<double>(W.xpart);
   }
+  return FPSK_OK;
+}
+
+// One sketch pass (stream + product) on `st`.
+fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const void* A,
+                         const void* B, const float* Cm, bool mom, int mode, int32_t* d_dirty,
+                         const int32_t* prow, const int32_t* pcol, const float* pval,
+                         hipStream_t st, hipEvent_t* ev = nullptr,
+                         double* stats_out = nullptr, double* sigma_acc_out = nullptr,
+                         BSide bside = BSide::kStream) {
+  const Decomp& d = W.d;
+  fpsk::StreamArgs s;
+  fpsk::ProductArgs a;
+  FPSK_TRY(pass_args(c, R, W, A, B, Cm, mom, mode, d_dirty, prow, pcol, pval, stats_out,
+                     sigma_acc_out, bside, s, a));
+  if (bside == BSide::kFillCache) {
+    FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, false, d.rb, d.g, d.ng,
+                                 d.lds_stream, st));
+    return FPSK_OK;
+  }
   // with ev: the dispatches themselves time-stamp ev[0..1] (stream kernel) and ev[2..3]
   // (first product dispatch start to last dispatch end)
   FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.ng,
                                d.lds_stream, st, ev ? ev[0] : nullptr, ev ? ev[1] : nullptr));
   FPSK_HIP(fpsk::launch_product(a, d.ts, d.kw, mom, st, ev ? ev[2] : nullptr,
                                 ev ? ev[3] : nullptr));
+  return FPSK_OK;
+}
+
+// Enqueue what deferred probes still owe (at most two launches of block products and
+// decisions) on their stream.  When the caller continues on another stream, wait for them.
+fpsketch_status pipe_flush(fpsketch_ctx* c, hipStream_t next_st) {
+  const bool had = c->pipe_has_prod || c->pipe_has_dec;
+  while (c->pipe_has_prod || c->pipe_has_dec) {
+    fpsk::StreamArgs none{};
+    const size_t lds = fpsk::probe_pipe_lds(c->pipe_xb);
+    FPSK_HIP(fpsk::launch_probe_pipe(none, c->pipe_prod, c->pipe_dec,
+                                     c->pipe_has_prod ? c->pipe_nprod : 0,
+                                     c->pipe_has_dec ? 1 : 0, c->dt == FPSK_BF16 ? 1 : 0,
+                                     c->pipe_xb, lds, c->pipe_stream));
+    c->pipe_dec = c->pipe_prod;
+    c->pipe_has_dec = c->pipe_has_prod;
+    c->pipe_has_prod = false;
+  }
+  if (had && next_st != c->pipe_stream) FPSK_HIP(hipStreamSynchronize(c->pipe_stream));
   return FPSK_OK;
 }
 
@@ -1136,12 +1180,14 @@ fpsketch_status fpsketch_create(int64_t n1, int64_t n2, int64_t n3, fpsketch_dty
 void fpsketch_destroy(fpsketch_ctx* c) {
   if (c == nullptr) return;
   (void)hipSetDevice(c->device);
+  (void)pipe_flush(c, c->pipe_stream);
   (void)hipDeviceSynchronize();
   for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
   free_round(c->probe_round);
   free_workspace(c->probe_ws);
   free_round(c->aux_round);
   free_workspace(c->aux_ws);
+  for (Workspace& w : c->pipe_ws) free_workspace(w);
   for (DevBuf* b : {&c->stats, &c->sigma_acc, &c->zero, &c->scan_counts, &c->scan_rows, &c->scan_base,
                     &c->scan_out, &c->samples, &c->patch_rowptr, &c->patch_col, &c->patch_val,
                     &c->rc_coords, &c->rc_gamma, &c->rc_abs, &c->rc_c, &c->sel_state,
@@ -1157,6 +1203,7 @@ fpsketch_status fpsketch_probe(fpsketch_ctx* c, const void* A, const void* B, co
   FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   hipEvent_t* ev = nullptr;
   if (c->timing) {
     while (c->events.size() < c->events_used + 4) {
@@ -1175,6 +1222,7 @@ fpsketch_status fpsketch_cache_b(fpsketch_ctx* c, const void* B, void* stream) {
   if (c == nullptr || B == nullptr) return fail(FPSK_EINVAL, "null argument");
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   const Decomp& d = c->probe_ws.d;
   const size_t fm = static_cast<size_t>(c->m) * static_cast<size_t>(d.ldp) * sizeof(float);
   FPSK_TRY(dev_alloc_zero(c->qcache, fm));
@@ -1195,6 +1243,7 @@ fpsketch_status fpsketch_probe_cached(fpsketch_ctx* c, const void* A, const void
   }
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   hipEvent_t* ev = nullptr;
   if (c->timing) {
     while (c->events.size() < c->events_used + 4) {
@@ -1208,6 +1257,55 @@ fpsketch_status fpsketch_probe_cached(fpsketch_ctx* c, const void* A, const void
   return run_pass(c, c->probe_round, c->probe_ws, A, c->zero.p, static_cast<const float*>(C),
                   false, 1, d_dirty, nullptr, nullptr, nullptr, st, ev, nullptr, nullptr,
                   BSide::kUseCache);
+}
+
+fpsketch_status fpsketch_probe_deferred(fpsketch_ctx* c, const void* A, const void* B,
+                                        const void* C, fpsketch_dtype c_dtype, int32_t* d_dirty,
+                                        void* stream) {
+  FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((c->pipe_has_prod || c->pipe_has_dec) && st != c->pipe_stream) {
+    return fail(FPSK_EINVAL, "deferred probes are pending on another stream");
+  }
+  const Decomp& d = c->probe_ws.d;
+  if (d.nX == 0 || d.xb > 3) {
+    // not the pipelined path (m > 48 or n2 > 16384): an ordinary probe, nothing left pending
+    FPSK_TRY(pipe_flush(c, st));
+    return run_pass(c, c->probe_round, c->probe_ws, A, B, static_cast<const float*>(C), false,
+                    1, d_dirty, nullptr, nullptr, nullptr, st);
+  }
+  Workspace& W = c->pipe_ws[c->pipe_next];
+  FPSK_TRY(ensure_workspace(W, c->n1, c->n2, c->n3, c->m, false, c->transb));
+  fpsk::StreamArgs s;
+  fpsk::ProductArgs a;
+  FPSK_TRY(pass_args(c, c->probe_round, W, A, B, static_cast<const float*>(C), false, 1, d_dirty,
+                     nullptr, nullptr, nullptr, nullptr, nullptr, BSide::kStream, s, a));
+  const size_t lds = std::max(d.lds_stream, fpsk::probe_pipe_lds(d.xb));
+  FPSK_HIP(fpsk::launch_probe_pipe(s, c->pipe_prod, c->pipe_dec,
+                                   c->pipe_has_prod ? c->pipe_nprod : 0,
+                                   c->pipe_has_dec ? 1 : 0, c->dt == FPSK_BF16 ? 1 : 0, d.xb,
+                                   lds, st));
+  c->pipe_dec = c->pipe_prod;
+  c->pipe_has_dec = c->pipe_has_prod;
+  c->pipe_prod = a;
+  c->pipe_has_prod = true;
+  c->pipe_nprod = d.nX;
+  c->pipe_xb = d.xb;
+  c->pipe_stream = st;
+  c->pipe_next = (c->pipe_next + 1) % 3;
+  return FPSK_OK;
+}
+
+fpsketch_status fpsketch_probe_flush(fpsketch_ctx* c, void* stream) {
+  if (c == nullptr) return fail(FPSK_EINVAL, "null context");
+  if (!(c->pipe_has_prod || c->pipe_has_dec)) return FPSK_OK;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (st != c->pipe_stream) {
+    return fail(FPSK_EINVAL, "deferred probes are pending on another stream");
+  }
+  FPSK_TRY(set_device(c));
+  return pipe_flush(c, st);
 }
 
 fpsketch_status fpsketch_timing(fpsketch_ctx* c, int32_t enable) {
@@ -1250,6 +1348,7 @@ fpsketch_status fpsketch_probe_stats(fpsketch_ctx* c, double* out, void* stream)
   if (c == nullptr || out == nullptr) return fail(FPSK_EINVAL, "null argument");
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   FPSK_HIP(hipMemcpyAsync(out, c->stats.p, 8 * sizeof(double), hipMemcpyDeviceToHost, st));
   FPSK_HIP(hipStreamSynchronize(st));
   return FPSK_OK;
@@ -1272,6 +1371,7 @@ fpsketch_status fpsketch_sketch(fpsketch_ctx* c, const void* A, const void* B, c
   if (m < 1 || m > fpsk::kMaxM) return fail(FPSK_ESHAPE, "bucket count outside [1, 4096]");
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   HostRound HR;
   std::vector<double> hS, hR, hT;
   double ma = 0, mb = 0;
@@ -1306,6 +1406,7 @@ fpsketch_status fpsketch_recheck(fpsketch_ctx* c, const void* A, const void* B,
   }
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   if (n == 0) return FPSK_OK;
   const size_t nn = static_cast<size_t>(n);
   FPSK_TRY(dev_alloc(c->rc_coords, 2 * nn * sizeof(int64_t)));
@@ -1345,6 +1446,7 @@ fpsketch_status fpsketch_apply(fpsketch_ctx* c, const void* A, const void* B, vo
   }
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   float* Cm = static_cast<float*>(C);
   if (n > 0) {
     FPSK_TRY(dev_alloc(c->apply_list, list.size() * sizeof(fpsk::ApplyEntry)));
@@ -1379,6 +1481,7 @@ fpsketch_status fpsketch_calibrate_noise(fpsketch_ctx* c, const void* C, fpsketc
   if (C == nullptr) return fail(FPSK_EINVAL, "null C");
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   double acc[2] = {0.0, 0.0};
   FPSK_HIP(hipMemcpyAsync(acc, c->sigma_acc.p, sizeof(acc), hipMemcpyDeviceToHost, st));
   FPSK_HIP(hipStreamSynchronize(st));
@@ -1413,6 +1516,7 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
   }
   FPSK_TRY(set_device(c));
   const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
   const float* Cf = static_cast<const float*>(C);
   const int32_t K = cap_K(c->p);
   std::vector<Found> F;

@@ -110,6 +110,13 @@ struct ProductArgs {
 
 // e0 / e1 (may be null): events that the first / last dispatch of the call records its
 // start / end time in.
+// Pipelined probe launch (m <= 64, block path): the decision of `dec` (if has_dec), the nprod
+// block products of `prod` and the stream pass of `s` (which may be empty: nA = nB = nC = 0).
+// lds_bytes covers the stream pass and probe_pipe_lds(xb).
+size_t probe_pipe_lds(int xb);
+hipError_t launch_probe_pipe(const StreamArgs& s, const ProductArgs& prod, const ProductArgs& dec,
+                             int nprod, int has_dec, int dt, int xb, size_t lds_bytes,
+                             hipStream_t st, hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int g, int ng,
                          size_t lds_bytes, hipStream_t st, hipEvent_t e0 = nullptr,
                          hipEvent_t e1 = nullptr);

@@ -8,299 +8,23 @@
 //           (Sec. III-I), strided samples of C for rms-hat (Sec. III-G) and the validation
 //           recomputation of candidates (Sec. III-D).
 // select:   exact order statistics, peel and candidate scan of a localize round (Algorithm 1).
-#include "fpsk_device.h"
+#include "fpsk_block.h"
 
 namespace fpsk {
 
 // ----------------------------------------------------------------------------------------
-// Reductions and the probe decision shared by the block and tile product paths.
-
-// Fixed-order work-group reduction of NV values per thread through LDS (cross-lane shuffles
-// of doubles cost tens of cycles each).  Levels of 16: at a level over N entries, thread
-// g < N / 16 of value i combines entries g, g + N / 16, ..., g + 15 N / 16 (consecutive threads
-// read consecutive addresses; the 16 reads are issued together), until at most 16 remain,
-// which one thread per value combines in order.  Bit i of max_mask selects max instead of sum
-// for value i.  buf holds NV * (2 NT / 16 + NT + 1) doubles; every thread receives the results.
-template <int N, int NV>
-__device__ __forceinline__ void lds_reduce_level(const double* src, double* dst,
-                                                 uint32_t max_mask) {
-  if constexpr (N <= 16) {
-    if (static_cast<int>(threadIdx.x) < NV) {
-      const int i = threadIdx.x;
-      const bool mx = (max_mask >> i) & 1u;
-      double e[N];
-#pragma unroll
-      for (int q = 0; q < N; ++q) e[q] = src[i * N + q];
-      double r = e[0];
-#pragma unroll
-      for (int q = 1; q < N; ++q) r = mx ? fmax(r, e[q]) : r + e[q];
-      dst[i] = r;
-    }
-    __syncthreads();
-  } else {
-    constexpr int GN = N / 16;
-    if (static_cast<int>(threadIdx.x) < NV * GN) {
-      const int i = threadIdx.x / GN, g = threadIdx.x - i * GN;
-      const bool mx = (max_mask >> i) & 1u;
-      const double* b = src + i * N + g;
-      double e[16];
-#pragma unroll
-      for (int q = 0; q < 16; ++q) e[q] = b[q * GN];
-      double r = e[0];
-#pragma unroll
-      for (int q = 1; q < 16; ++q) r = mx ? fmax(r, e[q]) : r + e[q];
-      dst[i * GN + g] = r;
-    }
-    __syncthreads();
-    lds_reduce_level<GN, NV>(dst, dst + NV * GN, max_mask);
-  }
-}
-
-template <int NT, int NV>
-__device__ void lds_reduce(double (&v)[NV], double* buf, uint32_t max_mask) {
-  static_assert(NT % 16 == 0 && NT <= 4096, "levels of 16");
-#pragma unroll
-  for (int i = 0; i < NV; ++i) buf[i * NT + threadIdx.x] = v[i];
-  __syncthreads();
-  double* tmp = buf + NV * NT;
-  lds_reduce_level<NT, NV>(buf, tmp, max_mask);
-  // the results follow the last level's inputs: locate them by replaying the level sizes
-  int n = NT;
-  double* res = tmp;
-  while (n > 16) {
-    res += NV * (n / 16);
-    n /= 16;
-  }
-#pragma unroll
-  for (int i = 0; i < NV; ++i) v[i] = res[i];
-  __syncthreads();
-}
-
-// The probe's decision from the reduced statistics (Sec. III-B): clipped-mean noise estimate,
-// validity bound from max|A| and max|B|, threshold and verdict.
-__device__ void decide_tail(const ProductArgs& pa, double sum_abs, double max_abs, double nbad,
-                            double clipped, double maxA, double maxB, double acc0, double acc1) {
-  const double mm = static_cast<double>(pa.m) * pa.m;
-  const double sigma = 1.2533 * (clipped / mm);
-  const double tau = pa.c_valid * static_cast<double>(pa.n2) * 0x1p-23 * maxA * maxB;
-  const double lim = pa.lim_factor * sigma;
-  const double thr = fmin(tau, lim);
-  const bool finite = nbad == 0.0;
-  const bool clean = finite && max_abs <= thr;
-  (void)sum_abs;
-  pa.stats[0] = sigma;
-  pa.stats[1] = thr;
-  pa.stats[2] = tau;
-  pa.stats[3] = max_abs;
-  pa.stats[4] = finite ? 1.0 : 0.0;
-  pa.stats[5] = clean ? 0.0 : 1.0;
-  pa.stats[6] = maxA;
-  pa.stats[7] = maxB;
-  if (clean) {
-    pa.sigma_acc[0] = acc0 + sigma;
-    pa.sigma_acc[1] = acc1 + 1.0;
-  } else if (pa.d_dirty != nullptr) {
-    *pa.d_dirty = 1;
-  }
-}
-
-// ----------------------------------------------------------------------------------------
-// Probe product for m <= 64: block_product_kernel, then block_decide_kernel.
-//   block_product_kernel (block, slice): outputs (a0 .. a0 + XB) x (b0 .. b0 + XB) over the
-//     k-slice [slice * kXSlice, + kXSlice).  Thread t takes k = 4 (t + 256 j) within the slice;
-//     the dot products run in FP64 on the FP32 factors (rows of P and of the transposed Q, both
-//     k-contiguous, read with 16-byte loads that the work-groups of an XCD share through its L2);
-//     the 4 waves are combined in fixed order.  Slice 0 subtracts the C grid (the sum of the
-//     column-group partials).
-//   block_decide_kernel (one work-group): S = sum of the slice partials in slice order (kept
-//     in registers, not stored), the probe statistics and the verdict.
+// Probe product for m <= 64 (bodies in fpsk_block.h): the block products, then one deciding
+// work-group of kDecideThreads.
 
 template <int XB>
 __global__ __launch_bounds__(kThreads) void block_product_kernel(ProductArgs pa) {
-  constexpr int NV = XB * XB;
-  __shared__ double red[NV * (kThreads + 2 * kThreads / 16 + 1)];
-  const int m = pa.m;
-  const int64_t mm = static_cast<int64_t>(m) * m;
-  // XCD-local slot of this launch index, then its slice and output block
-  const int per = gridDim.x / 8;
-  const int slot = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
-  const int slice = slot / pa.xslots;
-  if (slice >= pa.xns) return;
-  const int q = slot - slice * pa.xslots;
-  const int st = q / (pa.xsr * pa.xsc), within = q - st * (pa.xsr * pa.xsc);
-  const int rbk = (st / pa.xnstc) * pa.xsr + within / pa.xsc;
-  const int cbk = (st % pa.xnstc) * pa.xsc + within % pa.xsc;
-  if (rbk >= pa.xnb || cbk >= pa.xnb) return;
-  const int a0 = rbk * XB, b0 = cbk * XB;
-  // uniform row bases (rows past m repeat row m - 1; their results are dropped)
-  const float* prow[XB];
-  const float* qrow[XB];
-#pragma unroll
-  for (int i = 0; i < XB; ++i) {
-    prow[i] = pa.P + static_cast<int64_t>(a0 + i < m ? a0 + i : m - 1) * pa.ldp;
-    qrow[i] = pa.Q + static_cast<int64_t>(b0 + i < m ? b0 + i : m - 1) * pa.ldp;
-  }
-  // every load is issued before the first is used: the slice's factor rows, then the C grid of
-  // the block (slice 0; thread (v = t & 15, group t >> 4) takes every 16th column-group partial)
-  const int kb = slice * kXSlice;
-  // the slice in NJ / JH round trips of JH 16-byte loads per row (JH = 2 for the largest block
-  // keeps the loads within the register file)
-  constexpr int NJ = kXSlice / (4 * kThreads);
-  constexpr int JH = (XB <= 3 ? 4 : 2) < NJ ? (XB <= 3 ? 4 : 2) : NJ;
-  double acc[NV];
-#pragma unroll
-  for (int v = 0; v < NV; ++v) acc[v] = 0.0;
-  double c4[4];
-  const int cv = threadIdx.x & 15, gs = threadIdx.x >> 4;
-  const int ci = cv / XB, cj = cv - (cv / XB) * XB;
-  const bool vok = slice == 0 && cv < NV && a0 + ci < m && b0 + cj < m;
-  const int64_t co = vok ? static_cast<int64_t>(a0 + ci) * m + b0 + cj : 0;
-#pragma unroll
-  for (int h = 0; h < NJ / JH; ++h) {
-  float4 pv[XB][JH], qv[XB][JH];
-#pragma unroll
-  for (int j = 0; j < JH; ++j) {
-    const int k = kb + 4 * (static_cast<int>(threadIdx.x) + kThreads * (h * JH + j));
-    const bool kok = k < pa.kact;
-    const int kk = kok ? k : 0;
-#pragma unroll
-    for (int i = 0; i < XB; ++i) {
-      const float4 p = *reinterpret_cast<const float4*>(prow[i] + kk);
-      const float4 q = *reinterpret_cast<const float4*>(qrow[i] + kk);
-      const float4 z = {0.f, 0.f, 0.f, 0.f};
-      pv[i][j] = kok ? p : z;
-      qv[i][j] = kok ? q : z;
-    }
-  }
-  if (h == 0) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int g = gs + 16 * q;
-      const double c = pa.partS[static_cast<int64_t>(g < pa.npc ? g : 0) * mm + co];
-      c4[q] = (vok && g < pa.npc) ? c : 0.0;
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < JH; ++j)
-#pragma unroll
-    for (int i = 0; i < XB; ++i)
-#pragma unroll
-      for (int c = 0; c < XB; ++c) {
-        double t = acc[i * XB + c];
-        t = fma(static_cast<double>(pv[i][j].x), static_cast<double>(qv[c][j].x), t);
-        t = fma(static_cast<double>(pv[i][j].y), static_cast<double>(qv[c][j].y), t);
-        t = fma(static_cast<double>(pv[i][j].z), static_cast<double>(qv[c][j].z), t);
-        t = fma(static_cast<double>(pv[i][j].w), static_cast<double>(qv[c][j].w), t);
-        acc[i * XB + c] = t;
-      }
-  }
-  double cp = (c4[0] + c4[1]) + (c4[2] + c4[3]);
-  for (int g = gs + 64; g < pa.npc; g += 16) {   // more than 64 column groups (small m)
-    cp += vok ? pa.partS[static_cast<int64_t>(g) * mm + co] : 0.0;
-  }
-  lds_reduce<kThreads, NV>(acc, red, 0u);
-  // C grid of output v: the 16 column-group sums of threads v, 16 + v, ... in order
-  red[threadIdx.x] = cp;
-  __syncthreads();
-  if (static_cast<int>(threadIdx.x) < NV) {
-    const int v = threadIdx.x;
-    const int i = v / XB, c = v - (v / XB) * XB;
-    double cg = 0.0;
-    for (int g = 0; g < 16; ++g) cg += red[g * 16 + v];
-    if (a0 + i < m && b0 + c < m) {
-      pa.xpart[slice * mm + static_cast<int64_t>(a0 + i) * m + b0 + c] = acc[v] - cg;
-    }
-  }
+  __shared__ double red[lds_reduce_doubles<kThreads, XB * XB>()];
+  block_product_body<XB, (XB <= 3 ? 4 : 2), XB * XB>(pa, blockIdx.x, gridDim.x, red);
 }
 
-constexpr int kDecideThreads = 1024;
-
 __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArgs pa) {
-  constexpr int NQ = 4;                       // m <= 64: m^2 <= 4096 outputs
-  __shared__ double red[5 * (kDecideThreads + 2 * kDecideThreads / 16 + 1)];
-  const int m = pa.m;
-  const int mm = m * m;
-  // the first slice's partials and the first share of the maxima are loaded together; only
-  // outputs and maxima that exist are loaded
-  double v[NQ];
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
-    v[q] = o < mm ? pa.xpart[o] : 0.0;
-  }
-  const int t = threadIdx.x;
-  // the running noise sum, read now so that the verdict does not wait on it
-  double acc0 = 0.0, acc1 = 0.0;
-  if (t == 0) {
-    acc0 = pa.sigma_acc[0];
-    acc1 = pa.sigma_acc[1];
-  }
-  const float* mb = pa.maxpart_b != nullptr ? pa.maxpart_b : pa.maxpart + pa.nA;
-  float amax = t < pa.nA ? pa.maxpart[t] : 0.0f;
-  float bmax = t < pa.nB ? mb[t] : 0.0f;
-  // the other slices in slice order, four slices' loads issued before their sums
-  for (int sl0 = 1; sl0 < pa.xns; sl0 += 4) {
-    double x[4][NQ];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int o = t + kDecideThreads * q;
-        x[j][q] = (sl0 + j < pa.xns && o < mm)
-                      ? pa.xpart[static_cast<int64_t>(sl0 + j) * mm + o] : 0.0;
-      }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (sl0 + j < pa.xns) {
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) v[q] += x[j][q];
-      }
-    }
-  }
-  for (int i = t + kDecideThreads; i < pa.nA; i += kDecideThreads) {
-    amax = fmaxf(amax, pa.maxpart[i]);
-  }
-  for (int i = t + kDecideThreads; i < pa.nB; i += kDecideThreads) {
-    bmax = fmaxf(bmax, mb[i]);
-  }
-  double lsum = 0.0, lmax = 0.0, lbad = 0.0;
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
-    if (o < mm) {
-      const double av = fabs(v[q]);
-      if (__builtin_isfinite(v[q])) {
-        lsum += av;
-        lmax = fmax(lmax, av);
-      } else {
-        lbad += 1.0;
-      }
-    }
-  }
-  // the five first-phase reductions in one pass (sums: 0, 2; maxima: 1, 3, 4)
-  double r5[5] = {lsum, lmax, lbad, static_cast<double>(amax), static_cast<double>(bmax)};
-  lds_reduce<kDecideThreads, 5>(r5, red, 0x1au);
-  const double sum_abs = r5[0], max_abs = r5[1], nbad = r5[2];
-  const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / static_cast<double>(mm);
-  const double clip = 5.0 * mean_abs;
-  // When no bucket reaches the clip (the usual clean case) the clipped sum is sum|S| itself:
-  // the same terms in the same order through the same reduction tree.  Otherwise a second pass.
-  double clipped = sum_abs;
-  if (!(nbad == 0.0 && max_abs <= clip)) {
-    double c2 = 0.0;
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int o = static_cast<int>(threadIdx.x) + kDecideThreads * q;
-      if (o < mm) {
-        const double a = fabs(v[q]);
-        c2 += a < clip ? a : clip;
-      }
-    }
-    double r1[1] = {c2};
-    lds_reduce<kDecideThreads, 1>(r1, red, 0u);
-    clipped = r1[0];
-  }
-  if (threadIdx.x == 0) decide_tail(pa, sum_abs, max_abs, nbad, clipped, r5[3], r5[4], acc0, acc1);
+  __shared__ double red[lds_reduce_doubles<kDecideThreads, 5>()];
+  block_decide_body<kDecideThreads, 4>(pa, red);
 }
 
 // ----------------------------------------------------------------------------------------

@@ -5,7 +5,7 @@
 // weighted forms that give the first-moment sketches R and T (paper, Sec. III-B).  No atomics:
 // every sum has a fixed order, so sketches are bit-reproducible.  Streaming sums accumulate in
 // FP64.
-#include "fpsk_device.h"
+#include "fpsk_block.h"
 
 namespace fpsk {
 
@@ -677,6 +677,93 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : 4) void stream_kernel(StreamArg
     return;
   }
   a_unit<DT, MOM, VEC>(s, a_side(s), u - s.nB, lds_dyn, ldsu);
+}
+
+// ----------------------------------------------------------------------------------------
+// Pipelined probe (m <= 48: output blocks of at most 3 x 3, as the 4 x 4 block's product does
+// not fit the stream pass's 128 registers; no moments): one launch runs the decision of the call
+// before the previous one, the block products of the previous call and the stream pass of this
+// call.  The
+// three read and write disjoint workspace sets, and each reads only what an earlier launch
+// wrote, so they need no ordering among themselves; the product and decision work-groups run
+// beside the stream's.  Grid: [decision, 7 idle, nprod block products, C, B, A work-groups]
+// (the block products start at a multiple of 8 so that their XCD-local slots hold).  The
+// decision uses the kernel's 256 threads over kDecideThreads virtual threads: the same bits
+// as the stand-alone decision.
+template <int DT, bool VEC, int XB>
+__global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, ProductArgs prod,
+                                                                 ProductArgs dec, int nprod,
+                                                                 int has_dec) {
+  extern __shared__ double lds_dyn[];
+  __shared__ uint32_t ldsu[kThreads / 64];
+  int u = blockIdx.x;
+  if (u < 8) {
+    if (u == 0 && has_dec) block_decide_body<kThreads, 1>(dec, lds_dyn);
+    return;
+  }
+  u -= 8;
+  if (u < nprod) {
+    block_product_body<XB, 2, XB * XB>(prod, u, nprod, lds_dyn);
+    return;
+  }
+  u -= nprod;
+  uint16_t* tabL = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(lds_dyn) + s.tab_off);
+  if (u < s.nC) {
+    c_unit<false, 1, VEC>(s, u, lds_dyn, tabL);
+    return;
+  }
+  u -= s.nC;
+  if (u < s.nB) {
+    if (s.transb) {
+      a_unit<DT, false, VEC>(s, w_side(s), u, lds_dyn, ldsu);
+    } else {
+      b_unit<DT, false, 8, 1, 4, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
+    }
+    return;
+  }
+  a_unit<DT, false, VEC>(s, a_side(s), u - s.nB, lds_dyn, ldsu);
+}
+
+// LDS the pipelined launch needs besides the stream pass's: the block product's reductions
+// and the decision's.
+size_t probe_pipe_lds(int xb) {
+  const size_t prod = static_cast<size_t>(xb * xb) * (kThreads + 2 * kThreads / 16 + 1);
+  const size_t dec = lds_reduce_doubles<kDecideThreads, 1>();
+  return (prod > dec ? prod : dec) * sizeof(double);
+}
+
+template <int DT, bool VEC, int XB>
+static void pipe_launch(const StreamArgs& s, const ProductArgs& prod, const ProductArgs& dec,
+                        int nprod, int has_dec, size_t lds, hipStream_t st, hipEvent_t e0,
+                        hipEvent_t e1) {
+  const dim3 grid(8 + nprod + s.nC + s.nB + s.nA);
+  launch_k(probe_pipe_kernel<DT, VEC, XB>, grid, dim3(kThreads), lds, st, e0, e1, s, prod, dec,
+           nprod, has_dec);
+}
+
+template <int DT, bool VEC>
+static hipError_t pipe_dispatch(const StreamArgs& s, const ProductArgs& prod,
+                                const ProductArgs& dec, int nprod, int has_dec, int xb,
+                                size_t lds, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  switch (xb) {
+    case 1: pipe_launch<DT, VEC, 1>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
+    case 2: pipe_launch<DT, VEC, 2>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
+    case 3: pipe_launch<DT, VEC, 3>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_probe_pipe(const StreamArgs& s, const ProductArgs& prod, const ProductArgs& dec,
+                             int nprod, int has_dec, int dt, int xb, size_t lds_bytes,
+                             hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  const bool vec = s.vec_a && s.vec_b && s.vec_c;
+  if (dt == 1) {
+    return vec ? pipe_dispatch<1, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1)
+               : pipe_dispatch<1, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1);
+  }
+  return vec ? pipe_dispatch<0, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1)
+             : pipe_dispatch<0, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1);
 }
 
 // ----------------------------------------------------------------------------------------

@@ -66,6 +66,8 @@ _SIGS = {
                                          ctypes.POINTER(Fault), _I32, ctypes.POINTER(_I32), _P]),
     "fpsketch_cache_b": (ctypes.c_int, [_P, _P, _P]),
     "fpsketch_probe_cached": (ctypes.c_int, [_P, _P, _P, ctypes.c_int, _P, _P]),
+    "fpsketch_probe_deferred": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _P, _P]),
+    "fpsketch_probe_flush": (ctypes.c_int, [_P, _P]),
     "fpsketch_apply": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, ctypes.POINTER(Fault), _I32,
                                       _U64, ctypes.POINTER(_I32), _P]),
     "fpsketch_calibrate_noise": (ctypes.c_int, [_P, _P, ctypes.c_int, _P, ctypes.POINTER(_I32),
@@ -263,6 +265,16 @@ class Verifier:
 
     def probe(self, A, B, C, d_dirty=None, stream=None, c_dtype=None):
         _check(self.probe_status(A, B, C, d_dirty, stream, c_dtype), "fpsketch_probe")
+
+    def probe_deferred(self, A, B, C, d_dirty=None, stream=None, c_dtype=None):
+        """fpsketch_probe_deferred: the verdict is final after two more deferred calls or
+        probe_flush."""
+        _check(self.lib.fpsketch_probe_deferred(self.handle, _ptr(A), _ptr(B), _ptr(C),
+                                                _c_dtype(C, c_dtype), _ptr(d_dirty),
+                                                _stream(stream)), "fpsketch_probe_deferred")
+
+    def probe_flush(self, stream=None):
+        _check(self.lib.fpsketch_probe_flush(self.handle, _stream(stream)), "fpsketch_probe_flush")
 
     def cache_b(self, B, stream=None):
         """Forms and keeps the probe's B side (B H2^T and max|B|) for the current m."""
