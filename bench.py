@@ -391,9 +391,24 @@ def main() -> int:
         v.probe_cached(A, C)
     cs_ms, cp_ms, cn = v.timing_read()
     v.timing(False)
+    for k in range(args.warmup):
+        A, C = csets[k % args.sets]
+        v.probe_cached_deferred(A, C, d_dirty=dflags[k % args.steps:k % args.steps + 1])
+    v.probe_flush()
+    dflags.zero_()
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for k in range(args.steps):
+        A, C = csets[k % args.sets]
+        v.probe_cached_deferred(A, C, d_dirty=dflags[k:k + 1])
+    v.probe_flush()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    cached_def_us = t0.elapsed_time(t1) * 1e3 / args.steps
+    assert int(dflags.sum().item()) == 0, "a clean call was reported dirty (cached, deferred)"
     bytes_ac = 2 * w.n1 * w.n2 + 4 * w.n1 * w.n3
     log(f"cached B side: {cached_us:.2f} us/call ({bytes_ac / cached_us / 1e3:.0f} GB/s of A + C), "
-        f"stream kernel {cs_ms * 1e3 / cn:.2f} us")
+        f"stream kernel {cs_ms * 1e3 / cn:.2f} us; deferred {cached_def_us:.2f} us/call")
     del csets
 
     # recovery on dirty calls
@@ -504,7 +519,8 @@ def main() -> int:
         "b_cached": {"us_per_call": round(cached_us, 3), "bytes_per_call": bytes_ac,
                      "gbs_a_c": round(bytes_ac / cached_us / 1e3, 1),
                      "stream_us": round(cs_ms * 1e3 / cn, 3),
-                     "product_decide_us": round(cp_ms * 1e3 / cn, 3)},
+                     "product_decide_us": round(cp_ms * 1e3 / cn, 3),
+                     "deferred_us_per_call": round(cached_def_us, 3)},
         "recovery": {"rate": recovery, "recovered": recovered, "above_floor": above,
                      "injected": injected, "false_positives": false_pos,
                      "localize_ms_median": round(float(np.median(loc_us)) / 1e3, 3) if loc_us

@@ -189,6 +189,12 @@ fpsketch_status fpsketch_probe_deferred(fpsketch_ctx* ctx, const void* A, const 
                                         const void* C, fpsketch_dtype c_dtype, int32_t* d_dirty,
                                         void* stream);
 
+/* fpsketch_probe_cached, deferred as fpsketch_probe_deferred (the two may be mixed in one
+ * sequence).  Errors as fpsketch_probe_cached. */
+fpsketch_status fpsketch_probe_cached_deferred(fpsketch_ctx* ctx, const void* A, const void* C,
+                                               fpsketch_dtype c_dtype, int32_t* d_dirty,
+                                               void* stream);
+
 /* Enqueues what deferred probes still owe (at most two launches); nothing pending: no-op. */
 fpsketch_status fpsketch_probe_flush(fpsketch_ctx* ctx, void* stream);
 

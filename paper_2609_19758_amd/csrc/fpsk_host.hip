@@ -1259,12 +1259,9 @@ fpsketch_status fpsketch_probe_cached(fpsketch_ctx* c, const void* A, const void
                   BSide::kUseCache);
 }
 
-fpsketch_status fpsketch_probe_deferred(fpsketch_ctx* c, const void* A, const void* B,
-                                        const void* C, fpsketch_dtype c_dtype, int32_t* d_dirty,
-                                        void* stream) {
-  FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
-  FPSK_TRY(set_device(c));
-  const hipStream_t st = static_cast<hipStream_t>(stream);
+// A deferred probe (streamed or cached B side) on the caller's stream.
+fpsketch_status deferred_probe(fpsketch_ctx* c, const void* A, const void* B, const float* C,
+                               int32_t* d_dirty, hipStream_t st, BSide bside) {
   if ((c->pipe_has_prod || c->pipe_has_dec) && st != c->pipe_stream) {
     return fail(FPSK_EINVAL, "deferred probes are pending on another stream");
   }
@@ -1272,15 +1269,15 @@ fpsketch_status fpsketch_probe_deferred(fpsketch_ctx* c, const void* A, const vo
   if (d.nX == 0 || d.xb > 3) {
     // not the pipelined path (m > 48 or n2 > 16384): an ordinary probe, nothing left pending
     FPSK_TRY(pipe_flush(c, st));
-    return run_pass(c, c->probe_round, c->probe_ws, A, B, static_cast<const float*>(C), false,
-                    1, d_dirty, nullptr, nullptr, nullptr, st);
+    return run_pass(c, c->probe_round, c->probe_ws, A, B, C, false, 1, d_dirty, nullptr, nullptr,
+                    nullptr, st, nullptr, nullptr, nullptr, bside);
   }
   Workspace& W = c->pipe_ws[c->pipe_next];
   FPSK_TRY(ensure_workspace(W, c->n1, c->n2, c->n3, c->m, false, c->transb));
   fpsk::StreamArgs s;
   fpsk::ProductArgs a;
-  FPSK_TRY(pass_args(c, c->probe_round, W, A, B, static_cast<const float*>(C), false, 1, d_dirty,
-                     nullptr, nullptr, nullptr, nullptr, nullptr, BSide::kStream, s, a));
+  FPSK_TRY(pass_args(c, c->probe_round, W, A, B, C, false, 1, d_dirty, nullptr, nullptr, nullptr,
+                     nullptr, nullptr, bside, s, a));
   const size_t lds = std::max(d.lds_stream, fpsk::probe_pipe_lds(d.xb));
   FPSK_HIP(fpsk::launch_probe_pipe(s, c->pipe_prod, c->pipe_dec,
                                    c->pipe_has_prod ? c->pipe_nprod : 0,
@@ -1295,6 +1292,28 @@ fpsketch_status fpsketch_probe_deferred(fpsketch_ctx* c, const void* A, const vo
   c->pipe_stream = st;
   c->pipe_next = (c->pipe_next + 1) % 3;
   return FPSK_OK;
+}
+
+fpsketch_status fpsketch_probe_deferred(fpsketch_ctx* c, const void* A, const void* B,
+                                        const void* C, fpsketch_dtype c_dtype, int32_t* d_dirty,
+                                        void* stream) {
+  FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
+  FPSK_TRY(set_device(c));
+  return deferred_probe(c, A, B, static_cast<const float*>(C), d_dirty,
+                        static_cast<hipStream_t>(stream), BSide::kStream);
+}
+
+fpsketch_status fpsketch_probe_cached_deferred(fpsketch_ctx* c, const void* A, const void* C,
+                                               fpsketch_dtype c_dtype, int32_t* d_dirty,
+                                               void* stream) {
+  if (c == nullptr) return fail(FPSK_EINVAL, "null context");
+  FPSK_TRY(check_matrices(c, A, c->zero.p, C, c_dtype));
+  if (c->qcache_m != c->m) {
+    return fail(FPSK_EINVAL, "no B side cached for the probe's current m (call fpsketch_cache_b)");
+  }
+  FPSK_TRY(set_device(c));
+  return deferred_probe(c, A, c->zero.p, static_cast<const float*>(C), d_dirty,
+                        static_cast<hipStream_t>(stream), BSide::kUseCache);
 }
 
 fpsketch_status fpsketch_probe_flush(fpsketch_ctx* c, void* stream) {

@@ -68,6 +68,7 @@ _SIGS = {
     "fpsketch_probe_cached": (ctypes.c_int, [_P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_probe_deferred": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_probe_flush": (ctypes.c_int, [_P, _P]),
+    "fpsketch_probe_cached_deferred": (ctypes.c_int, [_P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_apply": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, ctypes.POINTER(Fault), _I32,
                                       _U64, ctypes.POINTER(_I32), _P]),
     "fpsketch_calibrate_noise": (ctypes.c_int, [_P, _P, ctypes.c_int, _P, ctypes.POINTER(_I32),
@@ -272,6 +273,13 @@ class Verifier:
         _check(self.lib.fpsketch_probe_deferred(self.handle, _ptr(A), _ptr(B), _ptr(C),
                                                 _c_dtype(C, c_dtype), _ptr(d_dirty),
                                                 _stream(stream)), "fpsketch_probe_deferred")
+
+    def probe_cached_deferred(self, A, C, d_dirty=None, stream=None, c_dtype=None):
+        """fpsketch_probe_cached_deferred (A and C streamed, verdict after the flush)."""
+        _check(self.lib.fpsketch_probe_cached_deferred(self.handle, _ptr(A), _ptr(C),
+                                                       _c_dtype(C, c_dtype), _ptr(d_dirty),
+                                                       _stream(stream)),
+               "fpsketch_probe_cached_deferred")
 
     def probe_flush(self, stream=None):
         _check(self.lib.fpsketch_probe_flush(self.handle, _stream(stream)), "fpsketch_probe_flush")

@@ -122,3 +122,33 @@ def test_deferred_stream_mismatch_is_rejected(fk):
     v.probe_flush()
     assert v.lib.fpsketch_probe_flush(v.handle, other.cuda_stream) == fk.OK   # nothing pending
     v.close()
+
+
+def test_cached_deferred_equals_cached(fk):
+    """Deferred cached probes mixed with deferred streamed ones: every verdict and the final
+    statistics equal the ordinary calls'."""
+    import torch
+    n1, n2, n3, m, fmt = 512, 1000, 384, 40, "bf16"
+    seq = _sequence(n1, n2, n3, fmt, 6, 101)
+    B = seq[0][1]
+    vd = fk.Verifier(n1, n2, n3, fmt, m=m)
+    vs = fk.Verifier(n1, n2, n3, fmt, m=m)
+    vd.cache_b(B)
+    vs.cache_b(B)
+    fd = [torch.zeros(1, dtype=torch.int32, device="cuda") for _ in seq]
+    fs = [torch.zeros(1, dtype=torch.int32, device="cuda") for _ in seq]
+    for k, (A, _, C, _) in enumerate(seq):
+        if k % 2:
+            vd.probe_cached_deferred(A, C, d_dirty=fd[k])
+            vs.probe_cached(A, C, d_dirty=fs[k])
+        else:
+            vd.probe_deferred(A, B, C, d_dirty=fd[k])
+            vs.probe(A, B, C, d_dirty=fs[k])
+    last = vs.probe_stats()
+    vd.probe_flush()
+    torch.cuda.synchronize()
+    for k, (_, _, _, dirty) in enumerate(seq):
+        assert int(fd[k].item()) == int(fs[k].item()) == int(dirty), k
+    assert vd.probe_stats() == last
+    vd.close()
+    vs.close()
