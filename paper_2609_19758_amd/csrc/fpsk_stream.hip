@@ -683,11 +683,11 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : 4) void stream_kernel(StreamArg
 // Pipelined probe (m <= 48: output blocks of at most 3 x 3, as the 4 x 4 block's product does
 // not fit the stream pass's 128 registers; no moments): one launch runs the decision of the call
 // before the previous one, the block products of the previous call and the stream pass of this
-// call.  The
-// three read and write disjoint workspace sets, and each reads only what an earlier launch
-// wrote, so they need no ordering among themselves; the product and decision work-groups run
-// beside the stream's.  Grid: [decision, 7 idle, nprod block products, C, B, A work-groups]
-// (the block products start at a multiple of 8 so that their XCD-local slots hold).  The
+// call.  The three read and write disjoint workspace sets, and each reads only what an earlier
+// launch wrote, so they need no ordering among themselves; the product and decision
+// work-groups run beside the stream's.  Grid: [decision, 7 idle, C, B, A work-groups, idle up to a multiple of
+// 8, nprod block products]: the block products start at a multiple of 8 so that their
+// XCD-local slots hold, and come last so that they fill the stream pass's tail.  The
 // decision uses the kernel's 256 threads over kDecideThreads virtual threads: the same bits
 // as the stand-alone decision.
 template <int DT, bool VEC, int XB>
@@ -702,11 +702,12 @@ __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, P
     return;
   }
   u -= 8;
-  if (u < nprod) {
-    block_product_body<XB, 2, XB * XB>(prod, u, nprod, lds_dyn);
+  const int pbase = (s.nC + s.nB + s.nA + 7) / 8 * 8;
+  if (u >= pbase) {
+    block_product_body<XB, 2, XB * XB>(prod, u - pbase, nprod, lds_dyn);
     return;
   }
-  u -= nprod;
+  if (u >= s.nC + s.nB + s.nA) return;
   uint16_t* tabL = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(lds_dyn) + s.tab_off);
   if (u < s.nC) {
     c_unit<false, 1, VEC>(s, u, lds_dyn, tabL);
@@ -736,7 +737,7 @@ template <int DT, bool VEC, int XB>
 static void pipe_launch(const StreamArgs& s, const ProductArgs& prod, const ProductArgs& dec,
                         int nprod, int has_dec, size_t lds, hipStream_t st, hipEvent_t e0,
                         hipEvent_t e1) {
-  const dim3 grid(8 + nprod + s.nC + s.nB + s.nA);
+  const dim3 grid(8 + (s.nC + s.nB + s.nA + 7) / 8 * 8 + nprod);
   launch_k(probe_pipe_kernel<DT, VEC, XB>, grid, dim3(kThreads), lds, st, e0, e1, s, prod, dec,
            nprod, has_dec);
 }
