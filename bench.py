@@ -73,7 +73,7 @@ def cpu_baseline(w, a_bits, b_bits, c, m: int, seed: int, budget_s: float) -> di
 
 # the sources the probe's stream kernel is built from (its counters stay valid while these do)
 KERNEL_SRC = [os.path.join(ROOT, "paper_2609_19758_amd", "csrc", f)
-              for f in ("fpsk_stream.hip", "fpsk_device.h", "fpsk_internal.h")]
+              for f in ("fpsk_stream.hip", "fpsk_device.h", "fpsk_internal.h", "fpsk_block.h")]
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "stream_kernel_square4096_bf16_pmc.txt")
 
 
@@ -167,15 +167,19 @@ def write_pmc_summary(workload: str, fetch_db: str, write_db: str) -> int:
     copy_kib = 256 * 1024                  # --copy-calibration 256: 256 MiB read and written
     fs, ws = copy_kib / fetch[ck][0], copy_kib / write[ck][0]
     traffic = (fetch[sk][0] * fs + write[sk][0] * ws) * 1024.0
+    fdir = os.path.basename(os.path.dirname(os.path.abspath(fetch_db)))
+    wdir = os.path.basename(os.path.dirname(os.path.abspath(write_db)))
     lines = [
         f"# HBM traffic of the FP-Sketch probe's stream kernel, {workload}",
         "# commands (from /tmp, repo at $R), one counter per run:",
-        "#   rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/fetch21 -o run -- python3 $R/bench.py "
-        "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --copy-calibration 256",
-        "#   rocprofv3 --pmc WRITE_SIZE -d $R/gpurun_out/write21 -o run -- python3 $R/bench.py "
-        "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --copy-calibration 256",
-        "#   python3 bench.py --write-pmc-summary gpurun_out/fetch21/run_results.db "
-        "gpurun_out/write21/run_results.db",
+        f"#   rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/{fdir} -o run -- python3 $R/bench.py "
+        "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --probe-only "
+        "--copy-calibration 256",
+        f"#   rocprofv3 --pmc WRITE_SIZE -d $R/gpurun_out/{wdir} -o run -- python3 $R/bench.py "
+        "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --probe-only "
+        "--copy-calibration 256",
+        f"#   python3 bench.py --write-pmc-summary gpurun_out/{fdir}/run_results.db "
+        f"gpurun_out/{wdir}/run_results.db",
         "# scale: the copy kernel moves 262144 KiB in and 262144 KiB out per dispatch",
         f"workload={workload}",
         f"kernel={sk}",
@@ -208,6 +212,9 @@ def main() -> int:
     ap.add_argument("--workload", default="square4096_bf16")
     ap.add_argument("--sets", type=int, default=4)
     ap.add_argument("--recovery-calls", type=int, default=4)
+    ap.add_argument("--probe-only", action="store_true",
+                    help="time and profile the ordinary probe only (no graph, deferred, "
+                         "transposed or cached-B runs)")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -297,119 +304,127 @@ def main() -> int:
     p_us = prod_ms * 1e3 / ncalls
     log(f"stream kernel {k_us:.2f} us, product+decide {p_us:.2f} us (event-timed)")
 
-    # the same probe calls captured in a HIP graph (the probe only enqueues kernels): one graph of
-    # 5 rounds over the buffer sets, replayed to the same number of calls
-    per_graph = 5 * args.sets
-    g = torch.cuda.CUDAGraph()
-    cap = torch.cuda.Stream()
-    cap.wait_stream(stream)
-    with torch.cuda.stream(cap):
-        with torch.cuda.graph(g, stream=cap):
-            for k in range(per_graph):
-                A, B, C = sets[k % args.sets]
-                v.probe(A, B, C, d_dirty=flag)
-    torch.cuda.synchronize()
-    replays = max(1, args.steps // per_graph)
-    g.replay()
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for _ in range(replays):
+    # the other entry points on the same workload (skipped with --probe-only, which profiles
+    # the ordinary probe alone)
+    graph_us = deferred_us = trans_us = cached_us = cached_def_us = None
+    if not args.probe_only:
+        # the same probe calls captured in a HIP graph (the probe only enqueues kernels): one
+        # graph of 5 rounds over the buffer sets, replayed to the same number of calls
+        per_graph = 5 * args.sets
+        g = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.stream(cap):
+            with torch.cuda.graph(g, stream=cap):
+                for k in range(per_graph):
+                    A, B, C = sets[k % args.sets]
+                    v.probe(A, B, C, d_dirty=flag)
+        torch.cuda.synchronize()
+        replays = max(1, args.steps // per_graph)
         g.replay()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    graph_us = t0.elapsed_time(t1) * 1e3 / (replays * per_graph)
-    assert int(flag.item()) == 0, "a clean call was reported dirty (graph replay)"
-    log(f"probe in a HIP graph: {graph_us:.2f} us/call ({replays} replays of {per_graph} calls)")
-    del g
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(replays):
+            g.replay()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        graph_us = t0.elapsed_time(t1) * 1e3 / (replays * per_graph)
+        assert int(flag.item()) == 0, "a clean call was reported dirty (graph replay)"
+        log(f"probe in a HIP graph: {graph_us:.2f} us/call "
+            f"({replays} replays of {per_graph} calls)")
+        del g
 
-    # deferred probes: each call's launch also runs the previous call's block products and the
-    # decision of the one before; the flush after the last call is inside the timed region
-    dflags = torch.zeros(args.steps, dtype=torch.int32, device="cuda")
-    for k in range(args.warmup):
-        A, B, C = sets[k % args.sets]
-        v.probe_deferred(A, B, C, d_dirty=dflags[k % args.steps:k % args.steps + 1])
-    v.probe_flush()
-    dflags.zero_()
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for k in range(args.steps):
-        A, B, C = sets[k % args.sets]
-        v.probe_deferred(A, B, C, d_dirty=dflags[k:k + 1])
-    v.probe_flush()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    deferred_us = t0.elapsed_time(t1) * 1e3 / args.steps
-    assert int(dflags.sum().item()) == 0, "a clean call was reported dirty (deferred)"
-    log(f"deferred probes: {deferred_us:.2f} us/call ({w.bytes_abc / deferred_us / 1e3:.0f} GB/s)")
+        # deferred probes: each call's launch also runs the previous call's block products and the
+        # decision of the one before; the flush after the last call is inside the timed region
+        dflags = torch.zeros(args.steps, dtype=torch.int32, device="cuda")
+        for k in range(args.warmup):
+            A, B, C = sets[k % args.sets]
+            v.probe_deferred(A, B, C, d_dirty=dflags[k % args.steps:k % args.steps + 1])
+        v.probe_flush()
+        dflags.zero_()
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for k in range(args.steps):
+            A, B, C = sets[k % args.sets]
+            v.probe_deferred(A, B, C, d_dirty=dflags[k:k + 1])
+        v.probe_flush()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        deferred_us = t0.elapsed_time(t1) * 1e3 / args.steps
+        assert int(dflags.sum().item()) == 0, "a clean call was reported dirty (deferred)"
+        log(f"deferred probes: {deferred_us:.2f} us/call "
+            f"({w.bytes_abc / deferred_us / 1e3:.0f} GB/s)")
 
-    # B passed transposed (a linear layer's weight W = B^T, n3 x n2): the same products, a context
-    # with b_layout = 1 at the calibrated m
-    vt = fk.Verifier(w.n1, w.n2, w.n3, w.fmt, m=v.m, rho_min=w.rho_min, s_budget=w.s_budget,
-                     b_layout=1)
-    tsets = [(A, B.t().contiguous(), C) for A, B, C in sets]
-    for k in range(args.warmup):
-        A, Wt, C = tsets[k % args.sets]
-        vt.probe(A, Wt, C, d_dirty=flag)
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for k in range(args.steps):
-        A, Wt, C = tsets[k % args.sets]
-        vt.probe(A, Wt, C, d_dirty=flag)
-    t1.record(stream)
-    torch.cuda.synchronize()
-    trans_us = t0.elapsed_time(t1) * 1e3 / args.steps
-    assert int(flag.item()) == 0, "a clean call was reported dirty (B transposed)"
-    vt.timing(True)
-    for k in range(args.steps):
-        A, Wt, C = tsets[k % args.sets]
-        vt.probe(A, Wt, C)
-    ts_ms, tp_ms, tn = vt.timing_read()
-    vt.close()
-    del tsets
-    log(f"B transposed: {trans_us:.2f} us/call, stream kernel {ts_ms * 1e3 / tn:.2f} us")
+        # B passed transposed (a linear layer's weight W = B^T, n3 x n2): the same products, a
+        # context with b_layout = 1 at the calibrated m
+        vt = fk.Verifier(w.n1, w.n2, w.n3, w.fmt, m=v.m, rho_min=w.rho_min, s_budget=w.s_budget,
+                         b_layout=1)
+        tsets = [(A, B.t().contiguous(), C) for A, B, C in sets]
+        for k in range(args.warmup):
+            A, Wt, C = tsets[k % args.sets]
+            vt.probe(A, Wt, C, d_dirty=flag)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for k in range(args.steps):
+            A, Wt, C = tsets[k % args.sets]
+            vt.probe(A, Wt, C, d_dirty=flag)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        trans_us = t0.elapsed_time(t1) * 1e3 / args.steps
+        assert int(flag.item()) == 0, "a clean call was reported dirty (B transposed)"
+        vt.timing(True)
+        for k in range(args.steps):
+            A, Wt, C = tsets[k % args.sets]
+            vt.probe(A, Wt, C)
+        ts_ms, tp_ms, tn = vt.timing_read()
+        vt.close()
+        del tsets
+        log(f"B transposed: {trans_us:.2f} us/call, stream kernel {ts_ms * 1e3 / tn:.2f} us")
 
-    # the probe with the B side cached (the paper's probe keeps BH2^T of the weight): one weight,
-    # the activations of every buffer set, their products C = A_k B_0; A and C streamed
-    B0 = sets[0][1]
-    csets = [(sets[k][0], gemm_f32(sets[k][0], B0)) for k in range(args.sets)]
-    v.cache_b(B0)
-    for k in range(args.warmup):
-        A, C = csets[k % args.sets]
-        v.probe_cached(A, C, d_dirty=flag)
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for k in range(args.steps):
-        A, C = csets[k % args.sets]
-        v.probe_cached(A, C, d_dirty=flag)
-    t1.record(stream)
-    torch.cuda.synchronize()
-    cached_us = t0.elapsed_time(t1) * 1e3 / args.steps
-    assert int(flag.item()) == 0, "a clean call was reported dirty (cached B side)"
-    v.timing(True)
-    for k in range(args.steps):
-        A, C = csets[k % args.sets]
-        v.probe_cached(A, C)
-    cs_ms, cp_ms, cn = v.timing_read()
-    v.timing(False)
-    for k in range(args.warmup):
-        A, C = csets[k % args.sets]
-        v.probe_cached_deferred(A, C, d_dirty=dflags[k % args.steps:k % args.steps + 1])
-    v.probe_flush()
-    dflags.zero_()
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for k in range(args.steps):
-        A, C = csets[k % args.sets]
-        v.probe_cached_deferred(A, C, d_dirty=dflags[k:k + 1])
-    v.probe_flush()
-    t1.record(stream)
-    torch.cuda.synchronize()
-    cached_def_us = t0.elapsed_time(t1) * 1e3 / args.steps
-    assert int(dflags.sum().item()) == 0, "a clean call was reported dirty (cached, deferred)"
-    bytes_ac = 2 * w.n1 * w.n2 + 4 * w.n1 * w.n3
-    log(f"cached B side: {cached_us:.2f} us/call ({bytes_ac / cached_us / 1e3:.0f} GB/s of A + C), "
-        f"stream kernel {cs_ms * 1e3 / cn:.2f} us; deferred {cached_def_us:.2f} us/call")
-    del csets
+        # the probe with the B side cached (the paper's probe keeps BH2^T of the weight): one
+        # weight, the activations of every buffer set, their products C = A_k B_0; A and C
+        # streamed
+        B0 = sets[0][1]
+        csets = [(sets[k][0], gemm_f32(sets[k][0], B0)) for k in range(args.sets)]
+        v.cache_b(B0)
+        for k in range(args.warmup):
+            A, C = csets[k % args.sets]
+            v.probe_cached(A, C, d_dirty=flag)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for k in range(args.steps):
+            A, C = csets[k % args.sets]
+            v.probe_cached(A, C, d_dirty=flag)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        cached_us = t0.elapsed_time(t1) * 1e3 / args.steps
+        assert int(flag.item()) == 0, "a clean call was reported dirty (cached B side)"
+        v.timing(True)
+        for k in range(args.steps):
+            A, C = csets[k % args.sets]
+            v.probe_cached(A, C)
+        cs_ms, cp_ms, cn = v.timing_read()
+        v.timing(False)
+        for k in range(args.warmup):
+            A, C = csets[k % args.sets]
+            v.probe_cached_deferred(A, C, d_dirty=dflags[k % args.steps:k % args.steps + 1])
+        v.probe_flush()
+        dflags.zero_()
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for k in range(args.steps):
+            A, C = csets[k % args.sets]
+            v.probe_cached_deferred(A, C, d_dirty=dflags[k:k + 1])
+        v.probe_flush()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        cached_def_us = t0.elapsed_time(t1) * 1e3 / args.steps
+        assert int(dflags.sum().item()) == 0, "a clean call was reported dirty (cached, deferred)"
+        bytes_ac = 2 * w.n1 * w.n2 + 4 * w.n1 * w.n3
+        log(f"cached B side: {cached_us:.2f} us/call "
+            f"({bytes_ac / cached_us / 1e3:.0f} GB/s of A + C), "
+            f"stream kernel {cs_ms * 1e3 / cn:.2f} us; deferred {cached_def_us:.2f} us/call")
+        del csets
 
     # recovery on dirty calls
     injected = recovered = false_pos = above = 0
@@ -510,17 +525,20 @@ def main() -> int:
         "kernel_us": {"stream": round(k_us, 3), "product_decide": round(p_us, 3)},
         "gemm_us": round(gemm_us, 2),
         "graph": {"us_per_call": round(graph_us, 3), "calls_per_graph": per_graph,
-                  "replays": replays},
+                  "replays": replays} if graph_us is not None else None,
         "deferred": {"us_per_call": round(deferred_us, 3),
-                     "gbs": round(w.bytes_abc / deferred_us / 1e3, 1)},
+                     "gbs": round(w.bytes_abc / deferred_us / 1e3, 1)}
+        if deferred_us is not None else None,
         "b_transposed": {"us_per_call": round(trans_us, 3),
                          "stream_us": round(ts_ms * 1e3 / tn, 3),
-                         "product_decide_us": round(tp_ms * 1e3 / tn, 3)},
+                         "product_decide_us": round(tp_ms * 1e3 / tn, 3)}
+        if trans_us is not None else None,
         "b_cached": {"us_per_call": round(cached_us, 3), "bytes_per_call": bytes_ac,
                      "gbs_a_c": round(bytes_ac / cached_us / 1e3, 1),
                      "stream_us": round(cs_ms * 1e3 / cn, 3),
                      "product_decide_us": round(cp_ms * 1e3 / cn, 3),
-                     "deferred_us_per_call": round(cached_def_us, 3)},
+                     "deferred_us_per_call": round(cached_def_us, 3)}
+        if cached_us is not None else None,
         "recovery": {"rate": recovery, "recovered": recovered, "above_floor": above,
                      "injected": injected, "false_positives": false_pos,
                      "localize_ms_median": round(float(np.median(loc_us)) / 1e3, 3) if loc_us

@@ -685,9 +685,10 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : 4) void stream_kernel(StreamArg
 // before the previous one, the block products of the previous call and the stream pass of this
 // call.  The three read and write disjoint workspace sets, and each reads only what an earlier
 // launch wrote, so they need no ordering among themselves; the product and decision
-// work-groups run beside the stream's.  Grid: [decision, 7 idle, C, B, A work-groups, idle up to a multiple of
-// 8, nprod block products]: the block products start at a multiple of 8 so that their
-// XCD-local slots hold, and come last so that they fill the stream pass's tail.  The
+// work-groups run beside the stream's.  Grid: [decision, 7 idle, C, B, A work-groups, idle
+// up to a multiple of 8, nprod block products]: the block products start at a multiple of 8
+// so that their XCD-local slots hold, and come last so that they fill the stream pass's
+// tail.  The
 // decision uses the kernel's 256 threads over kDecideThreads virtual threads: the same bits
 // as the stand-alone decision.
 template <int DT, bool VEC, int XB>
