@@ -757,6 +757,9 @@ fpsketch_status pass_args(fpsketch_ctx* c, const DevRound& R, Workspace& W, cons
   a.ldp = d.ldp;
   a.kact = d.kact;
   a.nt = d.nt;
+  a.ts = d.ts;
+  // large m: the clipped sum of the decision spread over one work-group per tile
+  a.clip_tiles = (mode == 1 && !mom && d.nX == 0 && d.m >= 192) ? 1 : 0;
   a.NS = d.NS;
   a.ksl = d.ksl;
   a.npc = d.npc;

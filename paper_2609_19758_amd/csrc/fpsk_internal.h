@@ -86,11 +86,14 @@ struct ProductArgs {
   double* R;
   double* T;
   double* scratch;      // NS x tiles x ts^2 (x 3 with moments) slice partials, row-major tiles
-  double* tilestat;     // tiles x 4: sum|S|, max|S|, non-finite count
+  double* tilestat;     // tiles x 4: sum|S|, max|S|, non-finite count, clipped sum
   int m, n2, nt, NS, ksl, npc;
   int ldp;              // row stride of the factors
   int kact;             // k-range the products cover: n2 rounded up to a multiple of 4
   int mode;             // 0: sketch only; 1: probe decision
+  int ts;               // tile edge of the tile path
+  int clip_tiles;       // probe, large m: clip_kernel writes each tile's clipped sum to
+                        // tilestat[4 tile + 3] and the decision adds those
   const float* maxpart;
   int nA, nB;
   const float* maxpart_b; // max |B| per B work-group when the B side is cached, else null

@@ -309,8 +309,66 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(ProductArgs pa) {
 // The probe's decision after the tile path (one work-group of 1024): the tile statistics and
 // operand maxima in one reduction, then the clipped sum over S, whose first 16 x 1024 entries
 // were loaded with the statistics.
+// The tile statistics reduced as the decision reduces them (1024 virtual threads, the same
+// bits on any work-group size): sum|S|, max|S|, non-finite count.
+template <int NTR>
+__device__ void tile_totals(const ProductArgs& pa, double* red, double (&out)[3]) {
+  constexpr int N = kDecideThreads;
+  constexpr int VT = N / NTR;
+  const int ntiles = pa.nt * pa.nt;
+  double v[VT][3];
+#pragma unroll
+  for (int j = 0; j < VT; ++j) {
+    double lsum = 0.0, lmax = 0.0, lbad = 0.0;
+    for (int i = threadIdx.x + NTR * j; i < ntiles; i += N) {
+      lsum += pa.tilestat[i * 4 + 0];
+      lmax = fmax(lmax, pa.tilestat[i * 4 + 1]);
+      lbad += pa.tilestat[i * 4 + 2];
+    }
+    v[j][0] = lsum;
+    v[j][1] = lmax;
+    v[j][2] = lbad;
+  }
+  if constexpr (VT == 1) {
+#pragma unroll
+    for (int i = 0; i < 3; ++i) out[i] = v[0][i];
+    lds_reduce<N, 3>(out, red, 0x2u);
+  } else {
+    lds_reduce_virtual<N, 3, NTR>(v, red, 0x2u, out);
+  }
+}
+
+// Probe, large m: one work-group per tile forms the global clip 5 mean|S| from the tile
+// statistics (the decision's own reduction, so the same clip) and, when some bucket reaches it,
+// the tile's sum of min(|S|, clip) into tilestat[4 tile + 3] (fixed order: thread partials over
+// the tile's row-major buckets, then the work-group reduction).  Replaces one work-group's pass
+// over all m^2 buckets.
+__global__ __launch_bounds__(kThreads) void clip_kernel(ProductArgs pa) {
+  __shared__ double red[lds_reduce_doubles<kDecideThreads, 1>()];
+  double tot[3];
+  tile_totals<kThreads>(pa, red, tot);
+  const int m = pa.m;
+  const double mm = static_cast<double>(m) * m;
+  const double mean_abs = tot[2] > 0.0 ? __builtin_nan("") : tot[0] / mm;
+  const double clip = 5.0 * mean_abs;
+  if (tot[2] == 0.0 && tot[1] <= clip) return;
+  const int tile = blockIdx.x;
+  const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
+  const int ts = pa.ts;
+  double c2 = 0.0;
+  for (int e = threadIdx.x; e < ts * ts; e += kThreads) {
+    const int r = ta * ts + e / ts, c = tb * ts + e % ts;
+    if (r < m && c < m) {
+      const double a = fabs(pa.S[static_cast<int64_t>(r) * m + c]);
+      c2 += a < clip ? a : clip;
+    }
+  }
+  double r1[1] = {c2};
+  lds_reduce<kThreads, 1>(r1, red, 0u);
+  if (threadIdx.x == 0) pa.tilestat[tile * 4 + 3] = r1[0];
+}
+
 __global__ __launch_bounds__(kDecideThreads) void tile_decide_kernel(ProductArgs pa) {
-  constexpr int NQ = 16;
   __shared__ double red[5 * (kDecideThreads + 2 * kDecideThreads / 16 + 1)];
   const int t = threadIdx.x;
   // the running noise sum, read now so that the verdict does not wait on it
@@ -321,18 +379,13 @@ __global__ __launch_bounds__(kDecideThreads) void tile_decide_kernel(ProductArgs
   }
   const int64_t mm = static_cast<int64_t>(pa.m) * pa.m;
   const int ntiles = pa.nt * pa.nt;
-  double v[NQ];
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const int64_t o = t + static_cast<int64_t>(kDecideThreads) * q;
-    v[q] = o < mm ? pa.S[o] : 0.0;
-  }
   double lsum = 0.0, lmax = 0.0, lbad = 0.0;
   for (int i = t; i < ntiles; i += kDecideThreads) {
     lsum += pa.tilestat[i * 4 + 0];
     lmax = fmax(lmax, pa.tilestat[i * 4 + 1]);
     lbad += pa.tilestat[i * 4 + 2];
   }
+  // (the same partials and tree as tile_totals, with the maxima of A and B as values 3 and 4)
   float amax = 0.0f, bmax = 0.0f;
   for (int i = t; i < pa.nA; i += kDecideThreads) amax = fmaxf(amax, pa.maxpart[i]);
   const float* mb = pa.maxpart_b != nullptr ? pa.maxpart_b : pa.maxpart + pa.nA;
@@ -344,21 +397,25 @@ __global__ __launch_bounds__(kDecideThreads) void tile_decide_kernel(ProductArgs
   // mean|S| over all buckets (a non-finite bucket makes the mean non-finite)
   const double mean_abs = nbad > 0.0 ? __builtin_nan("") : sum_abs / static_cast<double>(mm);
   const double clip = 5.0 * mean_abs;
-  double c2 = 0.0;
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    const int64_t o = t + static_cast<int64_t>(kDecideThreads) * q;
-    const double a = fabs(v[q]);
-    if (o < mm) c2 += a < clip ? a : clip;
-  }
+  // When no bucket reaches the clip (the usual clean case) the clipped sum is sum|S| itself and
+  // S is not read again; otherwise a pass over S.
+  double clipped = sum_abs;
+  if (!(nbad == 0.0 && max_abs <= clip)) {
+    double c2 = 0.0;
+    if (pa.clip_tiles) {
+      for (int i = t; i < ntiles; i += kDecideThreads) c2 += pa.tilestat[i * 4 + 3];
+    } else {
 #pragma unroll 8
-  for (int64_t o = t + static_cast<int64_t>(kDecideThreads) * NQ; o < mm; o += kDecideThreads) {
-    const double a = fabs(pa.S[o]);
-    c2 += a < clip ? a : clip;
+      for (int64_t o = t; o < mm; o += kDecideThreads) {
+        const double a = fabs(pa.S[o]);
+        c2 += a < clip ? a : clip;
+      }
+    }
+    double r1[1] = {c2};
+    lds_reduce<kDecideThreads, 1>(r1, red, 0u);
+    clipped = r1[0];
   }
-  double r1[1] = {c2};
-  lds_reduce<kDecideThreads, 1>(r1, red, 0u);
-  if (t == 0) decide_tail(pa, sum_abs, max_abs, nbad, r1[0], r5[3], r5[4], acc0, acc1);
+  if (t == 0) decide_tail(pa, sum_abs, max_abs, nbad, clipped, r5[3], r5[4], acc0, acc1);
 }
 
 // ----------------------------------------------------------------------------------------
@@ -655,6 +712,9 @@ hipError_t launch_product(const ProductArgs& a0, int ts, bool kw, bool moments, 
     if (red) {                                                                              \
       launch_k(reduce_kernel<TS_, MOM_>, rgrid, dim3(kThreads), 0, st, nullptr,             \
                dec ? nullptr : e1, a);                                                      \
+    }                                                                                       \
+    if (dec && a.clip_tiles) {                                                              \
+      launch_k(clip_kernel, rgrid, dim3(kThreads), 0, st, nullptr, nullptr, a);             \
     }                                                                                       \
     if (dec) launch_k(tile_decide_kernel, dim3(1), dim3(kDecideThreads), 0, st, nullptr, e1, a); \
     return hipGetLastError();                                                               \
