@@ -174,8 +174,8 @@ fpsketch_status fpsketch_probe_cached(fpsketch_ctx* ctx, const void* A, const vo
                                       fpsketch_dtype c_dtype, int32_t* d_dirty, void* stream);
 
 /* fpsketch_probe without waiting for its own product and decision (Sec. III-C: the verdict is a
- * device flag the caller reads later).  For the probe's block path up to m = 48 (n2 <= 16384)
- * each call enqueues ONE launch holding the decision of the call before the previous one, the
+ * device flag the caller reads later).  For the probe's block path (m <= 64, n2 <= 16384) each
+ * call enqueues ONE launch holding the decision of the call before the previous one, the
  * block products of the previous call and this call's pass over A, B and C; these run side by side
  * on three workspace sets in rotation, with the same arithmetic, hence the same bits, as
  * fpsketch_probe.  A call's verdict (ORed into its d_dirty), its statistics and its share of the

@@ -408,7 +408,10 @@ struct Decomp {
   int xsr = 1, xsc = 1, xnstc = 1, xslots = 0;   // supertiles of blocks (XCD-local sets)
 };
 
-Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool transb) {
+// pipe: the deferred probe's decomposition, whose output blocks stay at most 3 x 3 (the
+// pipelined launch holds the block product within the stream pass's registers).
+Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool transb,
+                 bool pipe = false) {
   (void)n1;
   Decomp d;
   d.m = m;
@@ -487,6 +490,7 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   const int xns = static_cast<int>((d.kact + fpsk::kXSlice - 1) / fpsk::kXSlice);
   if (!mom && m <= 64 && xns <= fpsk::kMaxXSlices) {
     d.xb = (m + 15) / 16;
+    if (pipe && d.xb > 3) d.xb = 3;
     d.xnb = (m + d.xb - 1) / d.xb;
     d.xns = xns;
     // The 8 XCDs take launch indices round-robin, and the kernel maps index i to slot
@@ -553,8 +557,8 @@ struct Workspace {
 };
 
 fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n3, int m,
-                                 bool mom, bool transb) {
-  const Decomp d = decompose(n1, n2, n3, m, mom, transb);
+                                 bool mom, bool transb, bool pipe = false) {
+  const Decomp d = decompose(n1, n2, n3, m, mom, transb, pipe);
   W.d = d;
   W.mom = mom;
   // factor rows are ldp long; the padding past n2 is never written and stays zero
@@ -1268,15 +1272,15 @@ fpsketch_status deferred_probe(fpsketch_ctx* c, const void* A, const void* B, co
   if ((c->pipe_has_prod || c->pipe_has_dec) && st != c->pipe_stream) {
     return fail(FPSK_EINVAL, "deferred probes are pending on another stream");
   }
-  const Decomp& d = c->probe_ws.d;
-  if (d.nX == 0 || d.xb > 3) {
-    // not the pipelined path (m > 48 or n2 > 16384): an ordinary probe, nothing left pending
+  if (c->probe_ws.d.nX == 0) {
+    // not the block path (m > 64 or n2 > 16384): an ordinary probe, nothing left pending
     FPSK_TRY(pipe_flush(c, st));
     return run_pass(c, c->probe_round, c->probe_ws, A, B, C, false, 1, d_dirty, nullptr, nullptr,
                     nullptr, st, nullptr, nullptr, nullptr, bside);
   }
   Workspace& W = c->pipe_ws[c->pipe_next];
-  FPSK_TRY(ensure_workspace(W, c->n1, c->n2, c->n3, c->m, false, c->transb));
+  FPSK_TRY(ensure_workspace(W, c->n1, c->n2, c->n3, c->m, false, c->transb, true));
+  const Decomp& d = W.d;
   fpsk::StreamArgs s;
   fpsk::ProductArgs a;
   FPSK_TRY(pass_args(c, c->probe_round, W, A, B, C, false, 1, d_dirty, nullptr, nullptr, nullptr,

@@ -680,8 +680,8 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : 4) void stream_kernel(StreamArg
 }
 
 // ----------------------------------------------------------------------------------------
-// Pipelined probe (m <= 48: output blocks of at most 3 x 3, as the 4 x 4 block's product does
-// not fit the stream pass's 128 registers; no moments): one launch runs the decision of the call
+// Pipelined probe (m <= 64, no moments; output blocks of at most 3 x 3, as the 4 x 4 block's
+// product does not fit the stream pass's 128 registers): one launch runs the decision of the call
 // before the previous one, the block products of the previous call and the stream pass of this
 // call.  The three read and write disjoint workspace sets, and each reads only what an earlier
 // launch wrote, so they need no ordering among themselves; the product and decision
