@@ -446,16 +446,17 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   // Bucket-space product on the matrix cores, tiles of ts x ts outputs over NS k-slices.
   // Without moments: 16 x 16 tiles whose k-range the 4 waves split, while there are fewer than
   // 256 of them (slices for about 2048 waves); else 64 x 64 tiles of four 32 x 32 wave quadrants.
-  // With moments: four 16 x 16 quadrants (32 x 32 tiles) up to m = 128, then 64 x 64.  Without
-  // the split, slices for about 1024 work-groups.  A wave takes k in steps of 16; at most 32
-  // slices.
+  // With moments: four 16 x 16 quadrants (32 x 32 tiles) up to m = 2048 (the 64 x 64 tile's
+  // three accumulator sets leave one wave per SIMD: 1.1 to 1.8x slower at m = 256 to 1024), then
+  // 64 x 64 (its operand reuse wins at m = 4096).  Without the split, slices for about 1024
+  // work-groups.  A wave takes k in steps of 16; at most 32 slices.
   if (!mom) {
     const int t16 = (m + 15) / 16;
     d.kw = t16 * t16 < 256;
     d.ts = d.kw ? 16 : 64;
   } else {
     d.kw = false;
-    d.ts = m <= 128 ? 32 : 64;
+    d.ts = m <= 2048 ? 32 : 64;
   }
   d.nt = (m + d.ts - 1) / d.ts;
   const int tiles = d.nt * d.nt;
