@@ -273,7 +273,10 @@ def main() -> int:
     for k in range(w.calib_calls):
         A, B, C = sets[k % args.sets]
         v.probe(A, B, C, d_dirty=flag)
+    torch.cuda.synchronize()
+    tc0 = time.perf_counter()
     m_cal, sigma_bar, rebuilt = v.calibrate_noise(sets[0][2])
+    calib_us = (time.perf_counter() - tc0) * 1e6
     log(f"calibration: m {m0} -> {m_cal} (sigma_bar {sigma_bar:.4g}, rebuilt {rebuilt})")
 
     for k in range(args.warmup):
@@ -303,6 +306,35 @@ def main() -> int:
     k_us = stream_ms * 1e3 / ncalls
     p_us = prod_ms * 1e3 / ncalls
     log(f"stream kernel {k_us:.2f} us, product+decide {p_us:.2f} us (event-timed)")
+
+    # per-call distribution: each call bracketed by its own events on the stream
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for k in range(args.steps):
+        A, B, C = sets[k % args.sets]
+        evs[k][0].record(stream)
+        v.probe(A, B, C, d_dirty=flag)
+        evs[k][1].record(stream)
+    torch.cuda.synchronize()
+    per_call = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+    p10, p50, p90 = (float(np.percentile(per_call, q)) for q in (10, 50, 90))
+    log(f"per call: median {p50:.2f} us, p10 {p10:.2f}, p90 {p90:.2f}")
+
+    # the achievable line: the library's plain read kernel over 512 MiB, same box
+    rd_bytes = 512 << 20
+    rbuf = torch.empty(rd_bytes // 4, dtype=torch.float32, device="cuda")
+    rout = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        fk.stream_read(rbuf, rd_bytes, rout, 2048)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(10):
+        fk.stream_read(rbuf, rd_bytes, rout, 2048)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    read_gbs = rd_bytes * 10 / (t0.elapsed_time(t1) * 1e-3) / 1e9
+    del rbuf
+    log(f"plain read of 512 MiB: {read_gbs:.0f} GB/s")
 
     # the other entry points on the same workload (skipped with --probe-only, which profiles
     # the ordinary probe alone)
@@ -524,6 +556,9 @@ def main() -> int:
         "us_per_call": round(ms_per * 1e3, 3),
         "kernel_us": {"stream": round(k_us, 3), "product_decide": round(p_us, 3)},
         "gemm_us": round(gemm_us, 2),
+        "per_call_us": {"median": round(p50, 3), "p10": round(p10, 3), "p90": round(p90, 3)},
+        "plain_read_gbs": round(read_gbs, 1),
+        "calibrate_us": round(calib_us, 1),
         "graph": {"us_per_call": round(graph_us, 3), "calls_per_graph": per_graph,
                   "replays": replays} if graph_us is not None else None,
         "deferred": {"us_per_call": round(deferred_us, 3),
