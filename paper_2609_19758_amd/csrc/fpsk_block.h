@@ -256,7 +256,7 @@ template <int NTR, int SB>
 __device__ void block_decide_body(const ProductArgs& pa, double* red) {
   constexpr int N = kDecideThreads;
   constexpr int VT = N / NTR;
-  constexpr int NQ = 4;                       // m <= 64: m^2 <= 4096 outputs
+  constexpr int NQ = 4096 / N;                // m <= 64: m^2 <= 4096 outputs
   const int m = pa.m;
   const int mm = m * m;
   const int t = threadIdx.x;
