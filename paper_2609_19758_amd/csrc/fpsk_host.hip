@@ -406,6 +406,8 @@ struct Decomp {
   // probe block product (nX > 0): work-groups of xb x xb outputs over xns k-slices
   int xb = 0, xnb = 0, xns = 0, nX = 0;
   int xsr = 1, xsc = 1, xnstc = 1, xslots = 0;   // supertiles of blocks (XCD-local sets)
+  // B work-groups of fewer than 8 rows write Q k-major (n2 x m), then a transpose forms Q
+  bool qk = false;
 };
 
 // pipe: the deferred probe's decomposition, whose output blocks stay at most 3 x 3 (the
@@ -437,6 +439,7 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.nB = static_cast<int>((n2 + d.rb - 1) / d.rb);
   // B passed transposed: row-bucket work-groups over the rows of W = B^T, as many as A's
   if (transb) d.nB = m * d.TA;
+  d.qk = !transb && d.rb < 8;
   d.TC = static_cast<int>((n3 + kColTile - 1) / kColTile);
   int npc = static_cast<int>((1024 + m - 1) / m);
   npc = std::max(1, std::min(npc, d.TC));
@@ -555,6 +558,7 @@ struct Workspace {
   bool mom = false;
   DevBuf P, Pw, Q, Qw, partS, partR, partT, scratch, S, R, T, maxpart, tilestat;
   DevBuf xpart;                // probe block-product partials
+  DevBuf Qk, Qwk;              // k-major B-side rows (qk passes), transposed into Q, Qw
 };
 
 fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n3, int m,
@@ -585,12 +589,17 @@ fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n
   FPSK_TRY(dev_alloc(W.maxpart, static_cast<size_t>(d.nA + d.nB) * sizeof(float)));
   FPSK_TRY(dev_alloc(W.tilestat, static_cast<size_t>(tiles) * 4 * sizeof(double)));
   if (d.nX > 0) FPSK_TRY(dev_alloc(W.xpart, static_cast<size_t>(d.xns) * mm));
+  if (d.qk) {
+    const size_t qk = static_cast<size_t>(n2) * static_cast<size_t>(m) * sizeof(float);
+    FPSK_TRY(dev_alloc(W.Qk, qk));
+    if (mom) FPSK_TRY(dev_alloc(W.Qwk, qk));
+  }
   return FPSK_OK;
 }
 
 void free_workspace(Workspace& W) {
   for (DevBuf* b : {&W.P, &W.Pw, &W.Q, &W.Qw, &W.partS, &W.partR, &W.partT, &W.scratch, &W.S,
-                    &W.R, &W.T, &W.maxpart, &W.tilestat, &W.xpart}) {
+                    &W.R, &W.T, &W.maxpart, &W.tilestat, &W.xpart, &W.Qk, &W.Qwk}) {
     dev_free(*b);
   }
 }
@@ -735,6 +744,11 @@ fpsketch_status pass_args(fpsketch_ctx* c, const DevRound& R, Workspace& W, cons
     return fail(FPSK_EINVAL, "internal: tables do not match the pass");
   }
   s.ldp = d.ldp;
+  if (d.qk) {
+    s.Qk = as<float>(W.Qk);
+    s.Qwk = mom ? as<float>(W.Qwk) : nullptr;
+    s.mq = d.m;
+  }
   if (bside == BSide::kFillCache) {
     // B work-groups only, into the cache (Q and the per-work-group max |B|)
     s.nA = 0;
@@ -814,12 +828,19 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   if (bside == BSide::kFillCache) {
     FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, false, d.rb, d.g, d.ng,
                                  d.lds_stream, st));
+    if (d.qk) {
+      FPSK_HIP(fpsk::launch_transpose_q(s.Qk, s.Q, d.m, c->n2, s.mq, d.ldp, st));
+    }
     return FPSK_OK;
   }
   // with ev: the dispatches themselves time-stamp ev[0..1] (stream kernel) and ev[2..3]
   // (first product dispatch start to last dispatch end)
   FPSK_HIP(fpsk::launch_stream(s, c->dt == FPSK_BF16 ? 1 : 0, mom, d.rb, d.g, d.ng,
                                d.lds_stream, st, ev ? ev[0] : nullptr, ev ? ev[1] : nullptr));
+  if (d.qk && s.nB > 0) {
+    FPSK_HIP(fpsk::launch_transpose_q(s.Qk, s.Q, d.m, c->n2, s.mq, d.ldp, st));
+    if (mom) FPSK_HIP(fpsk::launch_transpose_q(s.Qwk, s.Qw, d.m, c->n2, s.mq, d.ldp, st));
+  }
   FPSK_HIP(fpsk::launch_product(a, d.ts, d.kw, mom, st, ev ? ev[2] : nullptr,
                                 ev ? ev[3] : nullptr));
   return FPSK_OK;

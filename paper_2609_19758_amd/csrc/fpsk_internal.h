@@ -55,6 +55,12 @@ struct StreamArgs {
   float* Q;        // m x ldp      (B H2^T)^T: row b holds column b of B H2^T
   float* Qw;       // m x ldp      (B W2 H2^T)^T      (moments only)
   int ldp;
+  // B work-groups of fewer than 8 rows (m > 512) write Q (Qw) k-major instead, n2 x mq, for a
+  // transpose into Q: a bucket-major row per work-group would be a 16-byte or smaller piece per
+  // bucket, each a partial line write; null otherwise
+  float* Qk;
+  float* Qwk;
+  int mq;
   double* partS;   // npc x m x m  partial H1 C H2^T over column-tile groups
   double* partR;   // npc x m x m  partial H1 W1 C H2^T
   double* partT;   // npc x m x m  partial H1 C W2 H2^T
@@ -134,6 +140,9 @@ hipError_t launch_scan_extract(const float* C, int64_t n3, const int32_t* rows,
 hipError_t launch_sample(const float* C, int64_t stride, int64_t count, float* out,
                          hipStream_t st);
 // B[k][j] is read at B + k * bsk + j * bsj (n3, 1 for B as stored; 1, n2 for W = B^T).
+// dst (m x ldp) = transpose of src (n2 x mq), columns past m and rows past n2 left alone.
+hipError_t launch_transpose_q(const float* src, float* dst, int m, int64_t n2, int mq, int ldp,
+                              hipStream_t st);
 hipError_t launch_recheck(const uint16_t* A, const uint16_t* B, int64_t bsk, int64_t bsj,
                           const float* C, int64_t n2, int64_t n3, int dt, const int64_t* coords,
                           int n, double* gamma, double* abssum, float* cval, hipStream_t st);

@@ -419,6 +419,34 @@ __global__ __launch_bounds__(kDecideThreads) void tile_decide_kernel(ProductArgs
 }
 
 // ----------------------------------------------------------------------------------------
+// Q from the k-major rows of the B work-groups: 64 x 64 tiles through LDS (rows padded to 65
+// floats), read along the buckets and written along k, both coalesced.
+
+__global__ __launch_bounds__(kThreads) void transpose_q_kernel(const float* src, float* dst,
+                                                               int m, int64_t n2, int mq,
+                                                               int ldp) {
+  __shared__ float tile[64][65];
+  const int64_t tk = static_cast<int64_t>(blockIdx.x) * 64;
+  const int tb = blockIdx.y * 64;
+  const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int r = r0 + 4 * j;
+    const int64_t k = tk + r;
+    const int b = tb + c;
+    tile[r][c] = (k < n2 && b < m) ? src[k * mq + b] : 0.0f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int r = r0 + 4 * j;
+    const int b = tb + r;
+    const int64_t k = tk + c;
+    if (b < m && k < n2) dst[static_cast<int64_t>(b) * ldp + k] = tile[c][r];
+  }
+}
+
+// ----------------------------------------------------------------------------------------
 // Exact scan (non-finite or |C| > fp32max/16), samples, recheck.
 
 __device__ __forceinline__ bool is_absolute_entry(float x) {
@@ -797,6 +825,14 @@ hipError_t launch_above(const double* S, const double* R, const double* T, int64
                         double cut, Cand* out, uint32_t cap, uint32_t* count, hipStream_t st) {
   hipLaunchKernelGGL(above_kernel, dim3(grid_for(n)), dim3(kThreads), 0, st, S, R, T, n, cut,
                      out, cap, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_q(const float* src, float* dst, int m, int64_t n2, int mq, int ldp,
+                              hipStream_t st) {
+  if (m <= 0 || n2 <= 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((n2 + 63) / 64), static_cast<unsigned>((m + 63) / 64));
+  hipLaunchKernelGGL(transpose_q_kernel, grid, dim3(kThreads), 0, st, src, dst, m, n2, mq, ldp);
   return hipGetLastError();
 }
 

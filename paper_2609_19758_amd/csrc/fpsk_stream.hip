@@ -476,8 +476,14 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
       for (int r = 0; r < RBG; ++r) {
         const int64_t k = k0 + rg * RBG + r;
         if (k < s.n2) {
-          s.Q[static_cast<int64_t>(b) * s.ldp + k] = static_cast<float>(acc[g][r]);
-          if (MOM) s.Qw[static_cast<int64_t>(b) * s.ldp + k] = static_cast<float>(accw[g][r]);
+          if (s.Qk != nullptr) {
+            // k-major rows (consecutive buckets of a wave write consecutive floats)
+            s.Qk[k * s.mq + b] = static_cast<float>(acc[g][r]);
+            if (MOM) s.Qwk[k * s.mq + b] = static_cast<float>(accw[g][r]);
+          } else {
+            s.Q[static_cast<int64_t>(b) * s.ldp + k] = static_cast<float>(acc[g][r]);
+            if (MOM) s.Qw[static_cast<int64_t>(b) * s.ldp + k] = static_cast<float>(accw[g][r]);
+          }
         }
       }
     }
