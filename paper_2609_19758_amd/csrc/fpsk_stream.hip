@@ -302,9 +302,8 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
     }
   };
 
-  // Stage chunk c (signs v2(j) applied to the halves) and fold it.
-  auto process = [&](Chunk& ch, int c) {
-    const int64_t cbase = static_cast<int64_t>(c) * CW;
+  // Stage chunk c: signs v2(j) applied to the halves, columns and the sorted list into LDS.
+  auto stage = [&](Chunk& ch) {
 #pragma unroll
     for (int it = 0; it < NI; ++it) {
       const int g8 = threadIdx.x + kThreads * it;
@@ -333,6 +332,12 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
       if (t + kThreads <= m) boffL[t + kThreads] = ch.qe[0];
     }
     __syncthreads();
+  };
+
+  // Fold the staged chunk c into the bucket sums; qb, qe are this thread's segment bounds.
+  auto fold = [&](int c, const int* qb, const int* qe) {
+    const int64_t cbase = static_cast<int64_t>(c) * CW;
+    (void)cbase;
     if constexpr (GF) {
       const int32_t* boffL = reinterpret_cast<const int32_t*>(tabL + stride);
       const int ngroups = boffL[m] >> 3;
@@ -405,7 +410,7 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
       if constexpr (PADG == 8) {
         // segments are whole multiples of 8 entries (sentinels read the zero slot): 8 list
         // entries with one LDS read, their 8 columns summed in FP32, then added in FP64
-        for (int q = ch.qb[g]; q < ch.qe[g]; q += 8) {
+        for (int q = qb[g]; q < qe[g]; q += 8) {
           const u32x4 tw = *reinterpret_cast<const u32x4*>(tabL + q);
           float part[RBG], partw[RBG];
 #pragma unroll
@@ -436,27 +441,62 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
           }
         }
       } else {
-        for (int q = ch.qb[g]; q < ch.qe[g]; ++q) {
-          const int e = tabL[q];
-          float x[RBG];
-          load_col<DT, RBG>(L + (MOM ? col_slot<CW>(e) : e) * RB + rg * RBG, x);
-          const double wj = MOM ? static_cast<double>(cbase + e + 1) * s.inv_l3 : 0.0;
+        constexpr int UN = 2;
+        // Unpadded segments, two list entries per step so that their LDS reads overlap (four
+        // measured no faster and spill under prefetch); an entry past the segment's end reads
+        // the zero column (slot CW), which adds +0.
+        for (int q = qb[g]; q < qe[g]; q += UN) {
+          int e[UN];
 #pragma unroll
-          for (int r = 0; r < RBG; ++r) {
-            const double d = static_cast<double>(x[r]);
-            acc[g][r] += d;
-            if (MOM) accw[g][r] = fma(d, wj, accw[g][r]);
+          for (int z = 0; z < UN; ++z) e[z] = q + z < qe[g] ? static_cast<int>(tabL[q + z]) : -1;
+          float x[UN][RBG];
+#pragma unroll
+          for (int z = 0; z < UN; ++z) {
+            const int sl = e[z] < 0 ? CW : (MOM ? col_slot<CW>(e[z]) : e[z]);
+            load_col<DT, RBG>(L + sl * RB + rg * RBG, x[z]);
+          }
+#pragma unroll
+          for (int z = 0; z < UN; ++z) {
+            const double wj = MOM ? static_cast<double>(cbase + e[z] + 1) * s.inv_l3 : 0.0;
+#pragma unroll
+            for (int r = 0; r < RBG; ++r) {
+              const double d = static_cast<double>(x[z][r]);
+              acc[g][r] += d;
+              if (MOM) accw[g][r] = fma(d, wj, accw[g][r]);
+            }
           }
         }
       }
     }
-    __syncthreads();
   };
 
-  for (int c = 0; c < s.TB; ++c) {
+  // 4-row probe work-groups (m = 513 to 1024) fold chunk c while the loads of chunk c + 1 are
+  // in flight (the list bounds are copied out of the chunk registers first); their 3 resident
+  // work-groups per CU leave the registers for it.  Elsewhere it would spill.
+  constexpr bool PF = !GF && !MOM && RB == 4;
+  if constexpr (PF) {
     Chunk ch;
-    issue(ch, c);
-    process(ch, c);
+    issue(ch, 0);
+    for (int c = 0; c < s.TB; ++c) {
+      stage(ch);
+      int qb[G], qe[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        qb[g] = ch.qb[g];
+        qe[g] = ch.qe[g];
+      }
+      if (c + 1 < s.TB) issue(ch, c + 1);
+      fold(c, qb, qe);
+      __syncthreads();
+    }
+  } else {
+    for (int c = 0; c < s.TB; ++c) {
+      Chunk ch;
+      issue(ch, c);
+      stage(ch);
+      fold(c, ch.qb, ch.qe);
+      __syncthreads();
+    }
   }
   if constexpr (GF) {
 #pragma unroll
@@ -659,9 +699,12 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
 }
 
 // LDS layout of the stream kernel (dynamic): the A/C combine area or the staged B chunk first,
-// then the sorted column list of the current B chunk or C tile.
+// then the sorted column list of the current B chunk or C tile.  The longer lists of B chunks
+// with fewer rows hold the probe to 3 (4 rows) or 2 (1 or 2 rows) work-groups per CU, so those
+// instances may use the registers of that occupancy instead of spilling at 4's 128.
 template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
-__global__ __launch_bounds__(kThreads, MOM ? 2 : 4) void stream_kernel(StreamArgs s) {
+__global__ __launch_bounds__(kThreads, MOM ? 2 : (RB == 8 ? 4 : (RB == 4 ? 3 : 2))) void stream_kernel(
+    StreamArgs s) {
   extern __shared__ double lds_dyn[];
   __shared__ uint32_t ldsu[kThreads / 64];
   // the sorted column list of the current B chunk or C tile follows the data area
