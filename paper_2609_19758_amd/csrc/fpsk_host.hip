@@ -555,6 +555,9 @@ void free_round(DevRound& D) {
 
 struct Workspace {
   Decomp d;
+  // with moments: the product decomposition of S alone (localize rounds form R and T only at
+  // the selected buckets)
+  Decomp ds;
   bool mom = false;
   DevBuf P, Pw, Q, Qw, partS, partR, partT, scratch, S, R, T, maxpart, tilestat;
   DevBuf xpart;                // probe block-product partials
@@ -581,10 +584,12 @@ fpsketch_status ensure_workspace(Workspace& W, int64_t n1, int64_t n2, int64_t n
     FPSK_TRY(dev_alloc(W.R, mm));
     FPSK_TRY(dev_alloc(W.T, mm));
   }
-  const int tiles = d.nt * d.nt;
+  W.ds = mom ? decompose(n1, n2, n3, m, false, transb) : d;
+  const int tiles = std::max(d.nt * d.nt, W.ds.nt * W.ds.nt);
   // slice partials (also used with a single slice when the probe's decision is fused)
-  const size_t sc =
-      static_cast<size_t>(d.NS) * tiles * d.ts * d.ts * (mom ? 3 : 1) * sizeof(double);
+  const size_t sc = std::max(
+      static_cast<size_t>(d.NS) * d.nt * d.nt * d.ts * d.ts * (mom ? 3 : 1),
+      static_cast<size_t>(W.ds.NS) * W.ds.nt * W.ds.nt * W.ds.ts * W.ds.ts) * sizeof(double);
   FPSK_TRY(dev_alloc(W.scratch, sc));
   FPSK_TRY(dev_alloc(W.maxpart, static_cast<size_t>(d.nA + d.nB) * sizeof(float)));
   FPSK_TRY(dev_alloc(W.tilestat, static_cast<size_t>(tiles) * 4 * sizeof(double)));
@@ -631,6 +636,8 @@ struct fpsketch_ctx {
       patch_val, rc_coords, rc_gamma, rc_abs, rc_c;
   // localize rounds on the device: selection state and histogram, peel list, candidates
   DevBuf sel_state, sel_hist, peel_list, cands, cand_count;
+  // the selected buckets of a round and their moment sketches (R then T)
+  DevBuf mo_list, mo_rt;
   // apply step: the record list and the re-probe's statistics and scratch noise sum
   DevBuf apply_list, reprobe_stats, reprobe_acc;
   // the B-side cache of the probe: Q = (B H2^T)^T for the probe's round at m = qcache_m
@@ -819,7 +826,7 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
                          const int32_t* prow, const int32_t* pcol, const float* pval,
                          hipStream_t st, hipEvent_t* ev = nullptr,
                          double* stats_out = nullptr, double* sigma_acc_out = nullptr,
-                         BSide bside = BSide::kStream) {
+                         BSide bside = BSide::kStream, bool prod_mom = true) {
   const Decomp& d = W.d;
   fpsk::StreamArgs s;
   fpsk::ProductArgs a;
@@ -840,6 +847,19 @@ fpsketch_status run_pass(fpsketch_ctx* c, const DevRound& R, Workspace& W, const
   if (d.qk && s.nB > 0) {
     FPSK_HIP(fpsk::launch_transpose_q(s.Qk, s.Q, d.m, c->n2, s.mq, d.ldp, st));
     if (mom) FPSK_HIP(fpsk::launch_transpose_q(s.Qwk, s.Qw, d.m, c->n2, s.mq, d.ldp, st));
+  }
+  if (mom && !prod_mom) {
+    // the moment factors stay for launch_moments_at; the product forms S alone
+    const Decomp& ds = W.ds;
+    a.R = nullptr;
+    a.T = nullptr;
+    a.nt = ds.nt;
+    a.ts = ds.ts;
+    a.NS = ds.NS;
+    a.ksl = ds.ksl;
+    FPSK_HIP(fpsk::launch_product(a, ds.ts, ds.kw, false, st, ev ? ev[2] : nullptr,
+                                  ev ? ev[3] : nullptr));
+    return FPSK_OK;
   }
   FPSK_HIP(fpsk::launch_product(a, d.ts, d.kw, mom, st, ev ? ev[2] : nullptr,
                                 ev ? ev[3] : nullptr));
@@ -1005,7 +1025,9 @@ fpsketch_status sketch_round(fpsketch_ctx* c, uint64_t seed, int round, int m, b
   return FPSK_OK;
 }
 
-// One sketch pass at m whose S (R, T) stay in the auxiliary workspace; max|A|, max|B| to host.
+// One sketch pass at m whose S stays in the auxiliary workspace, with the moment factors and
+// C-grid partials when mom (R and T are then formed at selected buckets by launch_moments_at);
+// max|A|, max|B| to host.
 fpsketch_status sketch_round_device(fpsketch_ctx* c, uint64_t seed, int round, int m, bool mom,
                                     const void* A, const void* B, const float* C,
                                     const int32_t* prow, const int32_t* pcol, const float* pval,
@@ -1014,7 +1036,8 @@ fpsketch_status sketch_round_device(fpsketch_ctx* c, uint64_t seed, int round, i
   build_round(seed, round, c->n1, c->n3, m, d.cwb, mom, c->transb, HR);
   FPSK_TRY(upload_round(HR, d.cwb, c->aux_round, st));
   FPSK_TRY(ensure_workspace(c->aux_ws, c->n1, c->n2, c->n3, m, mom, c->transb));
-  FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, C, mom, 0, nullptr, prow, pcol, pval, st));
+  FPSK_TRY(run_pass(c, c->aux_round, c->aux_ws, A, B, C, mom, 0, nullptr, prow, pcol, pval, st,
+                    nullptr, nullptr, nullptr, BSide::kStream, false));
   std::vector<float> mp(static_cast<size_t>(d.nA + d.nB));
   FPSK_HIP(hipMemcpyAsync(mp.data(), c->aux_ws.maxpart.p, mp.size() * sizeof(float),
                           hipMemcpyDeviceToHost, st));
@@ -1221,6 +1244,7 @@ void fpsketch_destroy(fpsketch_ctx* c) {
                     &c->scan_out, &c->samples, &c->patch_rowptr, &c->patch_col, &c->patch_val,
                     &c->rc_coords, &c->rc_gamma, &c->rc_abs, &c->rc_c, &c->sel_state,
                     &c->sel_hist, &c->peel_list, &c->cands, &c->cand_count, &c->apply_list,
+                    &c->mo_list, &c->mo_rt,
                     &c->reprobe_stats, &c->reprobe_acc, &c->qcache, &c->maxb_cache}) {
     dev_free(*b);
   }
@@ -1655,9 +1679,8 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
     tau = c->p.c_valid * static_cast<double>(c->n2) * std::ldexp(1.0, -23) * maxA * maxB;
     const int64_t mm = static_cast<int64_t>(m) * m;
     double* dS = as<double>(c->aux_ws.S);
-    double* dR = as<double>(c->aux_ws.R);
-    double* dT = as<double>(c->aux_ws.T);
-    // peel every finite fault confirmed so far (Sec. III-H), in order, on the device
+    // peel every finite fault confirmed so far (Sec. III-H), in order, on the device (S here;
+    // R and T at the selected buckets below)
     std::vector<fpsk::PeelEntry> peel;
     for (const Found& f : F) {
       if (f.absolute) continue;
@@ -1670,7 +1693,7 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
       FPSK_TRY(dev_alloc(c->peel_list, peel.size() * sizeof(fpsk::PeelEntry)));
       FPSK_HIP(hipMemcpyAsync(c->peel_list.p, peel.data(), peel.size() * sizeof(fpsk::PeelEntry),
                               hipMemcpyHostToDevice, st));
-      FPSK_HIP(fpsk::launch_peel(dS, dR, dT, as<fpsk::PeelEntry>(c->peel_list),
+      FPSK_HIP(fpsk::launch_peel(dS, nullptr, nullptr, as<fpsk::PeelEntry>(c->peel_list),
                                  static_cast<int>(peel.size()), st));
     }
     double sig = 0.0;
@@ -1684,8 +1707,8 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
     FPSK_TRY(dev_alloc(c->cands, static_cast<size_t>(kCandCap) * sizeof(fpsk::Cand)));
     FPSK_TRY(dev_alloc(c->cand_count, sizeof(uint32_t)));
     FPSK_HIP(hipMemsetAsync(c->cand_count.p, 0, sizeof(uint32_t), st));
-    FPSK_HIP(fpsk::launch_above(dS, dR, dT, mm, cut, as<fpsk::Cand>(c->cands), kCandCap,
-                                as<uint32_t>(c->cand_count), st));
+    FPSK_HIP(fpsk::launch_above(dS, nullptr, nullptr, mm, cut, as<fpsk::Cand>(c->cands),
+                                kCandCap, as<uint32_t>(c->cand_count), st));
     uint32_t ncand = 0;
     FPSK_HIP(hipMemcpyAsync(&ncand, c->cand_count.p, sizeof(ncand), hipMemcpyDeviceToHost, st));
     FPSK_HIP(hipStreamSynchronize(st));
@@ -1699,13 +1722,11 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
       }
     } else {
       // more candidates than the buffer holds: scan the whole grid on the host
-      std::vector<double> S(mm), Rm(mm), T(mm);
+      std::vector<double> S(mm);
       FPSK_HIP(hipMemcpyAsync(S.data(), dS, mm * sizeof(double), hipMemcpyDeviceToHost, st));
-      FPSK_HIP(hipMemcpyAsync(Rm.data(), dR, mm * sizeof(double), hipMemcpyDeviceToHost, st));
-      FPSK_HIP(hipMemcpyAsync(T.data(), dT, mm * sizeof(double), hipMemcpyDeviceToHost, st));
       FPSK_HIP(hipStreamSynchronize(st));
       for (int64_t o = 0; o < mm; ++o)
-        if (std::fabs(S[o]) > cut) above.push_back({o, S[o], Rm[o], T[o]});
+        if (std::fabs(S[o]) > cut) above.push_back({o, S[o], 0.0, 0.0});
     }
     std::sort(above.begin(), above.end(), [](const fpsk::Cand& x, const fpsk::Cand& y) {
       const double ax = std::fabs(x.s), ay = std::fabs(y.s);
@@ -1713,6 +1734,41 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* c, const void* A, const void* B,
       return x.o < y.o;
     });
     if (static_cast<int64_t>(above.size()) > K) above.resize(K);
+    // R and T (Eq. 2) at the top-K buckets only, with the peel terms
+    if (!above.empty()) {
+      const size_t na = above.size();
+      std::vector<int64_t> ol(na);
+      for (size_t q = 0; q < na; ++q) ol[q] = above[q].o;
+      FPSK_TRY(dev_alloc(c->mo_list, na * sizeof(int64_t)));
+      FPSK_TRY(dev_alloc(c->mo_rt, 2 * na * sizeof(double)));
+      FPSK_HIP(hipMemcpyAsync(c->mo_list.p, ol.data(), na * sizeof(int64_t),
+                              hipMemcpyHostToDevice, st));
+      fpsk::MomentsAtArgs g{};
+      g.P = as<float>(c->aux_ws.P);
+      g.Pw = as<float>(c->aux_ws.Pw);
+      g.Q = as<float>(c->aux_ws.Q);
+      g.Qw = as<float>(c->aux_ws.Qw);
+      g.partR = as<double>(c->aux_ws.partR);
+      g.partT = as<double>(c->aux_ws.partT);
+      g.o = as<int64_t>(c->mo_list);
+      g.peel = peel.empty() ? nullptr : as<fpsk::PeelEntry>(c->peel_list);
+      g.npeel = static_cast<int>(peel.size());
+      g.r = as<double>(c->mo_rt);
+      g.t = g.r + na;
+      g.m = m;
+      g.ldp = c->aux_ws.d.ldp;
+      g.kact = c->aux_ws.d.kact;
+      g.npc = c->aux_ws.d.npc;
+      FPSK_HIP(fpsk::launch_moments_at(g, static_cast<int>(na), st));
+      std::vector<double> rt(2 * na);
+      FPSK_HIP(hipMemcpyAsync(rt.data(), c->mo_rt.p, 2 * na * sizeof(double),
+                              hipMemcpyDeviceToHost, st));
+      FPSK_HIP(hipStreamSynchronize(st));
+      for (size_t q = 0; q < na; ++q) {
+        above[q].r = rt[q];
+        above[q].t = rt[na + q];
+      }
+    }
     struct Center {
       int64_t ci, cj;
     };

@@ -162,6 +162,22 @@ struct PeelEntry {     // S[o] -= ds, R[o] -= dr, T[o] -= dt
   int64_t o;
   double ds, dr, dt;
 };
+// Moment sketches R, T at a list of n buckets o (launch_moments_at): the factors (rows ldp
+// apart, zero from n2 to kact), the npc C-grid partials of R and T, the peel list.
+struct MomentsAtArgs {
+  const float* P;
+  const float* Pw;
+  const float* Q;
+  const float* Qw;
+  const double* partR;
+  const double* partT;
+  const int64_t* o;
+  const PeelEntry* peel;
+  double* r;
+  double* t;
+  int m, ldp, kact, npc, npeel;
+};
+hipError_t launch_moments_at(const MomentsAtArgs& g, int n, hipStream_t st);
 struct ApplyEntry {    // one record of the apply step: C[o] <- d, or C[o] + d
   int64_t o;
   double d;

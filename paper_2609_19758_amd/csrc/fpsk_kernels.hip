@@ -620,9 +620,51 @@ __global__ __launch_bounds__(1) void peel_kernel(double* S, double* R, double* T
   for (int q = 0; q < n; ++q) {
     const PeelEntry e = list[q];
     S[e.o] -= e.ds;
-    R[e.o] -= e.dr;
-    T[e.o] -= e.dt;
+    if (R != nullptr) R[e.o] -= e.dr;
+    if (T != nullptr) T[e.o] -= e.dt;
   }
+}
+
+// The moment sketches of Eq. 2 at the selected buckets only: for bucket o = a m + b,
+// R = Pw[a] . Q[b] - R_C(a, b) and T = P[a] . Qw[b] - T_C(a, b), then the peel list's R and T
+// terms at o, in list order.  One work-group per bucket: exact FP32 x FP32 products summed in
+// FP64 over the factor rows (k-contiguous, zero past n2), threads combined in fixed order.
+__global__ __launch_bounds__(kThreads) void moments_at_kernel(MomentsAtArgs g) {
+  __shared__ double red[lds_reduce_doubles<kThreads, 2>()];
+  const int q = blockIdx.x;
+  const int64_t o = g.o[q];
+  const int64_t a = o / g.m, b = o - (o / g.m) * g.m;
+  const float* pw = g.Pw + a * g.ldp;
+  const float* pp = g.P + a * g.ldp;
+  const float* qq = g.Q + b * g.ldp;
+  const float* qw = g.Qw + b * g.ldp;
+  double v[2] = {0.0, 0.0};
+  for (int k = 4 * threadIdx.x; k < g.kact; k += 4 * kThreads) {
+    const f32x4 x1 = *reinterpret_cast<const f32x4*>(pw + k);
+    const f32x4 y1 = *reinterpret_cast<const f32x4*>(qq + k);
+    const f32x4 x2 = *reinterpret_cast<const f32x4*>(pp + k);
+    const f32x4 y2 = *reinterpret_cast<const f32x4*>(qw + k);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[0] = fma(static_cast<double>(x1[e]), static_cast<double>(y1[e]), v[0]);
+      v[1] = fma(static_cast<double>(x2[e]), static_cast<double>(y2[e]), v[1]);
+    }
+  }
+  lds_reduce<kThreads, 2>(v, red, 0u);
+  if (threadIdx.x != 0) return;
+  const int64_t mm = static_cast<int64_t>(g.m) * g.m;
+  for (int p = 0; p < g.npc; ++p) {
+    v[0] -= g.partR[p * mm + o];
+    v[1] -= g.partT[p * mm + o];
+  }
+  for (int p = 0; p < g.npeel; ++p) {
+    if (g.peel[p].o == o) {
+      v[0] -= g.peel[p].dr;
+      v[1] -= g.peel[p].dt;
+    }
+  }
+  g.r[q] = v[0];
+  g.t[q] = v[1];
 }
 
 // Apply step of Algorithm 2: one thread per record (the coordinates are distinct).
@@ -644,7 +686,7 @@ __global__ __launch_bounds__(kThreads) void above_kernel(const double* S, const 
     const double s = S[i];
     if (fabs(s) > cut) {
       const uint32_t p = atomicAdd(count, 1u);
-      if (p < cap) out[p] = Cand{i, s, R[i], T[i]};
+      if (p < cap) out[p] = Cand{i, s, R != nullptr ? R[i] : 0.0, T != nullptr ? T[i] : 0.0};
     }
   }
 }
@@ -825,6 +867,12 @@ hipError_t launch_above(const double* S, const double* R, const double* T, int64
                         double cut, Cand* out, uint32_t cap, uint32_t* count, hipStream_t st) {
   hipLaunchKernelGGL(above_kernel, dim3(grid_for(n)), dim3(kThreads), 0, st, S, R, T, n, cut,
                      out, cap, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_moments_at(const MomentsAtArgs& g, int n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(moments_at_kernel, dim3(static_cast<unsigned>(n)), dim3(kThreads), 0, st, g);
   return hipGetLastError();
 }
 

@@ -240,6 +240,35 @@ def test_localize_exact_matches_oracle(fk):
     v.close()
 
 
+def test_localize_large_mloc_matches_oracle(fk):
+    """m_loc above 240: the localize rounds form S on the 64 x 64 matrix-core tiles and R, T
+    only at the selected buckets (with the peel of earlier rounds' faults); the records equal
+    the oracle's, whose rounds form the three full sketches."""
+    n1, n2, n3, fmt = 2048, 1024, 2048, "bf16"
+    a_bits, b_bits = wl.gen_operands(n1, n2, n3, fmt, ("normal", 1.0), ("normal", 0.02), 41)
+    A, B = to_dev_half(a_bits, fmt), to_dev_half(b_bits, fmt)
+    c = gemm_f32(A, B).cpu().numpy()
+    a64, b64 = o.decode(a_bits, fmt), o.decode(b_bits, fmt)
+    sites = wl.fault_sites(n1, n3, 10, 42)
+    cf = wl.inject_additive(c, sites, wl.fault_magnitudes(10, 0.05, 4.0, wl.mean_abs(c), 43))
+    C = to_dev_f32(cf)
+    v = fk.Verifier(n1, n2, n3, fmt, rho_min=0.0015)
+    v.probe(A, B, C)
+    assert v.probe_stats()["dirty"] == 1.0
+    recs, n, st = v.localize(A, B, C, seed=6, sigma_from_probe=True)
+    plan = v.plan()
+    assert plan["m_loc"] > 240
+    pl = o.Params(rho_min=0.0015)
+    ref = o.localize(a64, b64, cf, fmt, v.m, 6, pl,
+                     plan=o.Plan(plan["m_loc"], plan["r"], plan["B"], bool(plan["fallback"])))
+    got = {(i, j): d for i, j, d, a, r in recs}
+    exp = {(f.i, f.j): f.delta for f in ref.faults}
+    assert set(got) == set(exp) == {tuple(x) for x in sites.tolist()}
+    for k in got:
+        assert abs(got[k] - exp[k]) <= 1e-3 * abs(exp[k])
+    v.close()
+
+
 def test_localize_float_matches_oracle(fk):
     import torch
     n1, n2, n3, fmt = 768, 512, 640, "bf16"
