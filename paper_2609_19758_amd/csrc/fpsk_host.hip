@@ -408,6 +408,7 @@ struct Decomp {
   int xsr = 1, xsc = 1, xnstc = 1, xslots = 0;   // supertiles of blocks (XCD-local sets)
   // B work-groups of fewer than 8 rows write Q k-major (n2 x m), then a transpose forms Q
   bool qk = false;
+  bool wt_a = false, wt_w = false;   // row-bucket work-groups of four tiles (small buckets)
 };
 
 // pipe: the deferred probe's decomposition, whose output blocks stay at most 3 x 3 (the
@@ -418,7 +419,11 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   Decomp d;
   d.m = m;
   d.TA = static_cast<int>((n2 + kColTile - 1) / kColTile);
-  d.nA = m * d.TA;
+  // buckets of at most about 16 rows: one wave per column tile, four tiles per work-group
+  d.wt_a = n1 <= 16 * static_cast<int64_t>(m);
+  d.wt_w = transb && n3 <= 16 * static_cast<int64_t>(m);
+  const int tq = (d.TA + 3) / 4;
+  d.nA = m * (d.wt_a ? tq : d.TA);
   if (m <= 64) {
     d.rb = 8, d.g = 1, d.ng = 4;
   } else if (m <= 128) {
@@ -438,7 +443,7 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.TB = static_cast<int>((n3 + d.cwb - 1) / d.cwb);
   d.nB = static_cast<int>((n2 + d.rb - 1) / d.rb);
   // B passed transposed: row-bucket work-groups over the rows of W = B^T, as many as A's
-  if (transb) d.nB = m * d.TA;
+  if (transb) d.nB = m * (d.wt_w ? tq : d.TA);
   d.qk = !transb && d.rb < 8;
   d.TC = static_cast<int>((n3 + kColTile - 1) / kColTile);
   int npc = static_cast<int>((1024 + m - 1) / m);
@@ -479,10 +484,12 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   const size_t bdata = (static_cast<size_t>(d.cwb) * d.rb + d.rb) * sizeof(uint16_t);
   const size_t data = (std::max(comb + cs, bdata) + 15) / 16 * 16;
   d.tab_off = static_cast<int>(data);
-  // (the probe's B group fold stages the m + 1 segment starts after the column list)
+  // (the probe's B group fold, 8-row work-groups up to m = 256, stages the m + 1 segment
+  // starts after the column list; at larger m they would take up to 16 KiB per work-group)
+  const bool group_fold = !mom && d.rb == 8 && d.g == 1;
   d.lds_stream = data + static_cast<size_t>(std::max(d.ctab_stride, d.btab_stride)) *
                             sizeof(uint16_t) +
-                 (static_cast<size_t>(m) + 1) * sizeof(int32_t);
+                 (group_fold ? (static_cast<size_t>(m) + 1) * sizeof(int32_t) : 0);
   d.kact = static_cast<int>((n2 + 3) / 4 * 4);
   // Factor rows sit 64 floats past a multiple of 1024 apart (an odd multiple of 256 bytes), so
   // that the 16 rows one matrix-core load instruction touches at the same k fall on 16
@@ -737,6 +744,8 @@ fpsketch_status pass_args(fpsketch_ctx* c, const DevRound& R, Workspace& W, cons
   s.TB = d.TB;
   s.npc = d.npc;
   s.tg = d.tg;
+  s.wt_a = d.wt_a ? 1 : 0;
+  s.wt_w = d.wt_w ? 1 : 0;
   s.inv_l1 = c->inv_l1;
   s.inv_l3 = c->inv_l3;
   auto aligned16 = [](const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; };

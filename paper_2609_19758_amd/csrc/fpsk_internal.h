@@ -73,6 +73,9 @@ struct StreamArgs {
   int nA, nB, nC;
   int TA, TC, TB;
   int npc, tg;
+  // small buckets: row-bucket work-groups of four tiles, one per wave (A side; W side with
+  // transb), m x ceil(TA / 4) of them
+  int wt_a, wt_w;
   double inv_l1, inv_l3;      // 1 / 2^ceil(log2 n1), 1 / 2^ceil(log2 n3)
   int vec_a, vec_b, vec_c;    // 16-byte vector loads allowed
   const void* zero;           // >= 64 bytes of zeros (read in place of invalid rows or lanes)

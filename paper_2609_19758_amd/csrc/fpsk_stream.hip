@@ -135,6 +135,116 @@ __device__ void a_unit(const StreamArgs& s, const RowSide& rs, int u, double* ld
   if (threadIdx.x == 0) rs.maxslot[u] = amax;
 }
 
+// Row-bucket work-group for small buckets (at most about 16 rows): bucket a, four column tiles,
+// wave w taking tile 4 tq + w over all of the bucket's rows, so no combine across waves.  The
+// same groups of 8 rows in FP32, then FP64, in list order.
+template <int DT, bool MOM, bool VEC>
+__device__ void a_unit_wt(const StreamArgs& s, const RowSide& rs, int u, uint32_t* ldsu) {
+  constexpr int U = 8;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int tq = (s.TA + 3) / 4;
+  const int a = u / tq, t = 4 * (u - a * tq) + w;
+  const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
+  const bool lane_ok = t < s.TA && col < s.n2;
+  const int32_t* prow = rs.perm + static_cast<int64_t>(a) * rs.cap;
+  double acc[8], accw[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    acc[k] = 0.0;
+    accw[k] = 0.0;
+  }
+  uint32_t mx = 0;
+  for (int base = 0; base < rs.cap; base += 64) {
+    const int32_t pe = base + lane < rs.cap ? prow[base + lane] : -1;
+    const int nr = __popcll(__ballot(pe != -1));   // valid entries are a prefix of the lanes
+    if (nr == 0) break;
+    for (int r0 = 0; r0 < nr; r0 += U) {
+      u32x4 v[U];
+      float sg[U], sw[U];
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+        const bool ok = r0 + q < nr;
+        const int32_t e = row_entry(pe, ok ? r0 + q : 0);
+        const int64_t row = e & 0x7fffffff;
+        sg[q] = ok ? (e < 0 ? -1.0f : 1.0f) : 0.0f;
+        sw[q] = MOM ? static_cast<float>(sg[q] * static_cast<double>(row + 1) * rs.inv_l) : 0.0f;
+        if (VEC) {
+          v[q] = load8h_sel(rs.X + row * s.n2 + col, ok && lane_ok, s.zero);
+        } else {
+          v[q] = ok && lane_ok ? load8h(rs.X + row * s.n2, col, s.n2, false)
+                               : u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+      float g32[8], gw32[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        g32[k] = 0.0f;
+        gw32[k] = 0.0f;
+      }
+#pragma unroll
+      for (int q = 0; q < U; ++q) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const uint32_t wd = v[q][h];
+          mx = absmax2(mx, wd);
+          const float x0 = lo_half<DT>(wd), x1 = hi_half<DT>(wd);
+          g32[2 * h] = fmaf(sg[q], x0, g32[2 * h]);
+          g32[2 * h + 1] = fmaf(sg[q], x1, g32[2 * h + 1]);
+          if (MOM) {
+            gw32[2 * h] = fmaf(sw[q], x0, gw32[2 * h]);
+            gw32[2 * h + 1] = fmaf(sw[q], x1, gw32[2 * h + 1]);
+          }
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        acc[k] += static_cast<double>(g32[k]);
+        if (MOM) accw[k] += static_cast<double>(gw32[k]);
+      }
+    }
+  }
+  if (lane_ok) {
+    float* o = rs.out + static_cast<int64_t>(a) * s.ldp + col;
+    float* ow = MOM ? rs.outw + static_cast<int64_t>(a) * s.ldp + col : nullptr;
+    if (col + 8 <= s.n2) {
+      // the row starts on a 256-byte boundary and col is a multiple of 8
+      reinterpret_cast<f32x4*>(o)[0] = f32x4{static_cast<float>(acc[0]), static_cast<float>(acc[1]),
+                                             static_cast<float>(acc[2]), static_cast<float>(acc[3])};
+      reinterpret_cast<f32x4*>(o)[1] = f32x4{static_cast<float>(acc[4]), static_cast<float>(acc[5]),
+                                             static_cast<float>(acc[6]), static_cast<float>(acc[7])};
+      if (MOM) {
+        reinterpret_cast<f32x4*>(ow)[0] =
+            f32x4{static_cast<float>(accw[0]), static_cast<float>(accw[1]),
+                  static_cast<float>(accw[2]), static_cast<float>(accw[3])};
+        reinterpret_cast<f32x4*>(ow)[1] =
+            f32x4{static_cast<float>(accw[4]), static_cast<float>(accw[5]),
+                  static_cast<float>(accw[6]), static_cast<float>(accw[7])};
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if (col + k < s.n2) {
+          o[k] = static_cast<float>(acc[k]);
+          if (MOM) ow[k] = static_cast<float>(accw[k]);
+        }
+      }
+    }
+  }
+  const float amax = block_absmax_half<DT>(mx, ldsu);   // contains __syncthreads
+  if (threadIdx.x == 0) rs.maxslot[u] = amax;
+}
+
+// Row-bucket unit of either kind.
+template <int DT, bool MOM, bool VEC>
+__device__ __forceinline__ void row_unit(const StreamArgs& s, const RowSide& rs, bool wt, int u,
+                                         double* lds, uint32_t* ldsu) {
+  if (wt) {
+    a_unit_wt<DT, MOM, VEC>(s, rs, u, ldsu);
+  } else {
+    a_unit<DT, MOM, VEC>(s, rs, u, lds, ldsu);
+  }
+}
+
 // ----------------------------------------------------------------------------------------
 // B work-group: RB consecutive rows of B, all columns, in chunks of CW = kBChunkHalfs / RB
 // columns.  Per chunk, every thread issues its 8 x 16-byte loads of B and its share of the
@@ -700,10 +810,10 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
 
 // LDS layout of the stream kernel (dynamic): the A/C combine area or the staged B chunk first,
 // then the sorted column list of the current B chunk or C tile.  The longer lists of B chunks
-// with fewer rows hold the probe to 3 (4 rows) or 2 (1 or 2 rows) work-groups per CU, so those
+// with fewer rows hold the probe to 3 (2 or 4 rows) or 2 (1 row) work-groups per CU, so those
 // instances may use the registers of that occupancy instead of spilling at 4's 128.
 template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
-__global__ __launch_bounds__(kThreads, MOM ? 2 : (RB == 8 ? 4 : (RB == 4 ? 3 : 2))) void stream_kernel(
+__global__ __launch_bounds__(kThreads, MOM ? 2 : (RB == 8 ? 4 : (RB >= 2 ? 3 : 2))) void stream_kernel(
     StreamArgs s) {
   extern __shared__ double lds_dyn[];
   __shared__ uint32_t ldsu[kThreads / 64];
@@ -719,13 +829,13 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : (RB == 8 ? 4 : (RB == 4 ? 3 : 2
   u -= s.nC;
   if (u < s.nB) {
     if (s.transb) {
-      a_unit<DT, MOM, VEC>(s, w_side(s), u, lds_dyn, ldsu);
+      row_unit<DT, MOM, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
     } else {
       b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
     }
     return;
   }
-  a_unit<DT, MOM, VEC>(s, a_side(s), u - s.nB, lds_dyn, ldsu);
+  row_unit<DT, MOM, VEC>(s, a_side(s), s.wt_a != 0, u - s.nB, lds_dyn, ldsu);
 }
 
 // ----------------------------------------------------------------------------------------
@@ -766,13 +876,13 @@ __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, P
   u -= s.nC;
   if (u < s.nB) {
     if (s.transb) {
-      a_unit<DT, false, VEC>(s, w_side(s), u, lds_dyn, ldsu);
+      row_unit<DT, false, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
     } else {
       b_unit<DT, false, 8, 1, 4, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
     }
     return;
   }
-  a_unit<DT, false, VEC>(s, a_side(s), u - s.nB, lds_dyn, ldsu);
+  row_unit<DT, false, VEC>(s, a_side(s), s.wt_a != 0, u - s.nB, lds_dyn, ldsu);
 }
 
 // LDS the pipelined launch needs besides the stream pass's: the block product's reductions
