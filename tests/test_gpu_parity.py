@@ -47,6 +47,8 @@ EXACT_CASES = [
     (400, 16, 3000, 1500, "bf16"),      # RB = 2, G = 8
     (700, 8, 5000, 4096, "fp16"),       # RB = 1, G = 16, m at the limit
     (2100, 520, 1030, 48, "bf16"),      # several A/C tiles and a ragged tail
+    (100, 37, 90, 13, "fp16"),          # small buckets (one wave per tile), element loads
+    (300, 2100, 200, 64, "bf16"),       # small buckets over 5 tiles: waves past the last idle
 ]
 
 
