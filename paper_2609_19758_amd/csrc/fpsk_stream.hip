@@ -651,7 +651,9 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
 
 template <bool MOM, int G, bool VEC>
 __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) {
-  constexpr int U = 8;
+  // rows in flight per wave: 4 at m > 2048 (a few rows per bucket, and the fold's 16 buckets
+  // per thread need the registers)
+  constexpr int U = G >= 16 ? 4 : 8;
   constexpr int PADG = G == 1 ? 8 : 1;       // bucket segments padded to this multiple
   const int m = s.m;
   const int a = u / s.npc, gi = u - a * s.npc;
