@@ -553,23 +553,31 @@ __global__ __launch_bounds__(kThreads) void sel_hist_kernel(const double* S, int
   if (h[threadIdx.x] != 0) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
 }
 
-// One work-group of 256: the digit whose cumulative count passes k; clears the histogram.
+// One work-group of 256: the digit whose cumulative count passes k (the first bin b with
+// k < count(bins 0..b), or bin 255 when none before it does); clears the histogram.  The
+// cumulative counts come from an inclusive scan across the 256 threads.
 __global__ __launch_bounds__(kThreads) void sel_step_kernel(SelState* st, uint32_t* hist) {
+  static_assert(kThreads == 256, "one thread per digit");
   __shared__ uint32_t h[256];
-  h[threadIdx.x] = hist[threadIdx.x];
+  const int t = threadIdx.x;
+  const uint64_t k = st->k;
+  const uint32_t mine = hist[t];
+  h[t] = mine;
+  hist[t] = 0;
   __syncthreads();
-  hist[threadIdx.x] = 0;
-  if (threadIdx.x == 0) {
+  for (int d = 1; d < 256; d <<= 1) {
+    const uint32_t add = t >= d ? h[t - d] : 0u;
+    __syncthreads();
+    h[t] += add;
+    __syncthreads();
+  }
+  const uint64_t incl = h[t], excl = incl - mine;
+  const bool hit = t == 255 ? excl <= k : (excl <= k && k < incl);
+  if (hit) {
     const int shift = 56 - 8 * st->pass;
-    uint64_t below = 0;
-    int b = 0;
-    for (; b < 255; ++b) {
-      if (st->k < below + h[b]) break;
-      below += h[b];
-    }
-    st->prefix |= static_cast<uint64_t>(b) << shift;
-    st->k -= below;
-    st->count_eq = h[b];
+    st->prefix |= static_cast<uint64_t>(t) << shift;
+    st->k = k - excl;
+    st->count_eq = mine;
     st->pass += 1;
   }
 }
