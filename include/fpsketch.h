@@ -146,9 +146,10 @@ fpsketch_status fpsketch_probe(fpsketch_ctx* ctx, const void* A, const void* B, 
  * when the records are on the host.  Steps: exact scan of C for non-finite entries and entries
  * above fp32max/16 in magnitude, at most K in row-major order, each recomputed as an absolute
  * value (Sec. III-I); the plan (m_loc, r) from the noise estimate and rms-hat(C) (Sec. III-G);
- * then hash rounds t = 1..k of `seed` at m_loc, each forming S, R, T with C holding the
- * recomputed values at the absolute entries, peeling the finite faults found so far, selecting
- * up to K buckets above max(tau_c, tau_d), decoding Eq. 2 and searching a (2r+1)^2 window in
+ * then hash rounds t = 1..k of `seed` at m_loc, each forming S with C holding the recomputed
+ * values at the absolute entries, peeling the finite faults found so far, selecting up to K
+ * buckets above max(tau_c, tau_d), forming R and T at those buckets only (with the same peel),
+ * decoding Eq. 2 and searching a (2r+1)^2 window in
  * Chebyshev-then-Manhattan order; a candidate (i, j) is accepted iff
  * |gamma - C_ij| > c 2^-23 sum_k |A_ik||B_kj| (Sec. III-D), with delta = gamma - C_ij.
  * `sigma_from_probe` = 1 uses the sigma_hat of this context's last probe (valid only if that
@@ -236,7 +237,8 @@ fpsketch_status fpsketch_get_m(fpsketch_ctx* ctx, int32_t* m_out);
 fpsketch_status fpsketch_probe_stats(fpsketch_ctx* ctx, double* out, void* stream);
 
 /* Sketches of E = AB - C at bucket count m with hash round `round` of `seed`, through the same
- * kernels as the probe and localize (Eq. 1 and the first-moment sketches).  Synchronous.
+ * kernels as the probe and localize (Eq. 1 and the first-moment sketches; with `moments`, R and
+ * T over the whole grid, which localize forms only at its selected buckets).  Synchronous.
  * Writes m*m doubles (row-major, bucket (a, b) at a*m + b) to the HOST arrays S and, when
  * `moments` is 1, R and T; maxab[0..1] receive max|A|, max|B| (maxab may be NULL). */
 fpsketch_status fpsketch_sketch(fpsketch_ctx* ctx, const void* A, const void* B, const void* C,
