@@ -117,6 +117,13 @@ def load():
     if not os.path.exists(LIB_PATH):
         raise FpsketchError(-1, "load", f"{LIB_PATH} is missing; build it with "
                                         "__graft_entry__.build()")
+    # torch carries its own HIP runtime.  Loaded before torch, this library bound a second runtime
+    # whose calls found no device once torch had initialized its own; importing torch first makes
+    # the library resolve its HIP dependency to the runtime torch already holds.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     for name, (res, args) in _SIGS.items():
         fn = getattr(lib, name)
