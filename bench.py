@@ -167,19 +167,20 @@ def write_pmc_summary(workload: str, fetch_db: str, write_db: str) -> int:
     copy_kib = 256 * 1024                  # --copy-calibration 256: 256 MiB read and written
     fs, ws = copy_kib / fetch[ck][0], copy_kib / write[ck][0]
     traffic = (fetch[sk][0] * fs + write[sk][0] * ws) * 1024.0
-    fdir = os.path.basename(os.path.dirname(os.path.abspath(fetch_db)))
-    wdir = os.path.basename(os.path.dirname(os.path.abspath(write_db)))
+    # the run directories as given, relative to the repository root
+    fdir = os.path.relpath(os.path.dirname(os.path.abspath(fetch_db)), ROOT)
+    wdir = os.path.relpath(os.path.dirname(os.path.abspath(write_db)), ROOT)
     lines = [
         f"# HBM traffic of the FP-Sketch probe's stream kernel, {workload}",
         "# commands (from /tmp, repo at $R), one counter per run:",
-        f"#   rocprofv3 --pmc FETCH_SIZE -d $R/gpurun_out/{fdir} -o run -- python3 $R/bench.py "
+        f"#   rocprofv3 --pmc FETCH_SIZE -d $R/{fdir} -o run -- python3 $R/bench.py "
         "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --probe-only "
         "--copy-calibration 256",
-        f"#   rocprofv3 --pmc WRITE_SIZE -d $R/gpurun_out/{wdir} -o run -- python3 $R/bench.py "
+        f"#   rocprofv3 --pmc WRITE_SIZE -d $R/{wdir} -o run -- python3 $R/bench.py "
         "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --probe-only "
         "--copy-calibration 256",
-        f"#   python3 bench.py --write-pmc-summary gpurun_out/{fdir}/run_results.db "
-        f"gpurun_out/{wdir}/run_results.db",
+        f"#   python3 bench.py --write-pmc-summary {fdir}/run_results.db "
+        f"{wdir}/run_results.db",
         "# scale: the copy kernel moves 262144 KiB in and 262144 KiB out per dispatch",
         f"workload={workload}",
         f"kernel={sk}",
