@@ -424,7 +424,11 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.wt_w = transb && n3 <= 16 * static_cast<int64_t>(m);
   const int tq = (d.TA + 3) / 4;
   d.nA = m * (d.wt_a ? tq : d.TA);
-  if (m <= 64) {
+  // the probe at m <= 64 (B as stored): 4-row B work-groups over whole 4096-column chunks
+  const bool probe4 = !mom && !transb && m <= 64;
+  if (probe4) {
+    d.rb = 4, d.g = 1, d.ng = 1;
+  } else if (m <= 64) {
     d.rb = 8, d.g = 1, d.ng = 4;
   } else if (m <= 128) {
     d.rb = 8, d.g = 1, d.ng = 2;
@@ -444,7 +448,7 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.nB = static_cast<int>((n2 + d.rb - 1) / d.rb);
   // B passed transposed: row-bucket work-groups over the rows of W = B^T, as many as A's
   if (transb) d.nB = m * (d.wt_w ? tq : d.TA);
-  d.qk = !transb && d.rb < 8;
+  d.qk = !transb && d.rb < 8 && !probe4;
   d.TC = static_cast<int>((n3 + kColTile - 1) / kColTile);
   int npc = static_cast<int>((1024 + m - 1) / m);
   npc = std::max(1, std::min(npc, d.TC));
@@ -493,6 +497,12 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.lds_stream = data + static_cast<size_t>(std::max(d.ctab_stride, d.btab_stride)) *
                             sizeof(uint16_t) +
                  (group_fold ? (static_cast<size_t>(m) + 1) * sizeof(int32_t) : 0);
+  if (probe4) {
+    // the 4-row B work-groups read their sorted lists from global memory and stage only the
+    // m + 1 segment starts after the data (the C tiles' lists use the same area)
+    d.lds_stream = data + std::max<size_t>(static_cast<size_t>(d.ctab_stride) * sizeof(uint16_t),
+                                           (static_cast<size_t>(m) + 1) * sizeof(int32_t));
+  }
   d.kact = static_cast<int>((n2 + 3) / 4 * 4);
   // Factor rows sit 64 floats past a multiple of 1024 apart (an odd multiple of 256 bytes), so
   // that the 16 rows one matrix-core load instruction touches at the same k fall on 16

@@ -642,6 +642,131 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
   if (threadIdx.x == 0) s.maxpart[s.nA + u] = bmax;
 }
 
+// B work-group of the probe at m <= 64: 4 consecutive rows of B over all columns, in chunks of
+// 4096 columns (one chunk when n3 <= 4096) whose loads are all issued at once, so a work-group
+// waits for memory once per chunk.  The columns are staged column-major in LDS ([slot][4 rows],
+// 8 bytes each, signs v2(j) applied).  Thread t sums the 8 columns of the groups t, t + 256 and
+// t + 512 of the chunk's bucket-sorted list (segments padded to whole groups; the list is read
+// from global memory, which keeps the work-group's LDS within four work-groups per CU) in FP32;
+// the group partials replace the staged data; thread b < m adds its bucket's partials in FP64
+// and at the end stores Q[b, k0 .. k0 + 3] with one 16-byte store.
+template <int DT, bool VEC>
+__device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t* ldsu) {
+  constexpr int RB = 4;
+  constexpr int CW = kBChunkHalfs / RB;          // 4096 columns per chunk
+  constexpr int NI = CW / 8 / kThreads;          // groups of 8 columns a thread loads
+  constexpr int NGT = 3;                         // sorted-list groups a thread folds
+  static_assert(CW == 4096 && NI == 2, "the slot format and the sentinel assume 4096 columns");
+  const int m = s.m;
+  const int stride = s.btab_stride;              // multiple of 8, at most 8 NGT kThreads
+  const int t = threadIdx.x;
+  const int64_t k0 = static_cast<int64_t>(u) * RB;
+  int32_t* boffL = reinterpret_cast<int32_t*>(L + CW * RB + 8);   // after the zero column
+  float* PL = reinterpret_cast<float*>(L);       // group partials, over the staged data
+  if (t < RB) L[CW * RB + t] = 0;                // zero sentinel column (slot CW)
+  double q[RB];
+#pragma unroll
+  for (int r = 0; r < RB; ++r) q[r] = 0.0;
+  uint32_t mx = 0;
+  const u32x4 sent = {0x10001000u, 0x10001000u, 0x10001000u, 0x10001000u};   // 8 x slot CW
+  for (int c = 0; c < s.TB; ++c) {
+    const int64_t cbase = static_cast<int64_t>(c) * CW;
+    u32x4 v[NI][RB];
+    uint32_t sb[NI];
+    u32x4 tw[NGT];
+#pragma unroll
+    for (int it = 0; it < NI; ++it) {
+      const int g8 = t + kThreads * it;
+      const int64_t col = cbase + static_cast<int64_t>(g8) * 8;
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const bool ok = k0 + r < s.n2 && col < s.n3;
+        if (VEC) {
+          v[it][r] = load8h_sel(s.B + (k0 + r) * s.n3 + col, ok, s.zero);
+        } else {
+          v[it][r] = ok ? load8h(s.B + (k0 + r) * s.n3, col, s.n3, false)
+                        : u32x4{0u, 0u, 0u, 0u};
+        }
+      }
+      sb[it] = s.bsign[cbase / 8 + g8];          // the sign bits cover whole chunks
+    }
+    const uint16_t* btab = s.btab + static_cast<int64_t>(c) * stride;
+#pragma unroll
+    for (int h = 0; h < NGT; ++h) {
+      const int o = 8 * (t + kThreads * h);
+      tw[h] = o < stride ? *reinterpret_cast<const u32x4*>(btab + o) : sent;
+    }
+    const int32_t bo = t <= m ? s.boff[static_cast<int64_t>(c) * (m + 1) + t] : 0;
+#pragma unroll
+    for (int it = 0; it < NI; ++it) {
+      const int g8 = t + kThreads * it;
+      u32x4 smask;
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        smask[h] = (((sb[it] >> (2 * h)) & 1u) << 15) | (((sb[it] >> (2 * h + 1)) & 1u) << 31);
+      }
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+#pragma unroll
+        for (int h = 0; h < 4; ++h) mx = absmax2(mx, v[it][r][h]);
+        v[it][r] ^= smask;
+      }
+      store_cols<RB>(L + static_cast<int64_t>(g8) * RB, v[it]);
+    }
+    if (t <= m) boffL[t] = bo;
+    __syncthreads();
+    float part[NGT][RB];
+#pragma unroll
+    for (int h = 0; h < NGT; ++h) {
+#pragma unroll
+      for (int r = 0; r < RB; ++r) part[h][r] = 0.0f;
+#pragma unroll
+      for (int z = 0; z < 8; ++z) {
+        const int e = static_cast<int>((tw[h][z >> 1] >> (16 * (z & 1))) & 0xffffu);
+        const u32x2 w = *reinterpret_cast<const u32x2*>(L + e * RB);
+        part[h][0] += lo_half<DT>(w[0]);
+        part[h][1] += hi_half<DT>(w[0]);
+        part[h][2] += lo_half<DT>(w[1]);
+        part[h][3] += hi_half<DT>(w[1]);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < NGT; ++h) {
+      const int grp = t + kThreads * h;
+      if (8 * grp < stride) {
+        *reinterpret_cast<f32x4*>(PL + 4 * grp) =
+            f32x4{part[h][0], part[h][1], part[h][2], part[h][3]};
+      }
+    }
+    __syncthreads();
+    if (t < m) {
+      const int g1 = boffL[t + 1] >> 3;
+      for (int g = boffL[t] >> 3; g < g1; ++g) {
+        const f32x4 p = *reinterpret_cast<const f32x4*>(PL + 4 * g);
+#pragma unroll
+        for (int r = 0; r < RB; ++r) q[r] += static_cast<double>(p[r]);
+      }
+    }
+    __syncthreads();
+  }
+  if (t < m) {
+    float* qo = s.Q + static_cast<int64_t>(t) * s.ldp + k0;
+    if (k0 + RB <= s.n2) {
+      // k0 is a multiple of 4 and the rows start on 256-byte boundaries
+      *reinterpret_cast<f32x4*>(qo) = f32x4{static_cast<float>(q[0]), static_cast<float>(q[1]),
+                                            static_cast<float>(q[2]), static_cast<float>(q[3])};
+    } else {
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        if (k0 + r < s.n2) qo[r] = static_cast<float>(q[r]);
+      }
+    }
+  }
+  const float bmax = block_absmax_half<DT>(mx, ldsu);
+  if (t == 0) s.maxpart[s.nA + u] = bmax;
+}
+
 // ----------------------------------------------------------------------------------------
 // C work-group: row bucket a, a group of tg column tiles.  Per tile, the 4 waves accumulate
 // v1(i) C[i, tile] (and w_i v1(i) C) over the bucket's rows in FP64, combine in fixed order,
@@ -815,7 +940,7 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
 // with fewer rows hold the probe to 3 (2 or 4 rows) or 2 (1 row) work-groups per CU, so those
 // instances may use the registers of that occupancy instead of spilling at 4's 128.
 template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
-__global__ __launch_bounds__(kThreads, MOM ? 2 : (RB == 8 ? 4 : (RB >= 2 ? 3 : 2))) void stream_kernel(
+__global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1)) ? 4 : (RB >= 2 ? 3 : 2))) void stream_kernel(
     StreamArgs s) {
   extern __shared__ double lds_dyn[];
   __shared__ uint32_t ldsu[kThreads / 64];
@@ -832,6 +957,8 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : (RB == 8 ? 4 : (RB >= 2 ? 3 : 2
   if (u < s.nB) {
     if (s.transb) {
       row_unit<DT, MOM, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
+    } else if constexpr (RB == 4 && G == 1 && !MOM) {
+      b_unit_probe4<DT, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
     } else {
       b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
     }
@@ -880,7 +1007,7 @@ __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, P
     if (s.transb) {
       row_unit<DT, false, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
     } else {
-      b_unit<DT, false, 8, 1, 4, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
+      b_unit_probe4<DT, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
     }
     return;
   }
@@ -953,6 +1080,7 @@ static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, int ng, si
   FPSK_STREAM_CASE(8, 1, 2)
   FPSK_STREAM_CASE(8, 1, 1)
   FPSK_STREAM_CASE(8, 2, 1)
+  FPSK_STREAM_CASE(4, 1, 1)
   FPSK_STREAM_CASE(4, 4, 1)
   FPSK_STREAM_CASE(2, 8, 1)
   FPSK_STREAM_CASE(1, 16, 1)
