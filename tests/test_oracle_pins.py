@@ -214,6 +214,103 @@ def test_table2_bucket_counts():
         assert o.m_start(n1, n2, n3, "fp16", P) == int(row["m_fp16"]), row
 
 
+def test_law_sigma_over_rms_against_table2():
+    """Eq. 3 (the noise law, per unit of rms(C)) pinned by Table II: at m = 1 and delta = rms(C),
+    Eq. 4 is Eq. 3 times max(n1, n3) / B*, so ceil(max(n1, n3) / B* x law(m = 1)) must equal
+    every printed bucket count, except where Eq. 5 raises it to m_comb = 48 (the count printed is
+    then 48 and the law's value is at most 48).  The law is evaluated through
+    law_sigma_over_rms alone; m_num is not used."""
+    mcomb = o.m_comb(P)
+    for row in load_golden("table2_bucket_counts.csv"):
+        n1, n2, n3 = int(row["n1"]), int(row["n2"]), int(row["n3"])
+        for fmt, key in (("bf16", "m_bf16"), ("fp16", "m_fp16")):
+            printed = int(row[key])
+            v = math.ceil(max(n1, n3) / P.b_star * o.law_sigma_over_rms(n1, n2, n3, 1, fmt, P))
+            if printed == mcomb:
+                assert v <= mcomb, (row, fmt, v)
+            else:
+                assert v == printed, (row, fmt, v)
+    # the law falls as 1/m: sigma of an m-bucket sketch is the m = 1 value over m
+    base = o.law_sigma_over_rms(8192, 4096, 4096, 1, "bf16", P)
+    for m in (2, 48, 1000):
+        assert abs(o.law_sigma_over_rms(8192, 4096, 4096, m, "bf16", P) * m - base) <= 1e-15 * base
+
+
+def _abs_contrib_loops(a, b, c, hr):
+    """Per-bucket sums of absolute contributions written out with explicit loops: for bucket
+    (a, b), sum_k (sum_{i in a} w|A_ik|)(sum_{j in b} w|B_kj|) + sum_{i in a, j in b} w|C_ij|,
+    with w = 1 for S, w_i = (i+1)/2^ceil(log2 n1) for R and w_j = (j+1)/2^ceil(log2 n3) for T."""
+    n1, n2 = a.shape
+    n3 = b.shape[1]
+    m = hr.m
+    L1 = 1
+    while L1 < n1:
+        L1 *= 2
+    L3 = 1
+    while L3 < n3:
+        L3 *= 2
+    out = {name: np.zeros((m, m)) for name in "SRT"}
+    for ba in range(m):
+        rows = [i for i in range(n1) if hr.h1[i] == ba]
+        for bb in range(m):
+            cols = [j for j in range(n3) if hr.h2[j] == bb]
+            for name in "SRT":
+                wi = (lambda i: (i + 1) / L1) if name == "R" else (lambda i: 1.0)
+                wj = (lambda j: (j + 1) / L3) if name == "T" else (lambda j: 1.0)
+                tot = 0.0
+                for k in range(n2):
+                    sa = sum(wi(i) * abs(a[i, k]) for i in rows)
+                    sb = sum(wj(j) * abs(b[k, j]) for j in cols)
+                    tot += sa * sb
+                for i in rows:
+                    for j in cols:
+                        tot += wi(i) * wj(j) * abs(c[i, j])
+                out[name][ba, bb] = tot
+    return out["S"], out["R"], out["T"]
+
+
+def test_abs_contributions_against_explicit_sums():
+    """The float-parity scale D^S, D^R, D^T (the sum of absolute contributions of the factored
+    evaluation of Eq. 1 and of the first-moment sketches) against its definition evaluated with
+    plain loops, on a ragged case whose buckets are of unequal size."""
+    rng = np.random.default_rng(11)
+    n1, n2, n3, m = 7, 5, 9, 3
+    a = rng.standard_normal((n1, n2))
+    b = rng.standard_normal((n2, n3))
+    c = rng.standard_normal((n1, n3))
+    hr = o.make_round(5, 1, n1, n3, m)
+    assert len(set(np.bincount(hr.h1, minlength=m))) > 1   # buckets of unequal size
+    DS, DR, DT = o.abs_contributions(a, b, c, hr)
+    eS, eR, eT = _abs_contrib_loops(a, b, c, hr)
+    for got, exp in ((DS, eS), (DR, eR), (DT, eT)):
+        assert np.allclose(got, exp, rtol=1e-13, atol=0.0)
+    # R weights rows and T weights columns: the three scales differ
+    assert not np.allclose(DR, DT) and not np.allclose(DS, DR)
+
+
+def test_abs_contributions_bounds_fp32_evaluation_of_eq1():
+    """What the scale is for: an FP32 evaluation of the factored form (H1 A)(B H2^T) - H1 C H2^T
+    differs from the exact S by a small multiple of 2^-24 D^S per bucket (a sum of n terms in
+    FP32 errs by at most about n 2^-24 times the sum of their magnitudes)."""
+    rng = np.random.default_rng(3)
+    n1, n2, n3, m = 64, 48, 40, 4
+    a = rng.standard_normal((n1, n2)).astype(np.float32).astype(np.float64)
+    b = rng.standard_normal((n2, n3)).astype(np.float32).astype(np.float64)
+    c = (a @ b).astype(np.float32).astype(np.float64)
+    hr = o.make_round(9, 0, n1, n3, m)
+    S, _, _ = o.sketches(o.error_matrix(a, b, c), hr, moments=False)
+    H1 = np.zeros((m, n1), dtype=np.float32)
+    H1[hr.h1, np.arange(n1)] = hr.v1
+    H2 = np.zeros((m, n3), dtype=np.float32)
+    H2[hr.h2, np.arange(n3)] = hr.v2
+    a32, b32, c32 = a.astype(np.float32), b.astype(np.float32), c.astype(np.float32)
+    s32 = (H1 @ a32) @ (b32 @ H2.T) - H1 @ c32 @ H2.T
+    DS, _, _ = o.abs_contributions(a, b, c, hr)
+    err = np.abs(s32.astype(np.float64) - S)
+    assert np.all(err <= (n1 + n2 + n3) * 2.0 ** -24 * DS)
+    assert err.max() > 0.0        # the FP32 evaluation does round
+
+
 def test_scaling_limits():
     for row in load_golden("scaling_limits.csv"):
         n1, n2, n3 = int(row["n1"]), int(row["n2"]), int(row["n3"])
