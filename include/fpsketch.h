@@ -218,7 +218,10 @@ fpsketch_status fpsketch_apply(fpsketch_ctx* ctx, const void* A, const void* B, 
  * m' = max(m_comb, 16, min(ceil(m B1 / B*), m_max)).  If m' lies outside [m/1.25, 1.25 m] the
  * context rebuilds its probe hash, tables and workspace at m' and restarts the average.
  * Outputs (each may be NULL): the probe's m after the call, sigma_bar, and 1 if rebuilt.
- * With no clean probe recorded nothing changes. */
+ * With no clean probe recorded nothing changes.  When the rule asks for a rebuild at an m'
+ * above 4096 (the kernels' largest bucket count; Eq. 5 reaches it only beyond about
+ * 16384 x 16384 outputs) the context is left as it was, the outputs report the unchanged m, and
+ * the call returns FPSK_ESHAPE. */
 fpsketch_status fpsketch_calibrate_noise(fpsketch_ctx* ctx, const void* C, fpsketch_dtype c_dtype,
                                          void* stream, int32_t* m_out, double* sigma_bar_out,
                                          int32_t* rebuilt_out);

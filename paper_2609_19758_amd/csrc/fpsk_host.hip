@@ -1586,8 +1586,16 @@ fpsketch_status fpsketch_calibrate_noise(fpsketch_ctx* c, const void* C, fpsketc
     FPSK_TRY(rms_hat_device(c, static_cast<const float*>(C), st, &rms));
     int32_t m_new = c->m;
     recalibrate(c->n1, c->n3, c->m, sigma_bar, rms, c->p, &m_new, &rebuilt);
+    if (rebuilt && m_new > fpsk::kMaxM) {
+      // the noise asks for more buckets than the kernels take: nothing changes
+      if (m_out) *m_out = c->m;
+      if (sigma_bar_out) *sigma_bar_out = sigma_bar;
+      if (rebuilt_out) *rebuilt_out = 0;
+      return fail(FPSK_ESHAPE, "recalibrated bucket count " + std::to_string(m_new) +
+                                   " is beyond the kernels' 4096; the probe keeps m = " +
+                                   std::to_string(c->m));
+    }
     if (rebuilt) {
-      if (m_new > fpsk::kMaxM) m_new = fpsk::kMaxM;
       FPSK_TRY(build_probe(c, m_new, st));
       const double zero[2] = {0.0, 0.0};
       FPSK_HIP(hipMemcpyAsync(c->sigma_acc.p, zero, sizeof(zero), hipMemcpyHostToDevice, st));

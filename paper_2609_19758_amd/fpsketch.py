@@ -171,6 +171,55 @@ def _stream(stream) -> Optional[int]:
     return int(stream.cuda_stream)
 
 
+def _check_tensor(x, what: str, shapes, dtypes, device: Optional[int]):
+    """Raises ValueError unless the torch tensor x has one of `shapes` (or is 1-D with as many
+    elements), a dtype in `dtypes` (None: any), is contiguous and lives on GPU `device` (None:
+    any GPU).  None and raw integer device pointers pass unchecked: those are the caller's
+    responsibility.  Checked before any call into the library, so that a wrong-sized buffer is
+    never read or written out of bounds and a half matrix of the other format is not decoded as
+    if it were the context's."""
+    if x is None or isinstance(x, int):
+        return
+    shape = tuple(x.shape)
+    if shape not in [tuple(s) for s in shapes] and not (
+            x.dim() == 1 and any(x.numel() == int(np.prod(s)) for s in shapes)):
+        raise ValueError(f"{what}: shape {shape}, expected "
+                         f"{' or '.join(str(tuple(s)) for s in shapes)}")
+    if dtypes is not None and x.dtype not in dtypes:
+        raise ValueError(f"{what}: dtype {x.dtype}, expected "
+                         f"{' or '.join(str(d) for d in dtypes)}")
+    if not x.is_contiguous():
+        raise ValueError(f"{what}: not contiguous (row-major without padding is required)")
+    if not x.is_cuda:
+        raise ValueError(f"{what}: on {x.device}, expected a GPU tensor")
+    if device is not None and x.device.index != device:
+        raise ValueError(f"{what}: on {x.device}, the context is on cuda:{device}")
+
+
+def half_dtype(fmt: str):
+    import torch
+    return {"bf16": torch.bfloat16, "fp16": torch.float16}[fmt]
+
+
+def check_operands(n1: int, n2: int, n3: int, fmt: str, b_layout: int, device: Optional[int],
+                   A=None, B=None, C=None, d_dirty=None, c_float: bool = True):
+    """Validates the operands of one call against a context's shape and format: A (n1 x n2) and B
+    (n2 x n3, or W = B^T n3 x n2 with b_layout 1) in the context's half format, C (n1 x n3, and
+    FP32 when c_float; otherwise its type code is passed on and checked by the library before it
+    reads C), d_dirty an int32 flag; all contiguous and on the context's GPU."""
+    import torch
+    h = [half_dtype(fmt)]
+    _check_tensor(A, "A", [(n1, n2)], h, device)
+    _check_tensor(B, "W = B^T" if b_layout else "B", [(n3, n2) if b_layout else (n2, n3)], h,
+                  device)
+    _check_tensor(C, "C", [(n1, n3)], [torch.float32] if c_float else None, device)
+    if d_dirty is not None and not isinstance(d_dirty, int):
+        if d_dirty.dtype != torch.int32 or d_dirty.numel() < 1:
+            raise ValueError(f"d_dirty: {d_dirty.dtype} with {d_dirty.numel()} elements, "
+                             "expected at least one int32")
+        _check_tensor(d_dirty, "d_dirty", [tuple(d_dirty.shape)], None, device)
+
+
 def _c_dtype(C, c_dtype: Optional[int]) -> int:
     if c_dtype is not None:
         return c_dtype
@@ -248,6 +297,14 @@ class Verifier:
         _check(self.lib.fpsketch_create(n1, n2, n3, DTYPE_CODE[fmt], ctypes.byref(self.params),
                                         ctypes.byref(h)), "fpsketch_create")
         self.handle = h
+        import torch
+        self.device = torch.cuda.current_device()
+
+    def _ops(self, A=None, B=None, C=None, d_dirty=None, c_dtype=None):
+        # C's type code goes to the library, which rejects anything but FP32 before it reads C;
+        # only a code of FP32 stated for a tensor of another type would make it read past C
+        check_operands(self.n1, self.n2, self.n3, self.fmt, self.params.b_layout, self.device,
+                       A, B, C, d_dirty, c_float=c_dtype == F32)
 
     def close(self):
         if getattr(self, "handle", None):
@@ -268,6 +325,7 @@ class Verifier:
 
     def probe_status(self, A, B, C, d_dirty=None, stream=None, c_dtype=None) -> int:
         """Raw status of fpsketch_probe (used to test error paths)."""
+        self._ops(A, B, C, d_dirty, c_dtype)
         return self.lib.fpsketch_probe(self.handle, _ptr(A), _ptr(B), _ptr(C),
                                        _c_dtype(C, c_dtype), _ptr(d_dirty), _stream(stream))
 
@@ -277,12 +335,14 @@ class Verifier:
     def probe_deferred(self, A, B, C, d_dirty=None, stream=None, c_dtype=None):
         """fpsketch_probe_deferred: the verdict is final after two more deferred calls or
         probe_flush."""
+        self._ops(A, B, C, d_dirty, c_dtype)
         _check(self.lib.fpsketch_probe_deferred(self.handle, _ptr(A), _ptr(B), _ptr(C),
                                                 _c_dtype(C, c_dtype), _ptr(d_dirty),
                                                 _stream(stream)), "fpsketch_probe_deferred")
 
     def probe_cached_deferred(self, A, C, d_dirty=None, stream=None, c_dtype=None):
         """fpsketch_probe_cached_deferred (A and C streamed, verdict after the flush)."""
+        self._ops(A, None, C, d_dirty, c_dtype)
         _check(self.lib.fpsketch_probe_cached_deferred(self.handle, _ptr(A), _ptr(C),
                                                        _c_dtype(C, c_dtype), _ptr(d_dirty),
                                                        _stream(stream)),
@@ -293,9 +353,11 @@ class Verifier:
 
     def cache_b(self, B, stream=None):
         """Forms and keeps the probe's B side (B H2^T and max|B|) for the current m."""
+        self._ops(B=B)
         _check(self.lib.fpsketch_cache_b(self.handle, _ptr(B), _stream(stream)), "fpsketch_cache_b")
 
     def probe_cached_status(self, A, C, d_dirty=None, stream=None, c_dtype=None) -> int:
+        self._ops(A, None, C, d_dirty, c_dtype)
         return self.lib.fpsketch_probe_cached(self.handle, _ptr(A), _ptr(C), _c_dtype(C, c_dtype),
                                               _ptr(d_dirty), _stream(stream))
 
@@ -312,6 +374,7 @@ class Verifier:
 
     def localize(self, A, B, C, seed: int, sigma_from_probe: bool = False, cap: int = 4096,
                  stream=None, c_dtype=None):
+        self._ops(A, B, C, None, c_dtype)
         buf = (Fault * max(cap, 1))()
         n = _I32()
         st = self.lib.fpsketch_localize(self.handle, _ptr(A), _ptr(B), _ptr(C),
@@ -326,6 +389,7 @@ class Verifier:
     def apply_status(self, A, B, C, recs, seed: int, stream=None, c_dtype=None):
         """Raw status and still-dirty flag of fpsketch_apply (records as localize returns them:
         (i, j, delta, absolute, round) tuples)."""
+        self._ops(A, B, C, None, c_dtype)
         n = len(recs)
         buf = (Fault * max(n, 1))()
         for t, (i, j, d, ab, rnd) in enumerate(recs):
@@ -358,6 +422,7 @@ class Verifier:
         return {k: getattr(pi, k) for k, _ in PlanInfo._fields_}
 
     def calibrate_noise(self, C, stream=None, c_dtype=None):
+        self._ops(C=C, c_dtype=c_dtype)
         m, sb, rb = _I32(), _D(), _I32()
         _check(self.lib.fpsketch_calibrate_noise(self.handle, _ptr(C), _c_dtype(C, c_dtype),
                                                  _stream(stream), ctypes.byref(m),
@@ -366,6 +431,7 @@ class Verifier:
         return m.value, sb.value, bool(rb.value)
 
     def sketch(self, A, B, C, seed: int, rnd: int, m: int, moments: bool = True, stream=None):
+        self._ops(A, B, C)
         S = np.empty(m * m, dtype=np.float64)
         R = np.empty(m * m, dtype=np.float64)
         T = np.empty(m * m, dtype=np.float64)
@@ -381,6 +447,7 @@ class Verifier:
                 T.reshape(shape) if moments else None, float(mx[0]), float(mx[1]))
 
     def recheck(self, A, B, coords, stream=None):
+        self._ops(A, B)
         cs = np.ascontiguousarray(np.asarray(coords, dtype=np.int64).reshape(-1, 2))
         n = cs.shape[0]
         g = np.empty(max(n, 1), dtype=np.float64)

@@ -52,3 +52,36 @@ def test_calibration_converges_in_one_step(fk, fmt):
     assert not res["measured"][2]
     assert res["paper"][2]
     assert abs(res["paper"][1] - res["measured"][0]) <= 0.25 * res["measured"][0]
+
+
+def test_recalibration_beyond_the_kernels_bucket_limit_is_an_error(fk):
+    """Eq. 5's m' above the kernels' 4096 buckets (possible beyond 16384 x 16384 outputs; a tiny
+    index budget B* forces it here at 65536 x 64 x 8192, where m_max = 5792): the call returns
+    FPSK_ESHAPE, the probe keeps its m and goes on probing."""
+    import torch
+    from oracle import fpsketch_oracle as o
+    n1, n2, n3 = 65536, 64, 8192
+    g = torch.Generator(device="cuda").manual_seed(5)
+    A = torch.randn(n1, n2, device="cuda", generator=g).to(torch.bfloat16)
+    B = torch.randn(n2, n3, device="cuda", generator=g).to(torch.bfloat16)
+    C = torch.mm(A, B, out_dtype=torch.float32)
+    v = fk.Verifier(n1, n2, n3, "bf16", m=64, b_star=0.001)
+    flag = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        v.probe(A, B, C, d_dirty=flag)
+    torch.cuda.synchronize()
+    assert int(flag.item()) == 0
+    sb = v.probe_stats()["sigma_hat"]
+    want, rebuild = o.recalibrate_m(n1, n3, 64, sb, float(C.double().pow(2).mean().sqrt()),
+                                    o.Params(b_star=0.001))
+    assert rebuild and want > 4096, want       # the rule itself asks for m_max
+    with pytest.raises(fk.FpsketchError) as e:
+        v.calibrate_noise(C)
+    assert e.value.status == fk.ESHAPE and "4096" in str(e.value)
+    assert v.m == 64
+    v.probe(A, B, C, d_dirty=flag)
+    torch.cuda.synchronize()
+    assert int(flag.item()) == 0 and v.probe_stats()["dirty"] == 0.0
+    v.close()
+    del A, B, C
+    torch.cuda.empty_cache()
