@@ -160,6 +160,21 @@ fpsketch_status fpsketch_localize(fpsketch_ctx* ctx, const void* A, const void* 
                                   fpsketch_dtype c_dtype, uint64_t seed, int32_t sigma_from_probe,
                                   fpsketch_fault* out, int32_t cap, int32_t* n_out, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): fpsketch_probe with the same kernels, the same
+ * statistics bit for bit and the same effect on d_dirty and on the context's noise average, but
+ * the stream pass's factors and partials live in a scratch array of 16 MiB that the library
+ * holds on each GPU it runs on until the process ends, instead of the context's workspace.  The
+ * call allocates nothing (no hipMalloc, hipFree or allocating library routine; it never creates
+ * timing events, so fpsketch_timing does not cover it) and enqueues only kernels on `stream`.
+ * Takes the probe's block path only (m <= 64, n2 <= 16384; every such shape fits the array):
+ * FPSK_ESHAPE otherwise.  Every call on one GPU shares its array, which keeps the last call's
+ * contents: calls that overlap in time on one GPU (other streams, contexts or host threads)
+ * race and must not be issued; calls ordered on one stream are safe.  Errors as fpsketch_probe. */
+fpsketch_status fpsketch_probe_noalloc(fpsketch_ctx* ctx, const void* A, const void* B,
+                                       const void* C, fpsketch_dtype c_dtype, int32_t* d_dirty,
+                                       void* stream);
+
 /* The B-side cache of the probe (Sec. III-C; Algorithm 2's probe keeps BH2^T of a weight):
  * forms Q = B H2^T for the probe's current hash round and m, and max |B|, from the device weight
  * B (n2 x n3, the context's half format, row-major) and keeps them in the context.  Enqueue only

@@ -10,6 +10,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <numeric>
 #include <string>
 #include <unordered_map>
@@ -632,6 +633,34 @@ void free_workspace(Workspace& W) {
 }  // namespace
 
 // ------------------------------------------------------------------------------------------
+// Scratch of fpsketch_probe_noalloc: one array per GPU that runs the library, held until the
+// process ends.  In host code `scratch` names a host-side stand-in, not device memory: kernels
+// and copies take the device address that hipGetSymbolAddress gives on each device, resolved
+// once per device (with that device current) when the first context on it is created.
+
+namespace {
+
+constexpr size_t kScratchBytes = size_t{16} << 20;    // 16 MiB
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+std::unordered_map<int, unsigned char*> g_scratch_addr;   // device -> address of its scratch
+
+fpsketch_status scratch_address(int dev, unsigned char** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  auto it = g_scratch_addr.find(dev);
+  if (it == g_scratch_addr.end()) {
+    void* p = nullptr;
+    FPSK_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    it = g_scratch_addr.emplace(dev, static_cast<unsigned char*>(p)).first;
+  }
+  *out = it->second;
+  return FPSK_OK;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------------
 // Context.
 
 struct fpsketch_ctx {
@@ -674,6 +703,7 @@ struct fpsketch_ctx {
   int pipe_nprod = 0, pipe_xb = 1;
   hipStream_t pipe_stream = nullptr;
   fpsketch_plan_info last_plan{};
+  unsigned char* scratch_dev = nullptr;   // this device's scratch (fpsketch_probe_noalloc)
 
   // optional per-probe events: start and end of the stream kernel, of the product dispatches
   bool timing = false;
@@ -1243,6 +1273,7 @@ fpsketch_status fpsketch_create(int64_t n1, int64_t n2, int64_t n3, fpsketch_dty
     if (e != hipSuccess) s = fail(FPSK_EHIP, std::string("hipMemset: ") + hipGetErrorString(e));
   }
   if (s == FPSK_OK) s = build_probe(c, static_cast<int>(m), nullptr);
+  if (s == FPSK_OK) s = scratch_address(dev, &c->scratch_dev);
   if (s != FPSK_OK) {
     fpsketch_destroy(c);
     return s;
@@ -1291,6 +1322,58 @@ fpsketch_status fpsketch_probe(fpsketch_ctx* c, const void* A, const void* B, co
   }
   return run_pass(c, c->probe_round, c->probe_ws, A, B, static_cast<const float*>(C), false, 1,
                   d_dirty, nullptr, nullptr, nullptr, st, ev);
+}
+
+// fpsketch_probe on the block path with its factors (P, Q), C-grid partials, block-product
+// partials and per-work-group maxima carved from this device's scratch instead of the
+// context's workspace.  The factors' padding columns [n2, kact) must read as zero in the
+// products; the scratch keeps whatever the previous call left there, so a fill kernel clears
+// them (a kernel, not a memset, so that the call stays capturable).
+fpsketch_status fpsketch_probe_noalloc(fpsketch_ctx* c, const void* A, const void* B,
+                                       const void* C, fpsketch_dtype c_dtype, int32_t* d_dirty,
+                                       void* stream) {
+  FPSK_TRY(check_matrices(c, A, B, C, c_dtype));
+  const Decomp& d = c->probe_ws.d;
+  if (d.nX == 0) {
+    return fail(FPSK_ESHAPE, "the probe without allocation takes the block path only (m <= 64, "
+                             "n2 <= 16384); this context has m = " + std::to_string(d.m));
+  }
+  if (c->scratch_dev == nullptr) return fail(FPSK_EINVAL, "internal: no scratch address");
+  FPSK_TRY(set_device(c));
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  FPSK_TRY(pipe_flush(c, st));
+  const size_t mm = static_cast<size_t>(d.m) * d.m;
+  const size_t fm = static_cast<size_t>(d.m) * d.ldp * sizeof(float);
+  size_t off = 0;
+  auto take = [&off](size_t bytes) {
+    const size_t o = off;
+    off += (bytes + 255) / 256 * 256;
+    return o;
+  };
+  const size_t oP = take(fm), oQ = take(fm);
+  const size_t oS = take(mm * d.npc * sizeof(double));
+  const size_t oX = take(mm * d.xns * sizeof(double));
+  const size_t oM = take(static_cast<size_t>(d.nA + d.nB) * sizeof(float));
+  if (off > kScratchBytes) {
+    return fail(FPSK_ESHAPE, "the probe without allocation needs " + std::to_string(off) +
+                                 " bytes of scratch, more than its " +
+                                 std::to_string(kScratchBytes));
+  }
+  Workspace W;            // a view of the scratch: owns nothing and is never freed
+  W.d = d;
+  W.ds = d;
+  W.P.p = c->scratch_dev + oP;
+  W.Q.p = c->scratch_dev + oQ;
+  W.partS.p = c->scratch_dev + oS;
+  W.xpart.p = c->scratch_dev + oX;
+  W.maxpart.p = c->scratch_dev + oM;
+  if (d.kact > c->n2) {
+    const int n2 = static_cast<int>(c->n2);
+    FPSK_HIP(fpsk::launch_zero_cols(as<float>(W.P), d.m, d.ldp, n2, d.kact, st));
+    FPSK_HIP(fpsk::launch_zero_cols(as<float>(W.Q), d.m, d.ldp, n2, d.kact, st));
+  }
+  return run_pass(c, c->probe_round, W, A, B, static_cast<const float*>(C), false, 1, d_dirty,
+                  nullptr, nullptr, nullptr, st);
 }
 
 fpsketch_status fpsketch_cache_b(fpsketch_ctx* c, const void* B, void* stream) {

@@ -188,6 +188,8 @@ struct ApplyEntry {    // one record of the apply step: C[o] <- d, or C[o] + d
   int32_t pad;
 };
 hipError_t launch_apply(float* C, const ApplyEntry* list, int n, hipStream_t st);
+// Zeroes columns [c0, c1) of rows x ld FP32 rows (c1 <= ld).
+hipError_t launch_zero_cols(float* base, int rows, int ld, int c0, int c1, hipStream_t st);
 struct Cand {          // a bucket above the cut with its three sketches
   int64_t o;
   double s, r, t;

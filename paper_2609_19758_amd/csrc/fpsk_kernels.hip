@@ -10,6 +10,8 @@
 // select:   exact order statistics, peel and candidate scan of a localize round (Algorithm 1).
 #include "fpsk_block.h"
 
+#include <algorithm>
+
 namespace fpsk {
 
 // ----------------------------------------------------------------------------------------
@@ -861,6 +863,27 @@ hipError_t launch_median_mad(const double* S, int64_t n, SelState* st, uint32_t*
   if (n <= 0) return hipErrorInvalidValue;
   select_median<0>(S, n, st, hist, s);
   select_median<1>(S, n, st, hist, s);
+  return hipGetLastError();
+}
+
+// Zeroes columns [c0, c1) of `rows` rows of a row-major FP32 matrix whose rows are ld apart.
+__global__ __launch_bounds__(kThreads) void zero_cols_kernel(float* base, int rows, int ld,
+                                                             int c0, int c1) {
+  const int64_t w = c1 - c0;
+  const int64_t total = static_cast<int64_t>(rows) * w;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < total;
+       i += static_cast<int64_t>(gridDim.x) * kThreads) {
+    const int64_t r = i / w;
+    base[r * ld + c0 + (i - r * w)] = 0.0f;
+  }
+}
+
+hipError_t launch_zero_cols(float* base, int rows, int ld, int c0, int c1, hipStream_t st) {
+  if (rows <= 0 || c1 <= c0) return hipSuccess;
+  if (c0 < 0 || c1 > ld) return hipErrorInvalidValue;
+  const int64_t total = static_cast<int64_t>(rows) * (c1 - c0);
+  const int grid = static_cast<int>(std::min<int64_t>(256, (total + kThreads - 1) / kThreads));
+  hipLaunchKernelGGL(zero_cols_kernel, dim3(grid), dim3(kThreads), 0, st, base, rows, ld, c0, c1);
   return hipGetLastError();
 }
 

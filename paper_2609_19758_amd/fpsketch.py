@@ -67,6 +67,7 @@ _SIGS = {
     "fpsketch_cache_b": (ctypes.c_int, [_P, _P, _P]),
     "fpsketch_probe_cached": (ctypes.c_int, [_P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_probe_deferred": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _P, _P]),
+    "fpsketch_probe_noalloc": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_probe_flush": (ctypes.c_int, [_P, _P]),
     "fpsketch_probe_cached_deferred": (ctypes.c_int, [_P, _P, _P, ctypes.c_int, _P, _P]),
     "fpsketch_apply": (ctypes.c_int, [_P, _P, _P, _P, ctypes.c_int, ctypes.POINTER(Fault), _I32,
@@ -331,6 +332,17 @@ class Verifier:
 
     def probe(self, A, B, C, d_dirty=None, stream=None, c_dtype=None):
         _check(self.probe_status(A, B, C, d_dirty, stream, c_dtype), "fpsketch_probe")
+
+    def probe_noalloc_status(self, A, B, C, d_dirty=None, stream=None, c_dtype=None) -> int:
+        """Raw status of fpsketch_probe_noalloc (the probe with the library's static scratch)."""
+        self._ops(A, B, C, d_dirty, c_dtype)
+        return self.lib.fpsketch_probe_noalloc(self.handle, _ptr(A), _ptr(B), _ptr(C),
+                                               _c_dtype(C, c_dtype), _ptr(d_dirty),
+                                               _stream(stream))
+
+    def probe_noalloc(self, A, B, C, d_dirty=None, stream=None, c_dtype=None):
+        _check(self.probe_noalloc_status(A, B, C, d_dirty, stream, c_dtype),
+               "fpsketch_probe_noalloc")
 
     def probe_deferred(self, A, B, C, d_dirty=None, stream=None, c_dtype=None):
         """fpsketch_probe_deferred: the verdict is final after two more deferred calls or
