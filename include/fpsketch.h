@@ -7,10 +7,10 @@
  *   - probes: forms the sum sketch S = H1 E H2^T of E = AB - C without forming AB (Eq. 1) and
  *     decides clean/dirty against the probe threshold (Sec. III-C, III-E, III-I, Algorithm 2);
  *   - localizes: on a dirty product, forms first-moment sketches R, T with power-of-two scaled
- *     index weights, recovers each isolated error as a ratio (Eq. 2) and accepts a candidate
- *     only if an independent recomputation of that entry disagrees with C (Sec. III-D,
- *     Algorithm 1), over k peeled hash rounds (Sec. III-H), after an exact scan for
- *     non-finite and out-of-range entries (Sec. III-I);
+ *     index weights, recovers each isolated error as a ratio (Eq. 2) and keeps a candidate
+ *     entry only when recomputing its dot product afresh differs from C beyond the rounding
+ *     bound (Sec. III-D, Algorithm 1), over k peeled hash rounds (Sec. III-H), after an exact
+ *     scan for non-finite and out-of-range entries (Sec. III-I);
  *   - recalibrates the probe's bucket count from noise measured on clean calls (Sec. III-G).
  *
  * Conventions (all entry points):

@@ -478,56 +478,84 @@ class RoundTrace:
     S: np.ndarray
 
 
-def localize_round(a64, b64, E, hr: HashRound, r: int, tau: float, F: list, p: Params,
-                   rnd: int, trace: list | None = None):
-    """Algorithm 1: one round of floating-point localization.  Appends accepted faults to F."""
-    n1, n3 = E.shape
-    m = hr.m
-    S, R, T = sketches(E, hr, moments=True)
-    peel(S, R, T, hr, F, n1, n3)
+def round_cut(S: np.ndarray, n1: int, n3: int, r: int, tau: float):
+    """The round's noise and thresholds (Sec. III-E, III-G): sigma_MAD of the peeled S, the
+    candidate threshold tau_c = min(tau, 2 sigma_MAD), the decodability threshold
+    tau_d = max(n1, n3) sigma_MAD / max(r, 1/2), and the cut max(tau_c, tau_d) a bucket must
+    exceed."""
     sig = mad_sigma(S)
     tau_c = min(tau, 2.0 * sig)
     tau_d = max(n1, n3) * sig / max(r, 0.5)
-    cut = max(tau_c, tau_d)
+    return sig, tau_c, tau_d, max(tau_c, tau_d)
+
+
+def candidate_buckets(S, R, T, cut: float, K: int):
+    """Buckets above the cut (Sec. III-E): Q is the K largest |S_ab| in the order |S_ab|
+    descending, then flat index a*m + b ascending; U keeps those of Q whose S is nonzero and
+    whose S, R and T are finite (Eq. 2 needs all three), in Q's order."""
     absS = np.abs(S).ravel()
-    # Q: the K largest |S_ab| above the cut; ties broken by the flat index a*m + b.
-    above = np.flatnonzero(absS > cut)
-    order = sorted(above.tolist(), key=lambda f: (-absS[f], f))[:p.K]
     Sf, Rf, Tf = S.ravel(), R.ravel(), T.ravel()
-    U = [f for f in order
-         if Sf[f] != 0.0 and math.isfinite(Sf[f]) and math.isfinite(Rf[f]) and math.isfinite(Tf[f])]
+    above = np.flatnonzero(absS > cut)
+    Q = sorted(above.tolist(), key=lambda f: (-absS[f], f))[:K]
+    U = [f for f in Q if Sf[f] != 0.0 and all(math.isfinite(x) for x in (Sf[f], Rf[f], Tf[f]))]
+    return Q, U
+
+
+def bucket_centers(U, S, R, T, n1: int, n3: int) -> dict:
+    """Eq. 2 for each usable bucket: the 1-based indices 2^L R/S and 2^L' T/S, rounded half to
+    even and returned 0-based; a non-finite ratio or one beyond 2^40 gives no center."""
     L1, L3 = pow2_ceil(n1), pow2_ceil(n3)
+    Sf, Rf, Tf = S.ravel(), R.ravel(), T.ravel()
     centers = {}
     for f in U:
-        # Eq. 2, rounded half to even; a non-finite or out-of-range ratio leaves no center.
         ri = L1 * Rf[f] / Sf[f]
         rj = L3 * Tf[f] / Sf[f]
-        if not (math.isfinite(ri) and math.isfinite(rj)) or abs(ri) > 2.0 ** 40 or \
-                abs(rj) > 2.0 ** 40:
-            continue
-        centers[f] = (int(np.rint(ri)) - 1, int(np.rint(rj)) - 1)
-    live = [f for f in U if f in centers]
-    inF = {(g.i, g.j) for g in F}
+        if all(math.isfinite(x) and abs(x) <= 2.0 ** 40 for x in (ri, rj)):
+            centers[f] = (int(np.rint(ri)) - 1, int(np.rint(rj)) - 1)
+    return centers
+
+
+def search_windows(order, centers: dict, E, a64, b64, r: int, F: list, p: Params, rnd: int):
+    """The validated search (Sec. III-D, Sec. III-E): the (2r+1)^2 windows around the centers
+    are visited offset by offset in the canonical window order, and at each offset every bucket
+    still searching, in `order`, tests its coordinate.  A coordinate outside C or already in F is
+    passed over; one whose FP64 error exceeds its validation bound tau_ij is accepted (appended to
+    F as round `rnd`) and ends its bucket's search."""
+    n1, n3 = E.shape
+    searching = [f for f in order if f in centers]
+    found = {(g.i, g.j) for g in F}
     for di, dj in window_offsets(r):
-        if not live:
+        if not searching:
             break
-        still = []
-        for f in live:
-            ci, cj = centers[f]
-            i, j = ci + di, cj + dj
-            if i < 0 or i >= n1 or j < 0 or j >= n3 or (i, j) in inF:
-                still.append(f)
-                continue
-            e = float(E[i, j])
-            if abs(e) > validation_bound(a64, b64, i, j, p):
-                F.append(Fault(i, j, e, False, rnd))
-                inF.add((i, j))
+        keep = []
+        for f in searching:
+            i, j = centers[f][0] + di, centers[f][1] + dj
+            inside = 0 <= i < n1 and 0 <= j < n3
+            if inside and (i, j) not in found and abs(float(E[i, j])) > \
+                    validation_bound(a64, b64, i, j, p):
+                F.append(Fault(i, j, float(E[i, j]), False, rnd))
+                found.add((i, j))
             else:
-                still.append(f)
-        live = still
+                keep.append(f)
+        searching = keep
+    return F
+
+
+def localize_round(a64, b64, E, hr: HashRound, r: int, tau: float, F: list, p: Params,
+                   rnd: int, trace: list | None = None):
+    """One round of localization (Algorithm 1) from the definitions above: the sketches of this
+    round's hash, with the faults found so far peeled; the cut; the candidate buckets; their
+    centers (Eq. 2); the validated search.  Appends accepted faults to F."""
+    n1, n3 = E.shape
+    S, R, T = sketches(E, hr, moments=True)
+    peel(S, R, T, hr, F, n1, n3)
+    sig, tau_c, tau_d, cut = round_cut(S, n1, n3, r, tau)
+    Q, U = candidate_buckets(S, R, T, cut, p.K)
+    centers = bucket_centers(U, S, R, T, n1, n3)
+    search_windows(U, centers, E, a64, b64, r, F, p, rnd)
     if trace is not None:
-        trace.append(RoundTrace(sig, tau_c, tau_d, int(np.count_nonzero(absS > tau_c)), order, U,
-                                centers, S))
+        trace.append(RoundTrace(sig, tau_c, tau_d, int(np.count_nonzero(np.abs(S) > tau_c)), Q,
+                                U, centers, S))
     return F
 
 

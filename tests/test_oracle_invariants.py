@@ -197,7 +197,8 @@ def _noise_case(n1, n2, n3, seed, noise=1e-3):
 
 
 def test_tau_c_clean_bucket_rate_inside_a_round():
-    """Sec. III-E: about 4.6 % of clean buckets clear tau_c = min(tau, 2 sigma_MAD)."""
+    """Sec. III-E puts the share of clean buckets above tau_c = min(tau, 2 sigma_MAD) near
+    4.6 % (two-sided Gaussian tail at 2 sigma); a round must see that share."""
     # bucket populations of ~64 x 64 entries keep S close to Gaussian
     a64, b64, cn = _noise_case(4096, 4, 4096, 31)
     E = o.error_matrix(a64, b64, cn)
@@ -288,3 +289,27 @@ def test_candidate_cap_limits_one_round():
     got = {(f.i, f.j) for f in F}
     assert len(got) == 128
     assert got == set(sites[72:])           # the 128 largest magnitudes
+
+
+def test_search_is_offset_major():
+    """The validated search visits offsets in the outer loop and buckets in the inner one
+    (Sec. III-E): at offset (0, 0) bucket 2 claims (5, 6) at its own center, so bucket 1, whose
+    window also holds (5, 6), passes over it and never reaches (5, 7), which lies outside its
+    window.  Searching bucket by bucket instead would let bucket 1 claim (5, 6) and bucket 2 then
+    claim (5, 7)."""
+    n1 = n3 = 12
+    P = o.Params()
+    a64 = np.full((n1, 2), 0.01)
+    b64 = np.full((2, n3), 0.01)            # validation bounds of about 2.4e-9
+    E = np.zeros((n1, n3))
+    E[5, 6] = E[5, 7] = 1.0
+    F = o.search_windows([10, 20], {10: (5, 5), 20: (5, 6)}, E, a64, b64, 1, [], P, 1)
+    assert [(f.i, f.j, f.round) for f in F] == [(5, 6, 1)]
+    # a coordinate outside C is passed over and the bucket goes on searching
+    E2 = np.zeros((n1, n3))
+    E2[0, 1] = -2.0
+    F2 = o.search_windows([7], {7: (0, 0)}, E2, a64, b64, 1, [], P, 2)
+    assert [(f.i, f.j, f.delta) for f in F2] == [(0, 1, -2.0)]
+    # an entry already found is not found again, and a bucket without a center is skipped
+    F3 = o.search_windows([7, 8], {7: (0, 0)}, E2, a64, b64, 1, list(F2), P, 3)
+    assert len(F3) == 1

@@ -178,7 +178,8 @@ def test_clipped_mean_constant_is_sqrt_pi_over_2():
 
 
 def test_mad_reading_matches_stated_clean_bucket_rate():
-    """Sec. III-E: about 4.6 % of clean buckets clear tau_c = 2 sigma_MAD."""
+    """Sec. III-E puts the share of clean buckets above tau_c = 2 sigma_MAD near 4.6 %; only the
+    MAD of the signed sketch gives that share (the two-sided Gaussian tail at 2 sigma)."""
     rng = np.random.Generator(np.random.PCG64(4))
     S = rng.standard_normal(2_000_000) * 1.7
     sig = o.mad_sigma(S)
@@ -201,7 +202,8 @@ def test_huge_limit():
 
 
 def test_bit26_flip_example():
-    """Sec. VI-A: a flip of bit 26 on an accumulator holding 16 produced exactly 4096."""
+    """Sec. VI-A's worked example: an FP32 value of 16 with bit 26 (an exponent bit) flipped
+    reads 4096, i.e. 256 times larger."""
     assert wl.flip_bit_value(16.0, wl.FP32_EXP_BIT26) == 4096.0
 
 
