@@ -24,6 +24,7 @@ if ROOT not in sys.path:
 METRIC = ("verify µs/call + HBM GB/s (A,B,C read) at 4096³ BF16; "
           "fault recovery rate")
 HBM_PEAK_GBS = 8000.0
+FP64_PEAK_TFLOPS = 78.6      # MI355X dense FP64, matrix and vector alike
 
 
 def log(msg: str):
@@ -601,6 +602,15 @@ def main() -> int:
                                "recomputed": recomputed, "delivered_correct": delivered_ok,
                                "apply_ms_median": round(float(np.median(apply_us)) / 1e3, 3)
                                if apply_us else None}},
+        # the bucket-space product S = P Q - S_C: 2 m^2 n2 FP64 FLOP per call against the FP64
+        # peak, over the event-timed product and decision (matrix cores above m = 64, FP64 FMAs
+        # on the block path below)
+        "product_roofline": {"bound": "fp64-matrix" if v.m > 64 else "fp64-vector",
+                             "flop": 2 * v.m * v.m * w.n2,
+                             "achieved": round(2 * v.m * v.m * w.n2 / (p_us * 1e-6) / 1e12, 3),
+                             "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s",
+                             "frac": round(2 * v.m * v.m * w.n2 / (p_us * 1e-6) / 1e12
+                                           / FP64_PEAK_TFLOPS, 4)},
         # the whole call (stream pass, product and decision) against the same roofline
         "call_roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                           "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)},

@@ -462,7 +462,7 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   // With moments: four 16 x 16 quadrants (32 x 32 tiles) up to m = 2048 (the 64 x 64 tile's
   // three accumulator sets leave one wave per SIMD: 1.1 to 1.8x slower at m = 256 to 1024), then
   // 64 x 64 (its operand reuse wins at m = 4096).  Without the split, slices for at most 1024
-  // work-groups.  A wave takes k in steps of 16; at most 32 slices.
+  // work-groups.  A wave takes k in steps of 32 or 16; at most 32 slices.
   if (!mom) {
     const int t16 = (m + 15) / 16;
     d.kw = t16 * t16 < 256;
@@ -473,7 +473,9 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   }
   d.nt = (m + d.ts - 1) / d.ts;
   const int tiles = d.nt * d.nt;
-  const int kstep = d.kw ? 64 : 16;
+  // k per work-group slice: whole steps of the waves' k-loops (32 k per step for S alone on the
+  // quadrant tiles, else 16; with the k-range split over the 4 waves, four of those)
+  const int kstep = d.kw ? 64 : (mom ? 16 : 32);
   // k-slices rounded down, so that tiles x slices stays within the work-groups one round of the
   // chip holds (4 per CU for the 64 x 64 tiles): rounding up left a second round of a few
   // work-groups (m = 698: 121 tiles x 9 slices = 1089; now 8 slices, 373 -> 337 us)

@@ -116,11 +116,17 @@ __global__ __launch_bounds__(kThreads) void mfma_product_kernel(ProductArgs pa) 
   const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int ro = KW ? 0 : (w >> 1) * WT, co = KW ? 0 : (w & 1) * WT;   // wave origin in the tile
-  // the wave's k-range: whole steps of 16 (loads at or past kact read zeros)
+  // k per step: 32 for S alone on the quadrant tiles (large m), so that the 4 lanes of a factor
+  // row read one whole 128-byte line (two 16-byte pieces each) per step (m = 698: 339 -> 332 us
+  // for product and decision); 16 with moments (the registers of three products) and on the
+  // k-split tiles of mid m, where it measured slower
+  constexpr int NE = (MOM || KW) ? 1 : 2;   // 16-byte pieces per lane and operand per step
+  constexpr int KS = 16 * NE;
+  // the wave's k-range: whole steps (loads at or past kact read zeros)
   const int kw = KW ? pa.ksl / 4 : pa.ksl;
   const int kbeg = slice * pa.ksl + (KW ? w * kw : 0);
   const int kend = (kbeg + kw < pa.kact) ? kbeg + kw : pa.kact;
-  const int kq = 4 * (lane >> 4);
+  const int kq = 4 * NE * (lane >> 4);
   // factor rows of this lane (rows past m repeat row m - 1; their outputs are dropped)
   const float* pr[NF][WB];
   const float* qr[NF][WB];
@@ -146,34 +152,37 @@ __global__ __launch_bounds__(kThreads) void mfma_product_kernel(ProductArgs pa) 
       for (int j = 0; j < WB; ++j) acc[x][i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
 
   // every step's loads are issued one step ahead (the last step reloads itself, in bounds)
-  auto load = [&](float4 (&pv)[NF][WB], float4 (&qv)[NF][WB], int k) {
-    const bool ok = k + kq < pa.kact;    // kact is a multiple of 4: a float4 is in or out
-    const int kk = ok ? k : -kq;         // a float4 past the row reads the row's first instead
+  auto load = [&](float4 (&pv)[NF][WB][NE], float4 (&qv)[NF][WB][NE], int k) {
     const float4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int f = 0; f < NF; ++f)
+    for (int h = 0; h < NE; ++h) {
+      const bool ok = k + kq + 4 * h < pa.kact;   // kact is a multiple of 4: a float4 is in or out
+      const int kk = ok ? k + 4 * h : -kq;        // one past the row reads the row's first
 #pragma unroll
-      for (int i = 0; i < WB; ++i) {
-        const float4 p = *reinterpret_cast<const float4*>(pr[f][i] + kk);
-        const float4 q = *reinterpret_cast<const float4*>(qr[f][i] + kk);
-        pv[f][i] = ok ? p : z;
-        qv[f][i] = ok ? q : z;
-      }
+      for (int f = 0; f < NF; ++f)
+#pragma unroll
+        for (int i = 0; i < WB; ++i) {
+          const float4 p = *reinterpret_cast<const float4*>(pr[f][i] + kk);
+          const float4 q = *reinterpret_cast<const float4*>(qr[f][i] + kk);
+          pv[f][i][h] = ok ? p : z;
+          qv[f][i][h] = ok ? q : z;
+        }
+    }
   };
-  float4 pv[NF][WB], qv[NF][WB];
+  float4 pv[NF][WB][NE], qv[NF][WB][NE];
   if (kbeg < kend) load(pv, qv, kbeg);
-  for (int k = kbeg; k < kend; k += 16) {
-    float4 pn[NF][WB], qn[NF][WB];
-    load(pn, qn, k + 16 < kend ? k + 16 : k);
+  for (int k = kbeg; k < kend; k += KS) {
+    float4 pn[NF][WB][NE], qn[NF][WB][NE];
+    load(pn, qn, k + KS < kend ? k + KS : k);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
+    for (int e = 0; e < 4 * NE; ++e) {
       double a[NF][WB], b[NF][WB];
 #pragma unroll
       for (int f = 0; f < NF; ++f)
 #pragma unroll
         for (int i = 0; i < WB; ++i) {
-          a[f][i] = static_cast<double>(pv[f][i][e]);
-          b[f][i] = static_cast<double>(qv[f][i][e]);
+          a[f][i] = static_cast<double>(pv[f][i][e >> 2][e & 3]);
+          b[f][i] = static_cast<double>(qv[f][i][e >> 2][e & 3]);
         }
 #pragma unroll
       for (int i = 0; i < WB; ++i)
@@ -192,10 +201,12 @@ __global__ __launch_bounds__(kThreads) void mfma_product_kernel(ProductArgs pa) 
 #pragma unroll
     for (int f = 0; f < NF; ++f)
 #pragma unroll
-      for (int i = 0; i < WB; ++i) {
-        pv[f][i] = pn[f][i];
-        qv[f][i] = qn[f][i];
-      }
+      for (int i = 0; i < WB; ++i)
+#pragma unroll
+        for (int h = 0; h < NE; ++h) {
+          pv[f][i][h] = pn[f][i][h];
+          qv[f][i][h] = qn[f][i][h];
+        }
   }
   // this wave's share of the C grid: groups g = g0, g0 + gs, ...
   {
