@@ -13,8 +13,12 @@ OUT = os.path.join(PKG, "libfpsketch.so")
 SOURCES = ["fpsk_stream.hip", "fpsk_kernels.hip", "fpsk_host.hip"]
 
 # gfx950 only; packed FP32 instructions disabled (hipcc forms them from plain float code).
+# Matrix-core accumulators in ordinary VGPRs: with the compiler's default the loop-carried
+# accumulators of the bucket-space product were copied between VGPRs and AGPRs on every k-step
+# and the 64 x 64 product tile took 192 registers (2 waves per SIMD) instead of 98.
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-mllvm", "-amdgpu-mfma-vgpr-form",
          "-Wall", "-Wno-unused-function", f"-I{os.path.join(ROOT, 'include')}"]
 
 

@@ -99,6 +99,41 @@ __device__ void lds_reduce_virtual(const double (&v)[N / NTR][NV], double* buf,
   }
 }
 
+// As lds_reduce_virtual, all NV values in one pass through a buffer of
+// lds_reduce_doubles<N, NV>() doubles (fewer barriers, more LDS).
+template <int N, int NV, int NTR>
+__device__ void lds_reduce_virtual_all(const double (&v)[N / NTR][NV], double* buf,
+                                       uint32_t max_mask, double (&out)[NV]) {
+  static_assert(N % NTR == 0 && N % 16 == 0 && N <= 4096, "levels of 16");
+  constexpr int VT = N / NTR;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+#pragma unroll
+    for (int j = 0; j < VT; ++j) buf[i * N + threadIdx.x + NTR * j] = v[j][i];
+  __syncthreads();
+  lds_reduce_level<N, NV, NTR>(buf, buf + NV * N, max_mask);
+  const double* res = lds_reduce_result<N, NV>(buf);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) out[i] = res[i];
+  __syncthreads();
+}
+
+// max of p[i] over i = t, t + stride, ... below n, with the loads issued eight at a time (a
+// loop of single loads waits one round trip per entry)
+__device__ __forceinline__ float strided_max(const float* p, int n, int t, int stride, float mx) {
+  for (int i0 = t; i0 < n; i0 += 8 * stride) {
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = i0 + j * stride;
+      x[j] = i < n ? p[i] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mx = fmaxf(mx, x[j]);
+  }
+  return mx;
+}
+
 // The probe's decision from the reduced statistics (Sec. III-B): clipped-mean noise estimate,
 // validity bound from max|A| and max|B|, threshold and verdict.
 __device__ inline void decide_tail(const ProductArgs& pa, double sum_abs, double max_abs,
@@ -303,8 +338,8 @@ __device__ void block_decide_body(const ProductArgs& pa, double* red) {
     }
   }
   // maxima are exact whatever the grouping
-  for (int i = t + NTR; i < pa.nA; i += NTR) amax = fmaxf(amax, pa.maxpart[i]);
-  for (int i = t + NTR; i < pa.nB; i += NTR) bmax = fmaxf(bmax, mb[i]);
+  amax = strided_max(pa.maxpart, pa.nA, t + NTR, NTR, amax);
+  bmax = strided_max(mb, pa.nB, t + NTR, NTR, bmax);
   double r5[VT][5];
 #pragma unroll
   for (int j = 0; j < VT; ++j) {

@@ -122,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void mfma_product_kernel(ProductArgs pa) 
   // k-split tiles of mid m, where it measured slower
   constexpr int NE = (MOM || KW) ? 1 : 2;   // 16-byte pieces per lane and operand per step
   constexpr int KS = 16 * NE;
-  // the wave's k-range: whole steps (loads at or past kact read zeros)
+  // the wave's k-range
   const int kw = KW ? pa.ksl / 4 : pa.ksl;
   const int kbeg = slice * pa.ksl + (KW ? w * kw : 0);
   const int kend = (kbeg + kw < pa.kact) ? kbeg + kw : pa.kact;
@@ -151,29 +151,22 @@ __global__ __launch_bounds__(kThreads) void mfma_product_kernel(ProductArgs pa) 
 #pragma unroll
       for (int j = 0; j < WB; ++j) acc[x][i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
 
-  // every step's loads are issued one step ahead (the last step reloads itself, in bounds)
+  // The wave's k-range in whole steps: past kend (the last slice's end at kact) the factor rows
+  // hold zeros up to ldp, which is at least kact rounded up to 1024, so the loads need no
+  // bounds test.  Two register sets alternate, each step's loads issued one step ahead.
+  const int kstop = kbeg < kend ? kbeg + (kend - kbeg + KS - 1) / KS * KS : kbeg;
   auto load = [&](float4 (&pv)[NF][WB][NE], float4 (&qv)[NF][WB][NE], int k) {
-    const float4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int h = 0; h < NE; ++h) {
-      const bool ok = k + kq + 4 * h < pa.kact;   // kact is a multiple of 4: a float4 is in or out
-      const int kk = ok ? k + 4 * h : -kq;        // one past the row reads the row's first
+    for (int h = 0; h < NE; ++h)
 #pragma unroll
       for (int f = 0; f < NF; ++f)
 #pragma unroll
         for (int i = 0; i < WB; ++i) {
-          const float4 p = *reinterpret_cast<const float4*>(pr[f][i] + kk);
-          const float4 q = *reinterpret_cast<const float4*>(qr[f][i] + kk);
-          pv[f][i][h] = ok ? p : z;
-          qv[f][i][h] = ok ? q : z;
+          pv[f][i][h] = *reinterpret_cast<const float4*>(pr[f][i] + k + 4 * h);
+          qv[f][i][h] = *reinterpret_cast<const float4*>(qr[f][i] + k + 4 * h);
         }
-    }
   };
-  float4 pv[NF][WB][NE], qv[NF][WB][NE];
-  if (kbeg < kend) load(pv, qv, kbeg);
-  for (int k = kbeg; k < kend; k += KS) {
-    float4 pn[NF][WB][NE], qn[NF][WB][NE];
-    load(pn, qn, k + KS < kend ? k + KS : k);
+  auto step = [&](const float4 (&pv)[NF][WB][NE], const float4 (&qv)[NF][WB][NE]) {
 #pragma unroll
     for (int e = 0; e < 4 * NE; ++e) {
       double a[NF][WB], b[NF][WB];
@@ -198,15 +191,22 @@ __global__ __launch_bounds__(kThreads) void mfma_product_kernel(ProductArgs pa) 
           }
         }
     }
-#pragma unroll
-    for (int f = 0; f < NF; ++f)
-#pragma unroll
-      for (int i = 0; i < WB; ++i)
-#pragma unroll
-        for (int h = 0; h < NE; ++h) {
-          pv[f][i][h] = pn[f][i][h];
-          qv[f][i][h] = qn[f][i][h];
-        }
+  };
+  // (a load past the last step rereads the last step: every iteration issues the same loads,
+  // so the waits for a step's operands never cover the next step's loads)
+  const int nst = (kstop - kbeg) / KS;
+  const int klast = kstop - KS;
+  if (nst > 0) {
+    float4 p0[NF][WB][NE], q0[NF][WB][NE], p1[NF][WB][NE], q1[NF][WB][NE];
+    load(p0, q0, kbeg);
+    int k = kbeg;
+    for (int s = 0; s + 2 <= nst; s += 2, k += 2 * KS) {
+      load(p1, q1, k + KS);
+      step(p0, q0);
+      load(p0, q0, k + 2 * KS <= klast ? k + 2 * KS : klast);
+      step(p1, q1);
+    }
+    if (nst & 1) step(p0, q0);
   }
   // this wave's share of the C grid: groups g = g0, g0 + gs, ...
   {
@@ -300,22 +300,43 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(ProductArgs pa) {
   const int ntiles = pa.nt * pa.nt;
   const int tile = blockIdx.x;
   const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
+  // each output's slices are added in slice order; SB slices' loads of all the thread's outputs
+  // are in flight together
+  constexpr int SB = MOM ? 1 : 4;
   double acc[NX][RT][RT];
 #pragma unroll
   for (int x = 0; x < NX; ++x)
 #pragma unroll
     for (int i = 0; i < RT; ++i)
 #pragma unroll
-      for (int j = 0; j < RT; ++j) {
-        double v = 0.0;
-#pragma unroll 8
-        for (int sl = 0; sl < pa.NS; ++sl) {
-          const int64_t o = ((static_cast<int64_t>(sl) * ntiles + tile) * NX + x) * TS * TS +
-                            (ty + 16 * i) * TS + tx + 16 * j;
-          v += pa.scratch[o];
-        }
-        acc[x][i][j] = v;
+      for (int j = 0; j < RT; ++j) acc[x][i][j] = 0.0;
+  for (int sl0 = 0; sl0 < pa.NS; sl0 += SB) {
+    double v[SB][NX][RT][RT];
+#pragma unroll
+    for (int s = 0; s < SB; ++s)
+#pragma unroll
+      for (int x = 0; x < NX; ++x)
+#pragma unroll
+        for (int i = 0; i < RT; ++i)
+#pragma unroll
+          for (int j = 0; j < RT; ++j) {
+            const int sl = sl0 + s < pa.NS ? sl0 + s : sl0;
+            const int64_t o = ((static_cast<int64_t>(sl) * ntiles + tile) * NX + x) * TS * TS +
+                              (ty + 16 * i) * TS + tx + 16 * j;
+            v[s][x][i][j] = pa.scratch[o];
+          }
+#pragma unroll
+    for (int s = 0; s < SB; ++s) {
+      if (sl0 + s < pa.NS) {
+#pragma unroll
+        for (int x = 0; x < NX; ++x)
+#pragma unroll
+          for (int i = 0; i < RT; ++i)
+#pragma unroll
+            for (int j = 0; j < RT; ++j) acc[x][i][j] += v[s][x][i][j];
       }
+    }
+  }
   finish_tile<TS, MOM>(pa, tile, acc, red);
 }
 
@@ -324,30 +345,52 @@ __global__ __launch_bounds__(kThreads) void reduce_kernel(ProductArgs pa) {
 // were loaded with the statistics.
 // The tile statistics reduced as the decision reduces them (1024 virtual threads, the same
 // bits on any work-group size): sum|S|, max|S|, non-finite count.
+static_assert(((kMaxM + 63) / 64) * ((kMaxM + 63) / 64) <= 4 * kDecideThreads,
+              "a probe's tiles (64 x 64, or 16 x 16 below 256 tiles) fit 4 per decision thread");
+
+// Virtual thread i's tile statistics: sum|S|, max|S| and non-finite count over tiles i,
+// i + kDecideThreads, ... in that order (at most 4096 tiles: the loads issued together).
+__device__ __forceinline__ void tile_partials(const ProductArgs& pa, int i, double& lsum,
+                                              double& lmax, double& lbad) {
+  const int ntiles = pa.nt * pa.nt;
+  lsum = 0.0;
+  lmax = 0.0;
+  lbad = 0.0;
+  for (int i0 = i; i0 < ntiles; i0 += 4 * kDecideThreads) {
+    double e[4][3];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int ti = i0 + j * kDecideThreads;
+      const bool ok = ti < ntiles;
+#pragma unroll
+      for (int q = 0; q < 3; ++q) e[j][q] = ok ? pa.tilestat[(ok ? ti : 0) * 4 + q] : 0.0;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (i0 + j * kDecideThreads < ntiles) {
+        lsum += e[j][0];
+        lmax = fmax(lmax, e[j][1]);
+        lbad += e[j][2];
+      }
+    }
+  }
+}
+
 template <int NTR>
 __device__ void tile_totals(const ProductArgs& pa, double* red, double (&out)[3]) {
   constexpr int N = kDecideThreads;
   constexpr int VT = N / NTR;
-  const int ntiles = pa.nt * pa.nt;
   double v[VT][3];
 #pragma unroll
   for (int j = 0; j < VT; ++j) {
-    double lsum = 0.0, lmax = 0.0, lbad = 0.0;
-    for (int i = threadIdx.x + NTR * j; i < ntiles; i += N) {
-      lsum += pa.tilestat[i * 4 + 0];
-      lmax = fmax(lmax, pa.tilestat[i * 4 + 1]);
-      lbad += pa.tilestat[i * 4 + 2];
-    }
-    v[j][0] = lsum;
-    v[j][1] = lmax;
-    v[j][2] = lbad;
+    tile_partials(pa, threadIdx.x + NTR * j, v[j][0], v[j][1], v[j][2]);
   }
   if constexpr (VT == 1) {
 #pragma unroll
     for (int i = 0; i < 3; ++i) out[i] = v[0][i];
     lds_reduce<N, 3>(out, red, 0x2u);
   } else {
-    lds_reduce_virtual<N, 3, NTR>(v, red, 0x2u, out);
+    lds_reduce_virtual_all<N, 3, NTR>(v, red, 0x2u, out);
   }
 }
 
@@ -357,7 +400,7 @@ __device__ void tile_totals(const ProductArgs& pa, double* red, double (&out)[3]
 // the tile's row-major buckets, then the work-group reduction).  Replaces one work-group's pass
 // over all m^2 buckets.
 __global__ __launch_bounds__(kThreads) void clip_kernel(ProductArgs pa) {
-  __shared__ double red[lds_reduce_doubles<kDecideThreads, 1>()];
+  __shared__ double red[lds_reduce_doubles<kDecideThreads, 3>()];
   double tot[3];
   tile_totals<kThreads>(pa, red, tot);
   const int m = pa.m;
@@ -369,11 +412,19 @@ __global__ __launch_bounds__(kThreads) void clip_kernel(ProductArgs pa) {
   const int ta = tile / pa.nt, tb = tile - ta * pa.nt;
   const int ts = pa.ts;
   double c2 = 0.0;
-  for (int e = threadIdx.x; e < ts * ts; e += kThreads) {
-    const int r = ta * ts + e / ts, c = tb * ts + e % ts;
-    if (r < m && c < m) {
-      const double a = fabs(pa.S[static_cast<int64_t>(r) * m + c]);
-      c2 += a < clip ? a : clip;
+  for (int e0 = threadIdx.x; e0 < ts * ts; e0 += 16 * kThreads) {   // 16 loads in flight
+    double a[16];
+    bool ok[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int e = e0 + j * kThreads;
+      const int r = ta * ts + e / ts, c = tb * ts + e % ts;
+      ok[j] = e < ts * ts && r < m && c < m;
+      a[j] = fabs(pa.S[ok[j] ? static_cast<int64_t>(r) * m + c : 0]);
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (ok[j]) c2 += a[j] < clip ? a[j] : clip;
     }
   }
   double r1[1] = {c2};
@@ -392,17 +443,12 @@ __global__ __launch_bounds__(kDecideThreads) void tile_decide_kernel(ProductArgs
   }
   const int64_t mm = static_cast<int64_t>(pa.m) * pa.m;
   const int ntiles = pa.nt * pa.nt;
-  double lsum = 0.0, lmax = 0.0, lbad = 0.0;
-  for (int i = t; i < ntiles; i += kDecideThreads) {
-    lsum += pa.tilestat[i * 4 + 0];
-    lmax = fmax(lmax, pa.tilestat[i * 4 + 1]);
-    lbad += pa.tilestat[i * 4 + 2];
-  }
+  double lsum, lmax, lbad;
+  tile_partials(pa, t, lsum, lmax, lbad);
   // (the same partials and tree as tile_totals, with the maxima of A and B as values 3 and 4)
-  float amax = 0.0f, bmax = 0.0f;
-  for (int i = t; i < pa.nA; i += kDecideThreads) amax = fmaxf(amax, pa.maxpart[i]);
   const float* mb = pa.maxpart_b != nullptr ? pa.maxpart_b : pa.maxpart + pa.nA;
-  for (int i = t; i < pa.nB; i += kDecideThreads) bmax = fmaxf(bmax, mb[i]);
+  const float amax = strided_max(pa.maxpart, pa.nA, t, kDecideThreads, 0.0f);
+  const float bmax = strided_max(mb, pa.nB, t, kDecideThreads, 0.0f);
   // sums: 0, 2; maxima: 1, 3, 4
   double r5[5] = {lsum, lmax, lbad, static_cast<double>(amax), static_cast<double>(bmax)};
   lds_reduce<kDecideThreads, 5>(r5, red, 0x1au);
@@ -416,7 +462,16 @@ __global__ __launch_bounds__(kDecideThreads) void tile_decide_kernel(ProductArgs
   if (!(nbad == 0.0 && max_abs <= clip)) {
     double c2 = 0.0;
     if (pa.clip_tiles) {
-      for (int i = t; i < ntiles; i += kDecideThreads) c2 += pa.tilestat[i * 4 + 3];
+      double e[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {       // at most 4096 tiles
+        const int ti = t + j * kDecideThreads;
+        e[j] = ti < ntiles ? pa.tilestat[ti * 4 + 3] : 0.0;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (t + j * kDecideThreads < ntiles) c2 += e[j];
+      }
     } else {
 #pragma unroll 8
       for (int64_t o = t; o < mm; o += kDecideThreads) {
