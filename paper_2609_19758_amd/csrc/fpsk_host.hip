@@ -407,7 +407,7 @@ struct Decomp {
   // probe block product (nX > 0): work-groups of xb x xb outputs over xns k-slices
   int xb = 0, xnb = 0, xns = 0, nX = 0;
   int xsr = 1, xsc = 1, xnstc = 1, xslots = 0;   // supertiles of blocks (XCD-local sets)
-  // B work-groups of fewer than 8 rows write Q k-major (n2 x m), then a transpose forms Q
+  // B work-groups of 1 or 2 rows write Q k-major (n2 x m), then a transpose forms Q
   bool qk = false;
   bool wt_a = false, wt_w = false;   // row-bucket work-groups of four tiles (small buckets)
 };
@@ -449,7 +449,7 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.nB = static_cast<int>((n2 + d.rb - 1) / d.rb);
   // B passed transposed: row-bucket work-groups over the rows of W = B^T, as many as A's
   if (transb) d.nB = m * (d.wt_w ? tq : d.TA);
-  d.qk = !transb && d.rb < 8 && !probe4;
+  d.qk = !transb && d.rb < 4;
   d.TC = static_cast<int>((n3 + kColTile - 1) / kColTile);
   int npc = static_cast<int>((1024 + m - 1) / m);
   npc = std::max(1, std::min(npc, d.TC));

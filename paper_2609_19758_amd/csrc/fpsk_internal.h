@@ -55,9 +55,9 @@ struct StreamArgs {
   float* Q;        // m x ldp      (B H2^T)^T: row b holds column b of B H2^T
   float* Qw;       // m x ldp      (B W2 H2^T)^T      (moments only)
   int ldp;
-  // B work-groups of fewer than 8 rows (m > 512) write Q (Qw) k-major instead, n2 x mq, for a
-  // transpose into Q: a bucket-major row per work-group would be a 16-byte or smaller piece per
-  // bucket, each a partial line write; null otherwise
+  // B work-groups of 1 or 2 rows (m > 1024) write Q (Qw) k-major instead, n2 x mq, for a
+  // transpose into Q: a bucket-major row per work-group would be an 8-byte or smaller piece per
+  // bucket; null otherwise
   float* Qk;
   float* Qwk;
   int mq;

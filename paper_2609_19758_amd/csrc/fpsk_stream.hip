@@ -328,6 +328,17 @@ struct BChunk {
   int qb[G], qe[G];
 };
 
+// The block of B rows that B work-group u takes.  A 4-row work-group writes a 16-byte piece of
+// every Q row; the 8 work-groups whose pieces fill one 128-byte line run on one XCD, one after
+// another, so that the line is whole in that XCD's L2 before it is written back.  Launch index i
+// runs on XCD i mod 8, so the units of one XCD are u, u + 8, u + 16, ...: unit u takes block
+// 64 (u / 64) + 8 (u mod 8) + (u / 8) mod 8 (whole groups of 64 units; the rest keep theirs).
+template <int RB>
+__device__ __forceinline__ int b_block(int u, int nB) {
+  if (RB != 4 || u >= nB / 64 * 64) return u;
+  return (u & ~63) | ((u & 7) << 3) | ((u >> 3) & 7);
+}
+
 template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
 __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, uint32_t* ldsu) {
   constexpr int CW = kBChunkHalfs / RB;      // columns per chunk
@@ -350,7 +361,7 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
   const int m = s.m;
   const int stride = s.btab_stride;
   const int rg = threadIdx.x / SLOTS, bslot = threadIdx.x - rg * SLOTS;
-  const int64_t k0 = static_cast<int64_t>(u) * RB;
+  const int64_t k0 = static_cast<int64_t>(b_block<RB>(u, s.nB)) * RB;
   double acc[G][RBG], accw[G][RBG];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -621,7 +632,19 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
 #pragma unroll
   for (int g = 0; g < (GF ? 0 : G); ++g) {
     const int b = bslot + SLOTS * g;
-    if (b < m) {
+    const int64_t kg = k0 + rg * RBG;        // this thread's first row
+    if (RBG == 4 && s.Qk == nullptr && b < m && kg + 4 <= s.n2) {
+      // one 16-byte piece per Q row (kg is a multiple of 4; rows start on 256-byte boundaries)
+      const int64_t o = static_cast<int64_t>(b) * s.ldp + kg;
+      *reinterpret_cast<f32x4*>(s.Q + o) =
+          f32x4{static_cast<float>(acc[g][0]), static_cast<float>(acc[g][1]),
+                static_cast<float>(acc[g][2]), static_cast<float>(acc[g][3])};
+      if (MOM) {
+        *reinterpret_cast<f32x4*>(s.Qw + o) =
+            f32x4{static_cast<float>(accw[g][0]), static_cast<float>(accw[g][1]),
+                  static_cast<float>(accw[g][2]), static_cast<float>(accw[g][3])};
+      }
+    } else if (b < m) {
 #pragma unroll
       for (int r = 0; r < RBG; ++r) {
         const int64_t k = k0 + rg * RBG + r;

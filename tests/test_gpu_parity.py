@@ -44,6 +44,7 @@ EXACT_CASES = [
     (300, 3, 1, 2, "fp16"),
     (1000, 40, 700, 300, "bf16"),       # G = 2
     (600, 24, 1100, 700, "fp16"),       # RB = 4, G = 4
+    (300, 1030, 700, 600, "fp16"),      # RB = 4 over 258 row blocks: XCD-grouped order, ragged
     (400, 16, 3000, 1500, "bf16"),      # RB = 2, G = 8
     (700, 8, 5000, 4096, "fp16"),       # RB = 1, G = 16, m at the limit
     (2100, 520, 1030, 48, "bf16"),      # several A/C tiles and a ragged tail
