@@ -683,7 +683,7 @@ __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t*
   const int m = s.m;
   const int stride = s.btab_stride;              // multiple of 8, at most 8 NGT kThreads
   const int t = threadIdx.x;
-  const int64_t k0 = static_cast<int64_t>(u) * RB;
+  const int64_t k0 = static_cast<int64_t>(b_block<RB>(u, s.nB)) * RB;
   int32_t* boffL = reinterpret_cast<int32_t*>(L + CW * RB + 8);   // after the zero column
   float* PL = reinterpret_cast<float*>(L);       // group partials, over the staged data
   if (t < RB) L[CW * RB + t] = 0;                // zero sentinel column (slot CW)
