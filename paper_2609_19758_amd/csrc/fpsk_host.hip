@@ -425,8 +425,8 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.wt_w = transb && n3 <= 16 * static_cast<int64_t>(m);
   const int tq = (d.TA + 3) / 4;
   d.nA = m * (d.wt_a ? tq : d.TA);
-  // the probe at m <= 64 (B as stored): 4-row B work-groups over whole 4096-column chunks
-  const bool probe4 = !mom && !transb && m <= 64;
+  // the probe at m <= 255 (B as stored): 4-row B work-groups over whole 4096-column chunks
+  const bool probe4 = !mom && !transb && m <= 255;
   if (probe4) {
     d.rb = 4, d.g = 1, d.ng = 1;
   } else if (m <= 64) {

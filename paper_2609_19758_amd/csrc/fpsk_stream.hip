@@ -665,7 +665,7 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
   if (threadIdx.x == 0) s.maxpart[s.nA + u] = bmax;
 }
 
-// B work-group of the probe at m <= 64: 4 consecutive rows of B over all columns, in chunks of
+// B work-group of the probe at m <= 255: 4 consecutive rows of B over all columns, in chunks of
 // 4096 columns (one chunk when n3 <= 4096) whose loads are all issued at once, so a work-group
 // waits for memory once per chunk.  The columns are staged column-major in LDS ([slot][4 rows],
 // 8 bytes each, signs v2(j) applied).  Thread t sums the 8 columns of the groups t, t + 256 and
