@@ -784,6 +784,12 @@ fpsketch_status pass_args(fpsketch_ctx* c, const DevRound& R, Workspace& W, cons
   s.nA = d.nA;
   s.nB = d.nB;
   s.nC = d.nC;
+  {
+    const double half_bytes = 2.0 * static_cast<double>(c->n2);
+    const double a_wg = half_bytes * static_cast<double>(c->n1) / std::max(1, d.nA);
+    const double b_wg = half_bytes * static_cast<double>(c->n3) / std::max(1, d.nB);
+    s.a_first = a_wg >= b_wg ? 1 : 0;
+  }
   s.TA = d.TA;
   s.TC = d.TC;
   s.TB = d.TB;

@@ -71,6 +71,9 @@ struct StreamArgs {
   const float* patch_val;
   // decomposition
   int nA, nB, nC;
+  // dispatch order after the C work-groups: A then B when an A work-group reads at least as many
+  // bytes as a B work-group (the smaller ones last, where they fill the tail), else B then A
+  int a_first;
   int TA, TC, TB;
   int npc, tg;
   // small buckets: row-bucket work-groups of four tiles, one per wave (A side; W side with

@@ -969,25 +969,30 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
   __shared__ uint32_t ldsu[kThreads / 64];
   // the sorted column list of the current B chunk or C tile follows the data area
   uint16_t* tabL = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(lds_dyn) + s.tab_off);
-  // Work-groups are dispatched in index order: the C work-groups (the largest) come first, then
-  // B, then A, so the short A work-groups fill the tail.
+  // Work-groups are dispatched in index order: the C work-groups (the largest) first, then A and
+  // B, the type with the smaller work-groups last, where they fill the tail in the smallest
+  // pieces.  (At 4096^3, A work-groups of about 85 KB last ran about 7 us each at the end of the
+  // pass and left the chip a third busy for its last 4 us; B last: 35.7 -> 35.3 us per call.
+  // Where B work-groups are the larger, as at 16384^3 or 2048 x 8192 x 8192, B last was 2 to
+  // 10 us slower.)
   int u = blockIdx.x;
   if (u < s.nC) {
     c_unit<MOM, G, VEC>(s, u, lds_dyn, tabL);
     return;
   }
   u -= s.nC;
-  if (u < s.nB) {
-    if (s.transb) {
-      row_unit<DT, MOM, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
-    } else if constexpr (RB == 4 && G == 1 && !MOM) {
-      b_unit_probe4<DT, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
-    } else {
-      b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
-    }
+  if (s.a_first ? u < s.nA : u >= s.nB) {
+    row_unit<DT, MOM, VEC>(s, a_side(s), s.wt_a != 0, s.a_first ? u : u - s.nB, lds_dyn, ldsu);
     return;
   }
-  row_unit<DT, MOM, VEC>(s, a_side(s), s.wt_a != 0, u - s.nB, lds_dyn, ldsu);
+  if (s.a_first) u -= s.nA;
+  if (s.transb) {
+    row_unit<DT, MOM, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
+  } else if constexpr (RB == 4 && G == 1 && !MOM) {
+    b_unit_probe4<DT, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
+  } else {
+    b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
+  }
 }
 
 // ----------------------------------------------------------------------------------------
@@ -996,12 +1001,11 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
 // before the previous one, the block products of the previous call and the stream pass of this
 // call.  The three read and write disjoint workspace sets, and each reads only what an earlier
 // launch wrote, so they need no ordering among themselves; the product and decision
-// work-groups run beside the stream's.  Grid: [decision, 7 idle, C, B, A work-groups, idle
-// up to a multiple of 8, nprod block products]: the block products start at a multiple of 8
-// so that their XCD-local slots hold, and come last so that they fill the stream pass's
-// tail.  The
-// decision uses the kernel's 256 threads over kDecideThreads virtual threads: the same bits
-// as the stand-alone decision.
+// work-groups run beside the stream's.  Grid: [decision, 7 idle, the C, A and B work-groups in
+// the stream kernel's order, idle up to a multiple of 8, nprod block products]: the block
+// products start at a multiple of 8 so that their XCD-local slots hold, and come last so that
+// they fill the stream pass's tail.  The decision uses the kernel's 256 threads over
+// kDecideThreads virtual threads: the same bits as the stand-alone decision.
 template <int DT, bool VEC, int XB>
 __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, ProductArgs prod,
                                                                  ProductArgs dec, int nprod,
@@ -1026,15 +1030,16 @@ __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, P
     return;
   }
   u -= s.nC;
-  if (u < s.nB) {
-    if (s.transb) {
-      row_unit<DT, false, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
-    } else {
-      b_unit_probe4<DT, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
-    }
+  if (s.a_first ? u < s.nA : u >= s.nB) {
+    row_unit<DT, false, VEC>(s, a_side(s), s.wt_a != 0, s.a_first ? u : u - s.nB, lds_dyn, ldsu);
     return;
   }
-  row_unit<DT, false, VEC>(s, a_side(s), s.wt_a != 0, u - s.nB, lds_dyn, ldsu);
+  if (s.a_first) u -= s.nA;
+  if (s.transb) {
+    row_unit<DT, false, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
+  } else {
+    b_unit_probe4<DT, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
+  }
 }
 
 // LDS the pipelined launch needs besides the stream pass's: the block product's reductions
