@@ -240,11 +240,13 @@ struct HostRound {
 };
 
 // Bucket segments are padded to a multiple of 8 for m <= 256 (the kernels then fold 8 list
-// entries per step); above that the lists are unpadded.
+// entries per step); above that the lists are unpadded, except the probe's B chunks up to
+// m = 512 (the 4-row B work-groups fold whole groups of 8).
 int table_pad(int m) { return m <= 256 ? 8 : 1; }
+int btab_pad(int m, bool mom) { return !mom && m <= 512 ? 8 : table_pad(m); }
 
-int64_t table_stride(int m, int64_t W) {
-  const int64_t s = W + static_cast<int64_t>(table_pad(m) - 1) * m;
+int64_t table_stride(int m, int64_t W, int pad) {
+  const int64_t s = W + static_cast<int64_t>(pad - 1) * m;
   return (s + 7) / 8 * 8;
 }
 
@@ -258,12 +260,11 @@ int64_t b_slot(int64_t cc, int64_t W) { return cc < W ? (cc & 7) * (W / 8) + (cc
 // segments padded with the sentinel W.  Entry format: 0 = offset | (v2 < 0) << 15 (C tiles),
 // 1 = offset (B chunks with moments), 2 = staged slot (B chunks of the probe).
 void build_col_tables(const std::vector<int32_t>& h2, const std::vector<int8_t>& v2, int m,
-                      int64_t W, int format, std::vector<uint16_t>& tab,
+                      int64_t W, int format, int pad, std::vector<uint16_t>& tab,
                       std::vector<int32_t>& off) {
   const int64_t n3 = static_cast<int64_t>(h2.size());
   const int64_t T = (n3 + W - 1) / W;
-  const int pad = table_pad(m);
-  const int64_t stride = table_stride(m, W);
+  const int64_t stride = table_stride(m, W, pad);
   tab.assign(static_cast<size_t>(T * stride), static_cast<uint16_t>(W));
   off.assign(static_cast<size_t>(T * (m + 1)), 0);
   std::vector<int32_t> cnt(static_cast<size_t>(m) + 1), pos(static_cast<size_t>(m));
@@ -327,8 +328,8 @@ void build_round(uint64_t seed, int round, int64_t n1, int64_t n3, int m, int64_
     R.perm[static_cast<size_t>(slot[b]) * R.cap + cnt[b]++] =
         static_cast<int32_t>(static_cast<uint32_t>(i) | (R.v1[i] < 0 ? 0x80000000u : 0u));
   }
-  build_col_tables(R.h2, R.v2, m, kColTile, 0, R.ctab, R.coff);
-  build_col_tables(R.h2, R.v2, m, cwb, mom ? 1 : 2, R.btab, R.boff);
+  build_col_tables(R.h2, R.v2, m, kColTile, 0, table_pad(m), R.ctab, R.coff);
+  build_col_tables(R.h2, R.v2, m, cwb, mom ? 1 : 2, btab_pad(m, mom), R.btab, R.boff);
   if (transb) {
     std::vector<int32_t> c2(static_cast<size_t>(m), 0);
     for (int64_t j = 0; j < n3; ++j) c2[R.h2[j]]++;
@@ -425,10 +426,11 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.wt_w = transb && n3 <= 16 * static_cast<int64_t>(m);
   const int tq = (d.TA + 3) / 4;
   d.nA = m * (d.wt_a ? tq : d.TA);
-  // the probe at m <= 255 (B as stored): 4-row B work-groups over whole 4096-column chunks
-  const bool probe4 = !mom && !transb && m <= 255;
+  // the probe at m <= 512 (B as stored): 4-row B work-groups over whole 4096-column chunks,
+  // G = 1 or 2 buckets per thread in their (and the C work-groups') per-bucket sums
+  const bool probe4 = !mom && !transb && m <= 512;
   if (probe4) {
-    d.rb = 4, d.g = 1, d.ng = 1;
+    d.rb = 4, d.g = m <= 256 ? 1 : 2, d.ng = 1;
   } else if (m <= 64) {
     d.rb = 8, d.g = 1, d.ng = 4;
   } else if (m <= 128) {
@@ -487,8 +489,8 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.NS = static_cast<int>((n2 + ksl - 1) / ksl);
   // dynamic LDS of the stream kernel: a data area (A/C combine and column sums, or the staged
   // B chunk plus its zero column), then the staged sorted column list
-  d.ctab_stride = static_cast<int>(table_stride(m, kColTile));
-  d.btab_stride = static_cast<int>(table_stride(m, d.cwb));
+  d.ctab_stride = static_cast<int>(table_stride(m, kColTile, table_pad(m)));
+  d.btab_stride = static_cast<int>(table_stride(m, d.cwb, btab_pad(m, mom)));
   const size_t comb = (mom ? 4096 : 2048) * sizeof(double);
   const size_t cs = (mom ? 1040 : 520) * sizeof(double);
   const size_t bdata = (static_cast<size_t>(d.cwb) * d.rb + d.rb) * sizeof(uint16_t);

@@ -665,21 +665,25 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
   if (threadIdx.x == 0) s.maxpart[s.nA + u] = bmax;
 }
 
-// B work-group of the probe at m <= 255: 4 consecutive rows of B over all columns, in chunks of
-// 4096 columns (one chunk when n3 <= 4096) whose loads are all issued at once, so a work-group
-// waits for memory once per chunk.  The columns are staged column-major in LDS ([slot][4 rows],
-// 8 bytes each, signs v2(j) applied).  Thread t sums the 8 columns of the groups t, t + 256 and
-// t + 512 of the chunk's bucket-sorted list (segments padded to whole groups; the list is read
-// from global memory, which keeps the work-group's LDS within four work-groups per CU) in FP32;
-// the group partials replace the staged data; thread b < m adds its bucket's partials in FP64
-// and at the end stores Q[b, k0 .. k0 + 3] with one 16-byte store.
-template <int DT, bool VEC>
+// B work-group of the probe at m <= 512: 4 consecutive rows of B over all columns, in chunks
+// of 4096 columns (one chunk when n3 <= 4096) whose loads are all issued at once, so a
+// work-group waits for memory once per chunk.  The columns are staged column-major in LDS
+// ([slot][4 rows], 8 bytes each, signs v2(j) applied).  The chunk's bucket-sorted list has its
+// segments padded to whole groups of 8 (at most 4096 + 7m entries: 3 groups per thread up to
+// m = 256, 4 up to m = 512) and is read from global memory, which keeps the work-group's LDS
+// small; thread t sums the 8 columns of its groups t, t + 256, ... in FP32, the group partials
+// replace the staged data, and thread t then adds the partials of buckets t, t + 256, ... (G of
+// them) in FP64.  At the end each bucket's Q[b, k0 .. k0 + 3] is one 16-byte store.
+template <int DT, bool VEC, int G>
 __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t* ldsu) {
   constexpr int RB = 4;
   constexpr int CW = kBChunkHalfs / RB;          // 4096 columns per chunk
   constexpr int NI = CW / 8 / kThreads;          // groups of 8 columns a thread loads
-  constexpr int NGT = 3;                         // sorted-list groups a thread folds
+  constexpr int NGT = G == 1 ? 3 : 4;            // sorted-list groups a thread folds
+  constexpr int NBO = G + 1;                     // segment starts a thread stages
   static_assert(CW == 4096 && NI == 2, "the slot format and the sentinel assume 4096 columns");
+  static_assert(8 * NGT * kThreads >= CW + 7 * 256 * G, "the padded list fits the groups");
+  static_assert(NGT * kThreads * RB * 4 <= CW * RB * 2, "the group partials fit the staging");
   const int m = s.m;
   const int stride = s.btab_stride;              // multiple of 8, at most 8 NGT kThreads
   const int t = threadIdx.x;
@@ -687,9 +691,11 @@ __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t*
   int32_t* boffL = reinterpret_cast<int32_t*>(L + CW * RB + 8);   // after the zero column
   float* PL = reinterpret_cast<float*>(L);       // group partials, over the staged data
   if (t < RB) L[CW * RB + t] = 0;                // zero sentinel column (slot CW)
-  double q[RB];
+  double q[G][RB];
 #pragma unroll
-  for (int r = 0; r < RB; ++r) q[r] = 0.0;
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int r = 0; r < RB; ++r) q[g][r] = 0.0;
   uint32_t mx = 0;
   const u32x4 sent = {0x10001000u, 0x10001000u, 0x10001000u, 0x10001000u};   // 8 x slot CW
   for (int c = 0; c < s.TB; ++c) {
@@ -719,7 +725,12 @@ __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t*
       const int o = 8 * (t + kThreads * h);
       tw[h] = o < stride ? *reinterpret_cast<const u32x4*>(btab + o) : sent;
     }
-    const int32_t bo = t <= m ? s.boff[static_cast<int64_t>(c) * (m + 1) + t] : 0;
+    int32_t bo[NBO];
+#pragma unroll
+    for (int j = 0; j < NBO; ++j) {
+      const int b = t + kThreads * j;
+      bo[j] = b <= m ? s.boff[static_cast<int64_t>(c) * (m + 1) + b] : 0;
+    }
 #pragma unroll
     for (int it = 0; it < NI; ++it) {
       const int g8 = t + kThreads * it;
@@ -736,7 +747,10 @@ __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t*
       }
       store_cols<RB>(L + static_cast<int64_t>(g8) * RB, v[it]);
     }
-    if (t <= m) boffL[t] = bo;
+#pragma unroll
+    for (int j = 0; j < NBO; ++j) {
+      if (t + kThreads * j <= m) boffL[t + kThreads * j] = bo[j];
+    }
     __syncthreads();
     float part[NGT][RB];
 #pragma unroll
@@ -763,26 +777,35 @@ __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t*
       }
     }
     __syncthreads();
-    if (t < m) {
-      const int g1 = boffL[t + 1] >> 3;
-      for (int g = boffL[t] >> 3; g < g1; ++g) {
-        const f32x4 p = *reinterpret_cast<const f32x4*>(PL + 4 * g);
 #pragma unroll
-        for (int r = 0; r < RB; ++r) q[r] += static_cast<double>(p[r]);
+    for (int g = 0; g < G; ++g) {
+      const int b = t + kThreads * g;
+      if (b < m) {
+        const int g1 = boffL[b + 1] >> 3;
+        for (int gg = boffL[b] >> 3; gg < g1; ++gg) {
+          const f32x4 p = *reinterpret_cast<const f32x4*>(PL + 4 * gg);
+#pragma unroll
+          for (int r = 0; r < RB; ++r) q[g][r] += static_cast<double>(p[r]);
+        }
       }
     }
     __syncthreads();
   }
-  if (t < m) {
-    float* qo = s.Q + static_cast<int64_t>(t) * s.ldp + k0;
-    if (k0 + RB <= s.n2) {
-      // k0 is a multiple of 4 and the rows start on 256-byte boundaries
-      *reinterpret_cast<f32x4*>(qo) = f32x4{static_cast<float>(q[0]), static_cast<float>(q[1]),
-                                            static_cast<float>(q[2]), static_cast<float>(q[3])};
-    } else {
 #pragma unroll
-      for (int r = 0; r < RB; ++r) {
-        if (k0 + r < s.n2) qo[r] = static_cast<float>(q[r]);
+  for (int g = 0; g < G; ++g) {
+    const int b = t + kThreads * g;
+    if (b < m) {
+      float* qo = s.Q + static_cast<int64_t>(b) * s.ldp + k0;
+      if (k0 + RB <= s.n2) {
+        // k0 is a multiple of 4 and the rows start on 256-byte boundaries
+        *reinterpret_cast<f32x4*>(qo) =
+            f32x4{static_cast<float>(q[g][0]), static_cast<float>(q[g][1]),
+                  static_cast<float>(q[g][2]), static_cast<float>(q[g][3])};
+      } else {
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+          if (k0 + r < s.n2) qo[r] = static_cast<float>(q[g][r]);
+        }
       }
     }
   }
@@ -988,8 +1011,8 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
   if (s.a_first) u -= s.nA;
   if (s.transb) {
     row_unit<DT, MOM, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
-  } else if constexpr (RB == 4 && G == 1 && !MOM) {
-    b_unit_probe4<DT, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
+  } else if constexpr (RB == 4 && G <= 2 && !MOM) {
+    b_unit_probe4<DT, VEC, G>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
   } else {
     b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
   }
@@ -1038,7 +1061,7 @@ __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, P
   if (s.transb) {
     row_unit<DT, false, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
   } else {
-    b_unit_probe4<DT, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
+    b_unit_probe4<DT, VEC, 1>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
   }
 }
 
@@ -1109,6 +1132,7 @@ static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, int ng, si
   FPSK_STREAM_CASE(8, 1, 1)
   FPSK_STREAM_CASE(8, 2, 1)
   FPSK_STREAM_CASE(4, 1, 1)
+  FPSK_STREAM_CASE(4, 2, 1)
   FPSK_STREAM_CASE(4, 4, 1)
   FPSK_STREAM_CASE(2, 8, 1)
   FPSK_STREAM_CASE(1, 16, 1)

@@ -43,6 +43,7 @@ EXACT_CASES = [
     (1, 8, 300, 4, "bf16"),
     (300, 3, 1, 2, "fp16"),
     (1000, 40, 700, 300, "bf16"),       # G = 2
+    (300, 520, 9000, 400, "fp16"),      # G = 2 over three B chunks, the last partial
     (600, 24, 1100, 700, "fp16"),       # RB = 4, G = 4
     (300, 1030, 700, 600, "fp16"),      # RB = 4 over 258 row blocks: XCD-grouped order, ragged
     (400, 16, 3000, 1500, "bf16"),      # RB = 2, G = 8
