@@ -421,8 +421,12 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   Decomp d;
   d.m = m;
   d.TA = static_cast<int>((n2 + kColTile - 1) / kColTile);
-  // buckets of at most about 16 rows: one wave per column tile, four tiles per work-group
-  d.wt_a = n1 <= 16 * static_cast<int64_t>(m);
+  // buckets of at most about 16 rows: one wave per column tile, four tiles per work-group; also
+  // up to 32 rows when the one-tile work-groups would number 8192 or more, each too short for
+  // its dispatch (16384^3 FP16, m = 697: 22,304 work-groups of 3.8 us; four tiles each, the
+  // pass took 470 -> 445 us; at 2048 x 8192 x 8192, m = 100, with 1600 it was 0.4 us slower)
+  d.wt_a = n1 <= 16 * static_cast<int64_t>(m) ||
+           (n1 <= 32 * static_cast<int64_t>(m) && static_cast<int64_t>(m) * d.TA >= 8192);
   d.wt_w = transb && n3 <= 16 * static_cast<int64_t>(m);
   const int tq = (d.TA + 3) / 4;
   d.nA = m * (d.wt_a ? tq : d.TA);
