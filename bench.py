@@ -222,6 +222,246 @@ def write_pmc_summary(workload: str, fetch_db: str, write_db: str) -> int:
     return 0
 
 
+def wg_timeline(args) -> int:
+    """Per-work-group timeline of the probe's stream kernel from the diagnostic build
+    (libfpsketch_timeline.so: the same kernels, each work-group stamping its start, end, XCD and
+    type).  Splits the pass by work-group type (C, A, B): counts, durations, the window each type
+    occupies, its bytes over that window and an estimate of the HBM rate over time (each
+    work-group's bytes spread evenly over its duration), against the library's plain read of
+    the same bytes on the same box.  Prints a text summary."""
+    import ctypes
+
+    import numpy as np
+    import torch
+    from paper_2609_19758_amd import fpsketch as fk
+    from paper_2609_19758_amd import workloads as wl
+
+    path = os.path.join(ROOT, "paper_2609_19758_amd", "libfpsketch_timeline.so")
+    if not os.path.exists(path):
+        print(f"bench.py: {path} is missing; build it with "
+              "python3 paper_2609_19758_amd/csrc/build.py --timeline", file=sys.stderr)
+        return 1
+    fk.LIB_PATH = path
+    lib = fk.load()
+    for name in ("fpsketch_wg_timeline", "fpsketch_wg_timeline_tail"):
+        getattr(lib, name).restype = ctypes.c_int
+        getattr(lib, name).argtypes = [ctypes.c_void_p, ctypes.c_int64]
+
+    w = wl.workload(args.workload)
+    torch.cuda.set_device(0)
+    sets = []
+    for s in range(args.sets):
+        a_bits, b_bits = wl.gen_operands(w.n1, w.n2, w.n3, w.fmt, w.dist_a, w.dist_b,
+                                         seed=100 + s, seed_b=200 + s)
+        A, B = upload_half(a_bits, w.fmt), upload_half(b_bits, w.fmt)
+        sets.append((A, B, gemm_f32(A, B)))
+    v = fk.Verifier(w.n1, w.n2, w.n3, w.fmt, m=w.m_forced, rho_min=w.rho_min,
+                    s_budget=w.s_budget)
+    for k in range(w.calib_calls):
+        v.probe(*sets[k % args.sets])
+    torch.cuda.synchronize()
+    m0 = v.m
+    v.calibrate_noise(sets[0][2])
+    for k in range(args.warmup):
+        v.probe(*sets[k % args.sets])
+    torch.cuda.synchronize()
+
+    total = {0: w.n1 * w.n3 * 4, 1: w.n1 * w.n2 * 2, 2: w.n2 * w.n3 * 2}
+    buf = np.zeros((1 << 16, 4), dtype=np.uint64)
+    tbuf = np.zeros((4097, 4), dtype=np.uint64)      # block products, then the decision
+    calls, tails = [], []
+    for k in range(args.steps):
+        v.probe(*sets[k % args.sets])
+        torch.cuda.synchronize()
+        if (lib.fpsketch_wg_timeline(buf.ctypes.data, buf.shape[0]) != 0
+                or lib.fpsketch_wg_timeline_tail(tbuf.ctypes.data, tbuf.shape[0] - 1) != 0):
+            print("bench.py: reading the work-group timeline failed", file=sys.stderr)
+            return 1
+        grid = int(buf[0, 3] >> np.uint64(8))
+        calls.append(buf[:grid].copy())
+        pgrid = min(int(tbuf[0, 3] >> np.uint64(8)), tbuf.shape[0] - 1)
+        tails.append((tbuf[:pgrid].copy(), tbuf[-1].copy()))
+    # the plain read of the call's bytes on the same box
+    # (four buffers in turn, 4x the 256 MB Infinity Cache at 4096^3, as the probe's buffer sets)
+    nbytes = sum(total.values())
+    rbufs = [torch.empty(nbytes // 4, dtype=torch.float32, device="cuda") for _ in range(4)]
+    rout = torch.zeros(1, dtype=torch.int32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for k in range(4):
+        fk.stream_read(rbufs[k], nbytes, rout, 2048)
+    e0.record()
+    for k in range(20):
+        fk.stream_read(rbufs[k % 4], nbytes, rout, 2048)
+    e1.record()
+    torch.cuda.synchronize()
+    read_gbs = nbytes * 20 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+    head = [f"workload {w.name}: {w.n1}x{w.n2}x{w.n3} {w.fmt}, m {m0} -> {v.m}; "
+            f"{len(calls)} traced probe calls over {args.sets} buffer sets",
+            f"stream kernel work-groups: {len(calls[0])}; bytes of A, B, C: {nbytes}",
+            f"plain read of the same {nbytes} bytes (library read kernel, 2048 work-groups, "
+            f"4 buffers in turn, same box): {read_gbs:.0f} GB/s = {nbytes / read_gbs / 1e3:.2f} us"]
+    lines = timeline_summary(calls, total, head)
+    lines += tail_summary(calls, tails)
+    print("\n".join(lines))
+    return 0
+
+
+def tail_summary(calls, tails) -> list:
+    """The block products and the decision after each traced stream launch (m <= 64), on the
+    same clock: when the stream kernel's last work-group ends, when the first block product
+    starts (per XCD too), when the last ends, and the decision's start and end.  Calls whose
+    tail records predate their stream launch (the matrix-core path at m > 64 leaves none)
+    are skipped."""
+    import numpy as np
+
+    tick_us = 0.01
+    rows = []
+    for r, (p, d) in zip(calls, tails):
+        base = int(r[:, 0].astype(np.int64).min())
+        s_end = (int(r[:, 1].astype(np.int64).max()) - base) * tick_us
+        if len(p) == 0 or int(p[:, 0].astype(np.int64).min()) < base or int(d[0]) < base:
+            continue
+        ps = (p[:, 0].astype(np.int64) - base) * tick_us
+        pe = (p[:, 1].astype(np.int64) - base) * tick_us
+        px = ((p[:, 2] >> np.uint64(32)) & np.uint64(15)).astype(np.int64)
+        ds, de = (int(d[0]) - base) * tick_us, (int(d[1]) - base) * tick_us
+        xs = [float(ps[px == x].min()) - s_end if (px == x).any() else float("nan")
+              for x in range(8)]
+        rows.append({"stream_end": s_end, "prod_first": float(ps.min()) - s_end,
+                     "prod_last_start": float(ps.max()) - s_end,
+                     "prod_last_end": float(pe.max()) - s_end,
+                     "prod_dur": float(np.median(pe - ps)),
+                     "dec_start": ds - s_end, "dec_end": de - s_end, "xcd": xs,
+                     "n": len(p)})
+    if not rows:
+        return []
+    med = {k: float(np.median([q[k] for q in rows])) for k in rows[0] if k != "xcd"}
+    xs = np.array([q["xcd"] for q in rows])
+    xmed = [float(np.median(c[np.isfinite(c)])) if np.isfinite(c).any() else float("nan")
+            for c in xs.T]
+    return [
+        "",
+        f"after the stream kernel (block path, {len(rows)} calls; us from the stream kernel's "
+        "last work-group end, medians):",
+        f"  block products ({int(med['n'])} work-groups): first start {med['prod_first']:.2f}, "
+        f"last start {med['prod_last_start']:.2f}, last end {med['prod_last_end']:.2f}; "
+        f"work-group duration {med['prod_dur']:.2f}",
+        "  first block-product start per XCD: " + "  ".join(
+            f"XCD{x} {xmed[x]:.2f}" for x in range(8) if np.isfinite(xmed[x])),
+        f"  decision: start {med['dec_start']:.2f}, end {med['dec_end']:.2f} "
+        f"(duration {med['dec_end'] - med['dec_start']:.2f}); stream kernel first start to "
+        f"decision end {med['stream_end'] + med['dec_end']:.2f}",
+    ]
+
+
+def timeline_summary(calls, total: dict, head: list) -> list:
+    """Text summary of per-work-group stream-kernel records (one (grid, 4) uint64 array per call:
+    start and end on the 100 MHz clock, XCD and hardware id, launch size and type; type bytes in
+    `total`, keyed 0: C, 1: A, 2: B), after the lines in `head`."""
+    import numpy as np
+
+    tick_us = 0.01                          # the constant clock runs at 100 MHz
+    names = {0: "C", 1: "A", 2: "B"}
+
+    def analyse(r):
+        t0 = r[:, 0].astype(np.int64)
+        t1 = r[:, 1].astype(np.int64)
+        base = t0.min()
+        s = (t0 - base) * tick_us
+        e = (t1 - base) * tick_us
+        typ = (r[:, 3] & np.uint64(0xff)).astype(np.int64)
+        xcd = ((r[:, 2] >> np.uint64(32)) & np.uint64(15)).astype(np.int64)
+        hw = (r[:, 2] & np.uint64(0xffffffff)).astype(np.int64)
+        out = {"span": float(e.max()), "types": {}, "s": s, "e": e, "typ": typ, "xcd": xcd,
+               "hw": hw}
+        for ty in (0, 1, 2):
+            sel = typ == ty
+            n = int(sel.sum())
+            if n == 0:
+                continue
+            d = e[sel] - s[sel]
+            win = float(e[sel].max() - s[sel].min())
+            out["types"][ty] = {
+                "n": n, "kb": total[ty] / n / 1024.0, "dur_mean": float(d.mean()),
+                "dur_p50": float(np.median(d)), "dur_p90": float(np.percentile(d, 90)),
+                "first": float(s[sel].min()), "last_start": float(s[sel].max()),
+                "last_end": float(e[sel].max()), "win_gbs": total[ty] / (win * 1e-6) / 1e9,
+                "wg_gbs": total[ty] / n / (float(d.mean()) * 1e-6) / 1e9}
+        return out
+
+    res = [analyse(r) for r in calls]
+    spans = np.array([x["span"] for x in res])
+    med = res[int(np.argsort(spans)[len(spans) // 2])]
+    nbytes = sum(total.values())
+    lines = list(head)
+    lines.append(f"first start to last end, median over calls: {np.median(spans):.2f} us "
+                 f"(min {spans.min():.2f}, max {spans.max():.2f}) = "
+                 f"{nbytes / (np.median(spans) * 1e-6) / 1e9:.0f} GB/s")
+    lines.append("")
+    lines.append("per type, medians over calls (window: first start to last end of the type; "
+                 "window GB/s: the type's bytes over its window;")
+    lines.append("work-group GB/s: mean bytes over mean duration of one work-group)")
+    lines.append(f"{'type':>4} {'WGs':>6} {'KB/WG':>7} {'dur mean':>9} {'dur p50':>8} "
+                 f"{'dur p90':>8} {'first':>7} {'last st':>8} {'last end':>9} "
+                 f"{'window GB/s':>12} {'WG GB/s':>8}")
+    for ty in (0, 1, 2):
+        rows = [x["types"][ty] for x in res if ty in x["types"]]
+        if not rows:
+            continue
+        mdn = {k: float(np.median([q[k] for q in rows])) for k in rows[0]}
+        lines.append(f"{names[ty]:>4} {int(mdn['n']):>6} {mdn['kb']:>7.1f} "
+                     f"{mdn['dur_mean']:>9.2f} {mdn['dur_p50']:>8.2f} {mdn['dur_p90']:>8.2f} "
+                     f"{mdn['first']:>7.2f} {mdn['last_start']:>8.2f} {mdn['last_end']:>9.2f} "
+                     f"{mdn['win_gbs']:>12.0f} {mdn['wg_gbs']:>8.1f}")
+    lines.append("")
+    step = 1.0 if med["span"] < 60 else float(round(med["span"] / 40))
+    lines.append(f"median call ({med['span']:.2f} us) in {step:.0f} us steps: work-groups "
+                 "active by type "
+                 "(time-weighted) and the estimated rate (each work-group's bytes spread over "
+                 "its duration)")
+    lines.append(f"{'t us':>5} {'C':>6} {'A':>6} {'B':>6} {'GB/s':>6}")
+    s, e, typ = med["s"], med["e"], med["typ"]
+    kb = np.array([total[ty] / max(1, int((typ == ty).sum())) for ty in (0, 1, 2)])
+    rate = kb[typ] / np.maximum(e - s, 1e-3)          # bytes per us
+    for b0 in np.arange(0.0, med["span"], step):
+        ov = np.clip(np.minimum(e, b0 + step) - np.maximum(s, b0), 0.0, None)
+        act = [float(ov[typ == ty].sum()) / step for ty in (0, 1, 2)]
+        gbs = float((ov * rate).sum()) / step / 1e3
+        lines.append(f"{b0:>5.0f} {act[0]:>6.1f} {act[1]:>6.1f} {act[2]:>6.1f} {gbs:>6.0f}")
+    lines.append("")
+    lines.append("median call per XCD: work-groups, first start, 90th-percentile start of the "
+                 "first 128 (its first resident round), last end (us)")
+    xcd = med["xcd"]
+    for x in range(8):
+        sel = xcd == x
+        if not sel.any():
+            continue
+        st = np.sort(s[sel])
+        k = min(len(st), 128)
+        lines.append(f"  XCD{x}: {int(sel.sum()):>5} {st[0]:>8.2f} {st[int(0.9 * (k - 1))]:>8.2f} "
+                     f"{float(e[sel].max()):>8.2f}")
+    # refill gap: a work-group starting after the first end on its CU waited since the latest
+    # end on that CU before its start (the slot it takes was free that long at most)
+    cu = (xcd << 8) | ((med["hw"] >> 8) & 0x7f)
+    gaps = []
+    for c in np.unique(cu):
+        sel = cu == c
+        cs, ce = s[sel], e[sel]
+        ends = np.sort(ce)
+        for st in cs:
+            j = np.searchsorted(ends, st, side="right")
+            if j > 0:
+                gaps.append(st - ends[j - 1])
+    if gaps:
+        g = np.array(gaps)
+        lines.append(f"refill gap (start minus the latest end on the same CU before it), median "
+                     f"call: {len(g)} work-groups, median {np.median(g):.2f} us, p90 "
+                     f"{np.percentile(g, 90):.2f}, mean {g.mean():.2f}; CUs used: "
+                     f"{len(np.unique(cu))}")
+    return lines
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -242,7 +482,13 @@ def main() -> int:
                     help="write the HBM traffic summary of the probe's stream kernel from two "
                          "rocprofv3 --pmc databases (FETCH_SIZE, WRITE_SIZE) of a run with "
                          "--copy-calibration, and exit")
+    ap.add_argument("--wg-timeline", action="store_true",
+                    help="print the per-work-group timeline of the probe's stream kernel from "
+                         "the diagnostic build (libfpsketch_timeline.so) and exit; --steps "
+                         "traced calls after --warmup")
     args = ap.parse_args()
+    if args.wg_timeline:
+        return wg_timeline(args)
     if args.summarize:
         return summarize_db(args.summarize)
     if args.write_pmc_summary:

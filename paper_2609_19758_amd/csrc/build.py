@@ -10,6 +10,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 OUT = os.path.join(PKG, "libfpsketch.so")
+# Diagnostic build: the same kernels with the stream pass's per-work-group timeline recorded
+# (bench.py --wg-timeline reads it).  The binding never loads it for the probe path.
+OUT_TIMELINE = os.path.join(PKG, "libfpsketch_timeline.so")
 SOURCES = ["fpsk_stream.hip", "fpsk_kernels.hip", "fpsk_host.hip"]
 
 # gfx950 only; packed FP32 instructions disabled (hipcc forms them from plain float code).
@@ -29,9 +32,11 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    tmp = OUT + ".tmp"
-    cmd = [hipcc(), *FLAGS, "-o", tmp, *[os.path.join(HERE, s) for s in SOURCES]]
+def build(verbose: bool = False, timeline: bool = False) -> str:
+    out = OUT_TIMELINE if timeline else OUT
+    tmp = out + ".tmp"
+    extra = ["-DFPSK_WG_TIMELINE"] if timeline else []
+    cmd = [hipcc(), *FLAGS, *extra, "-o", tmp, *[os.path.join(HERE, s) for s in SOURCES]]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -40,9 +45,9 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed with status {res.returncode}")
     if verbose and res.stderr.strip():
         sys.stderr.write(res.stderr)
-    os.replace(tmp, OUT)
-    return OUT
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, timeline="--timeline" in sys.argv[1:]))

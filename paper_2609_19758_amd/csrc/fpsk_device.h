@@ -150,4 +150,36 @@ static void launch_k(K kernel, dim3 grid, dim3 block, size_t shmem, hipStream_t 
   }
 }
 
+// ----------------------------------------------------------------------------------------
+// Work-group timeline, compiled only with FPSK_WG_TIMELINE (a diagnostic build of the library;
+// the build the binding loads has none of it).  A work-group that holds a WgStamp leaves one
+// record of four words at slot `slot` of `base`: its start and end on the 100 MHz constant
+// clock, the XCD and the hardware-id word of the CU it ran on, and the launch's work-group
+// count with the work-group's type.  Thread 0 stamps the end after the kernel's last block
+// reduction, so the record spans the whole work-group.  Each launch overwrites the records of
+// the one before.
+#ifdef FPSK_WG_TIMELINE
+constexpr int kTimelineMax = 1 << 16;
+
+struct WgStamp {
+  unsigned long long* rec;
+  unsigned long long t0;
+  int type;
+  __device__ WgStamp(unsigned long long* base, unsigned slot, int ty)
+      : rec(slot < static_cast<unsigned>(kTimelineMax) ? base + 4 * slot : nullptr),
+        t0(__builtin_amdgcn_s_memrealtime()), type(ty) {}
+  __device__ ~WgStamp() {
+    if (threadIdx.x == 0 && rec != nullptr) {
+      const unsigned long long t1 = __builtin_amdgcn_s_memrealtime();
+      const unsigned hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);     // HW_ID, 32 bits
+      const unsigned xcc = __builtin_amdgcn_s_getreg((15 << 11) | 20);   // XCC_ID, 16 bits
+      rec[0] = t0;
+      rec[1] = t1;
+      rec[2] = (static_cast<unsigned long long>(xcc & 15u) << 32) | hw;
+      rec[3] = (static_cast<unsigned long long>(gridDim.x) << 8) | static_cast<unsigned>(type);
+    }
+  }
+};
+#endif
+
 }  // namespace fpsk

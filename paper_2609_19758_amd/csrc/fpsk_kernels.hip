@@ -16,15 +16,25 @@ namespace fpsk {
 
 // ----------------------------------------------------------------------------------------
 // Probe product for m <= 64 (bodies in fpsk_block.h): the block products, then one deciding
-// work-group of kDecideThreads.
+// work-group of kDecideThreads.  The diagnostic timeline build records the block products at
+// their launch indices (type 3) and the decision in the last slot (type 4).
+
+#ifdef FPSK_WG_TIMELINE
+static __device__ unsigned long long wg_timeline_tail[4 * kTimelineMax];
+#define FPSK_TAIL_STAMP(slot, type) const WgStamp wg_stamp_(wg_timeline_tail, slot, type)
+#else
+#define FPSK_TAIL_STAMP(slot, type)
+#endif
 
 template <int XB>
 __global__ __launch_bounds__(kThreads) void block_product_kernel(ProductArgs pa) {
+  FPSK_TAIL_STAMP(blockIdx.x, 3);
   __shared__ double red[lds_reduce_doubles<kThreads, XB * XB>()];
   block_product_body<XB, (XB <= 3 ? 4 : 2), XB * XB>(pa, blockIdx.x, gridDim.x, red);
 }
 
 __global__ __launch_bounds__(kDecideThreads) void block_decide_kernel(ProductArgs pa) {
+  FPSK_TAIL_STAMP(kTimelineMax - 1, 4);
   __shared__ double red[lds_reduce_doubles<kDecideThreads, 5>()];
   block_decide_body<kDecideThreads, 4>(pa, red);
 }
@@ -1009,3 +1019,22 @@ hipError_t launch_copy(const void* src, void* dst, int64_t bytes, int grid, hipS
 }
 
 }  // namespace fpsk
+
+#ifdef FPSK_WG_TIMELINE
+// Copies the records of the last block-product launch (its first max_records slots) and of the
+// last decision (the final slot) to host memory, out[0 .. 4 max_records) and
+// out[4 max_records .. + 4); synchronous.  Returns 0, or -1 on a bad argument or a failed copy.
+// Exported by the diagnostic build only.
+extern "C" int fpsketch_wg_timeline_tail(unsigned long long* out, int64_t max_records) {
+  if (out == nullptr || max_records < 1) return -1;
+  const int64_t n = max_records < fpsk::kTimelineMax - 1 ? max_records : fpsk::kTimelineMax - 1;
+  const size_t rec = 4 * sizeof(unsigned long long);
+  if (hipMemcpyFromSymbol(out, HIP_SYMBOL(fpsk::wg_timeline_tail), static_cast<size_t>(n) * rec,
+                          0, hipMemcpyDeviceToHost) != hipSuccess) {
+    return -1;
+  }
+  return hipMemcpyFromSymbol(out + 4 * max_records, HIP_SYMBOL(fpsk::wg_timeline_tail), rec,
+                             static_cast<size_t>(fpsk::kTimelineMax - 1) * rec,
+                             hipMemcpyDeviceToHost) == hipSuccess ? 0 : -1;
+}
+#endif

@@ -9,6 +9,15 @@
 
 namespace fpsk {
 
+// Work-group timeline of the stream kernel (diagnostic build only; the stamp is in
+// fpsk_device.h): one record per work-group of the last stream launch, at its launch index.
+#ifdef FPSK_WG_TIMELINE
+static __device__ unsigned long long wg_timeline_stream[4 * kTimelineMax];
+#define FPSK_WG_STAMP(type) const WgStamp wg_stamp_(wg_timeline_stream, blockIdx.x, type)
+#else
+#define FPSK_WG_STAMP(type)
+#endif
+
 // ----------------------------------------------------------------------------------------
 // Row-bucket passes (A and C work-groups).  Wave w of a work-group takes rows w, w + 4, ... of
 // the bucket's sorted row list.  The row entries of up to 64 of its rows arrive with one vector
@@ -1000,15 +1009,18 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
   // 10 us slower.)
   int u = blockIdx.x;
   if (u < s.nC) {
+    FPSK_WG_STAMP(0);
     c_unit<MOM, G, VEC>(s, u, lds_dyn, tabL);
     return;
   }
   u -= s.nC;
   if (s.a_first ? u < s.nA : u >= s.nB) {
+    FPSK_WG_STAMP(1);
     row_unit<DT, MOM, VEC>(s, a_side(s), s.wt_a != 0, s.a_first ? u : u - s.nB, lds_dyn, ldsu);
     return;
   }
   if (s.a_first) u -= s.nA;
+  FPSK_WG_STAMP(2);
   if (s.transb) {
     row_unit<DT, MOM, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
   } else if constexpr (RB == 4 && G <= 2 && !MOM) {
@@ -1151,3 +1163,17 @@ hipError_t launch_stream(const StreamArgs& s, int dt, bool moments, int rb, int 
 }
 
 }  // namespace fpsk
+
+#ifdef FPSK_WG_TIMELINE
+// Copies the first max_records work-group records of the last stream launch (four 64-bit words
+// each, as WgStamp writes them) to host memory; synchronous.  Returns 0, or -1 on a bad
+// argument or a failed copy.  Exported by the diagnostic build only.
+extern "C" int fpsketch_wg_timeline(unsigned long long* out, int64_t max_records) {
+  if (out == nullptr || max_records < 1) return -1;
+  const int64_t n = max_records < fpsk::kTimelineMax ? max_records : fpsk::kTimelineMax;
+  const hipError_t e = hipMemcpyFromSymbol(out, HIP_SYMBOL(fpsk::wg_timeline_stream),
+                                           static_cast<size_t>(n) * 4 * sizeof(unsigned long long),
+                                           0, hipMemcpyDeviceToHost);
+  return e == hipSuccess ? 0 : -1;
+}
+#endif
