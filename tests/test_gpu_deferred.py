@@ -2,7 +2,8 @@
 previous call's block products and the decision of the call before run in one launch.  Every
 call's verdict, the statistics and the running noise sum equal those of the same sequence of
 ordinary probes bit for bit; other calls on the context flush first; shapes off the block path
-run ordinary probes."""
+run ordinary probes.  The verdicts and the last call's statistics are also checked against the
+oracle's probe."""
 import numpy as np
 import pytest
 
@@ -22,19 +23,23 @@ def fk():
     return fpsketch
 
 
-def _sequence(n1, n2, n3, fmt, calls, seed):
-    """(A_k, B, C_k, dirty_k): one weight, fresh activations, every third product faulted."""
+def _sequence(n1, n2, n3, fmt, calls, seed, bits=None):
+    """(A_k, B, C_k, dirty_k): one weight, fresh activations, every third product faulted.  With
+    a list `bits`, the operands' bits (a_k, b) are appended to it per call."""
     import torch
     b_bits = wl.gen_side(n2, n3, fmt, ("normal", 0.02), seed, 0xB)
     B = to_dev_half(b_bits, fmt)
     out = []
     for k in range(calls):
-        A = to_dev_half(wl.gen_side(n1, n2, fmt, ("normal", 1.0), seed + 1 + k, 0xA), fmt)
+        a_bits = wl.gen_side(n1, n2, fmt, ("normal", 1.0), seed + 1 + k, 0xA)
+        A = to_dev_half(a_bits, fmt)
         C = gemm_f32(A, B)
         dirty = k % 3 == 1
         if dirty:
             C[(7 * k) % n1, (11 * k) % n3] += 0.5 * float(C.abs().mean().item())
         out.append((A, B, C, dirty))
+        if bits is not None:
+            bits.append((a_bits, b_bits))
     torch.cuda.synchronize()
     return out
 
@@ -48,7 +53,8 @@ def _sequence(n1, n2, n3, fmt, calls, seed):
 ])
 def test_deferred_equals_ordinary(fk, n1, n2, n3, m, fmt):
     import torch
-    seq = _sequence(n1, n2, n3, fmt, 7, 61)
+    bits = []
+    seq = _sequence(n1, n2, n3, fmt, 7, 61, bits)
     vd = fk.Verifier(n1, n2, n3, fmt, m=m)
     vs = fk.Verifier(n1, n2, n3, fmt, m=m)
     fd = [torch.zeros(1, dtype=torch.int32, device="cuda") for _ in seq]
@@ -63,6 +69,18 @@ def test_deferred_equals_ordinary(fk, n1, n2, n3, m, fmt):
     for k, (_, _, _, dirty) in enumerate(seq):
         assert int(fd[k].item()) == int(fs[k].item()) == int(dirty), k
     assert vd.probe_stats() == stats[-1]
+    # the deferred verdicts and the last call's statistics against the oracle's probe (the same
+    # hash round, the definition of S in FP64; its noise estimate within 5 %, as for the
+    # ordinary probe: the FP32 factors round differently from the FP64 definition)
+    hr = o.make_round(vd.params.seed, 0, n1, n3, m)
+    p = o.Params()
+    b64 = o.decode(bits[0][1], fmt)
+    for k in (0, 1, len(seq) - 1):
+        ref = o.probe(o.decode(bits[k][0], fmt), b64, seq[k][2].cpu().numpy(), hr, p)
+        assert ref.dirty == bool(int(fd[k].item())), k
+    st = vd.probe_stats()
+    assert abs(st["tau"] / ref.tau - 1) < 1e-12
+    assert abs(st["sigma_hat"] / ref.sigma_hat - 1) < 0.05
     # the running noise sums agree: the same calibration outcome
     assert vd.calibrate_noise(seq[0][2]) == vs.calibrate_noise(seq[0][2])
     vd.close()
