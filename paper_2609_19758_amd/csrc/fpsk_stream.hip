@@ -990,6 +990,120 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
   }
 }
 
+// C work-group with one column tile per wave (probe, 256 < m <= 1024, whose tile lists hold 512
+// entries): wave w sums all of bucket a's rows over tile tq + w, four tiles at a time, so no
+// partial sums cross waves.  The four tiles' column sums and lists go to LDS; thread b then folds
+// bucket b over the four tiles in tile order (the same order as the one-tile form; the column
+// sums add each tile's rows in one wave's order instead of four waves' interleaved order).
+// Two barriers per four tiles instead of three per tile.
+template <int G, bool VEC>
+__device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tabL) {
+  constexpr int U = 8;
+  const int m = s.m;
+  const int a = u / s.npc, gi = u - a * s.npc;
+  const int t0 = gi * s.tg;
+  const int t1 = (t0 + s.tg < s.TC) ? t0 + s.tg : s.TC;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int32_t* prow = s.perm + static_cast<int64_t>(a) * s.cap;
+  const bool patched = s.patch_rowptr != nullptr;
+  double* cs = lds;                    // [4][520]: the four tiles' column sums and sentinels
+  double fS[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) fS[g] = 0.0;
+  for (int tq = t0; tq < t1; tq += 4) {
+    const int t = tq + w;
+    const bool tok = t < t1;
+    const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
+    const bool lane_ok = tok && col < s.n3;
+    // this wave's tile list (512 entries, 8 per lane), loaded with the first rows
+    const u32x4 tv = tok ? *reinterpret_cast<const u32x4*>(s.ctab + static_cast<int64_t>(t) * 512 +
+                                                           lane * 8)
+                         : u32x4{0u, 0u, 0u, 0u};
+    double acc[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = 0.0;
+    if (tok) {
+      for (int base = 0; base < s.cap; base += 64) {
+        const int32_t pe = base + lane < s.cap ? prow[base + lane] : -1;
+        const int nr = __popcll(__ballot(pe != -1));
+        if (nr == 0) break;
+        for (int r0 = 0; r0 < nr; r0 += U) {
+          f32x4 v0[U], v1[U];
+          double sg[U];
+          int64_t rows[U];
+#pragma unroll
+          for (int q = 0; q < U; ++q) {
+            const bool ok = r0 + q < nr;
+            const int32_t e = row_entry(pe, ok ? r0 + q : 0);
+            const int64_t row = e & 0x7fffffff;
+            rows[q] = row;
+            sg[q] = ok ? (e < 0 ? -1.0 : 1.0) : 0.0;
+            if (VEC) {
+              load8f_sel(s.C + row * s.n3 + col, ok && lane_ok, s.zero, v0[q], v1[q]);
+            } else if (ok && lane_ok) {
+              load8f(s.C + row * s.n3, col, s.n3, false, v0[q], v1[q]);
+            } else {
+              v0[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+              v1[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+          }
+          if (patched) {
+#pragma unroll
+            for (int q = 0; q < U; ++q) {
+              if (r0 + q < nr && lane_ok) apply_patches(s, rows[q], col, v0[q], v1[q]);
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < U; ++q) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const double x = static_cast<double>(e < 4 ? v0[q][e] : v1[q][e - 4]);
+              acc[e] = fma(x, sg[q], acc[e]);
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cs[w * 520 + lane * 8 + e] = acc[e];
+    if (lane == 0) cs[w * 520 + kColTile] = 0.0;
+    *reinterpret_cast<u32x4*>(tabL + w * 512 + lane * 8) = tv;
+    // segment starts of this thread's buckets in the four tiles, all loads issued at once
+    int qb[G][4], qe[G][4];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int b = threadIdx.x + kThreads * g;
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti) {
+        const bool ok = b < m && tq + ti < t1;
+        const int32_t* co =
+            s.coff + static_cast<int64_t>(ok ? tq + ti : 0) * (m + 1) + (ok ? b : 0);
+        qb[g][ti] = ok ? co[0] : 0;
+        qe[g][ti] = ok ? co[1] : 0;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti) {
+        for (int q = qb[g][ti]; q < qe[g][ti]; ++q) {
+          const uint32_t ez = tabL[ti * 512 + q];
+          const int cc = ez & 0x7fff;
+          const double sgd = (ez & 0x8000u) ? -1.0 : 1.0;
+          fS[g] += sgd * cs[ti * 520 + cc];
+        }
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int b = threadIdx.x + kThreads * g;
+    if (b < m) s.partS[(static_cast<int64_t>(gi) * m + a) * m + b] = fS[g];
+  }
+}
+
 // LDS layout of the stream kernel (dynamic): the A/C combine area or the staged B chunk first,
 // then the sorted column list of the current B chunk or C tile.  The longer lists of B chunks
 // with fewer rows hold the probe to 3 (2 or 4 rows) or 2 (1 row) work-groups per CU, so those
@@ -1010,6 +1124,12 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
   int u = blockIdx.x;
   if (u < s.nC) {
     FPSK_WG_STAMP(0);
+    if constexpr (!MOM && G >= 2 && G <= 4) {
+      if (s.wt_c) {
+        c_unit_wt<G, VEC>(s, u, lds_dyn, tabL);
+        return;
+      }
+    }
     c_unit<MOM, G, VEC>(s, u, lds_dyn, tabL);
     return;
   }

@@ -46,6 +46,8 @@ EXACT_CASES = [
     (300, 520, 9000, 400, "fp16"),      # G = 2 over three B chunks, the last partial
     (600, 24, 1100, 700, "fp16"),       # RB = 4, G = 4
     (300, 1030, 700, 600, "fp16"),      # RB = 4 over 258 row blocks: XCD-grouped order, ragged
+    (300, 24, 6145, 300, "bf16"),       # C tiles one per wave, element loads, last group 1 tile
+    (2000, 8, 7000, 1000, "fp16"),      # C tiles one per wave, G = 4, 7 tiles per group
     (400, 16, 3000, 1500, "bf16"),      # RB = 2, G = 8
     (700, 8, 5000, 4096, "fp16"),       # RB = 1, G = 16, m at the limit
     (2100, 520, 1030, 48, "bf16"),      # several A/C tiles and a ragged tail
