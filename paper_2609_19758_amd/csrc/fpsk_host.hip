@@ -410,7 +410,7 @@ struct Decomp {
   int xsr = 1, xsc = 1, xnstc = 1, xslots = 0;   // supertiles of blocks (XCD-local sets)
   // B work-groups of 1 or 2 rows write Q k-major (n2 x m), then a transpose forms Q
   bool qk = false;
-  bool wt_c = false;                  // probe C work-groups of one tile per wave
+  bool wt_c = false;                  // C work-groups of one tile per wave
   bool wt_a = false, wt_w = false;   // row-bucket work-groups of four tiles (small buckets)
 };
 
@@ -463,12 +463,12 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   d.tg = (d.TC + npc - 1) / npc;
   d.npc = (d.TC + d.tg - 1) / d.tg;
   d.nC = m * d.npc;
-  // Probe C work-groups with one tile per wave where buckets hold few rows: the four waves of
+  // C work-groups with one tile per wave where buckets hold few rows: the four waves of
   // the one-tile form each hold a handful of rows per tile and meet at three barriers per
   // tile (16384^3 FP16, m = 698: stream pass 445.8 -> 426.7 us; 2048 x 4096 x 12288 at
   // m = 400: 82.5 -> 59.2 us).  The 512-entry tile lists of m > 256 let one 16-byte load per
   // thread stage all four; m <= 1024 keeps the fold's segment starts (8 G) in registers.
-  d.wt_c = !mom && m > 256 && m <= 1024 && n1 <= 32 * static_cast<int64_t>(m) && d.tg >= 4;
+  d.wt_c = m > 256 && m <= 1024 && n1 <= 32 * static_cast<int64_t>(m) && d.tg >= 4;
   // Bucket-space product on the matrix cores, tiles of ts x ts outputs over NS k-slices.
   // Without moments: 16 x 16 tiles whose k-range the 4 waves split, while there are fewer than
   // 256 of them (slices for about 2048 waves); else 64 x 64 tiles of four 32 x 32 wave quadrants.
@@ -505,7 +505,7 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   const size_t comb = (mom ? 4096 : 2048) * sizeof(double);
   const size_t cs = (mom ? 1040 : 520) * sizeof(double);
   const size_t bdata = (static_cast<size_t>(d.cwb) * d.rb + d.rb) * sizeof(uint16_t);
-  const size_t wtc = d.wt_c ? 4 * 520 * sizeof(double) : 0;   // four tiles' column sums
+  const size_t wtc = d.wt_c ? (mom ? 8 : 4) * 520 * sizeof(double) : 0;   // 4 tiles' column sums
   const size_t data = (std::max({comb + cs, bdata, wtc}) + 15) / 16 * 16;
   d.tab_off = static_cast<int>(data);
   // (the probe's B group fold, 8-row work-groups up to m = 256, stages the m + 1 segment

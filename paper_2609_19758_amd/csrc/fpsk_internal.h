@@ -79,7 +79,7 @@ struct StreamArgs {
   // small buckets: row-bucket work-groups of four tiles, one per wave (A side; W side with
   // transb), m x ceil(TA / 4) of them
   int wt_a, wt_w;
-  // probe C work-groups with one column tile per wave, four tiles at a time (256 < m <= 1024,
+  // C work-groups with one column tile per wave, four tiles at a time (256 < m <= 1024,
   // buckets of at most 32 rows, at least 4 tiles per work-group)
   int wt_c;
   double inv_l1, inv_l3;      // 1 / 2^ceil(log2 n1), 1 / 2^ceil(log2 n3)

@@ -990,13 +990,14 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
   }
 }
 
-// C work-group with one column tile per wave (probe, 256 < m <= 1024, whose tile lists hold 512
-// entries): wave w sums all of bucket a's rows over tile tq + w, four tiles at a time, so no
-// partial sums cross waves.  The four tiles' column sums and lists go to LDS; thread b then folds
-// bucket b over the four tiles in tile order (the same order as the one-tile form; the column
-// sums add each tile's rows in one wave's order instead of four waves' interleaved order).
-// Two barriers per four tiles instead of three per tile.
-template <int G, bool VEC>
+// C work-group with one column tile per wave (256 < m <= 1024, whose tile lists hold 512
+// entries): wave w sums all of bucket a's rows over tile tq + w (and, with moments, the
+// row-weighted sums), four tiles at a time, so no partial sums cross waves.  The four tiles'
+// column sums and lists go to LDS; thread b then folds bucket b over the four tiles in tile
+// order (the same order as the one-tile form; the column sums add each tile's rows in one wave's
+// order instead of four waves' interleaved order).  Two barriers per four tiles instead of three
+// per tile.
+template <bool MOM, int G, bool VEC>
 __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tabL) {
   constexpr int U = 8;
   const int m = s.m;
@@ -1007,9 +1008,14 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
   const int32_t* prow = s.perm + static_cast<int64_t>(a) * s.cap;
   const bool patched = s.patch_rowptr != nullptr;
   double* cs = lds;                    // [4][520]: the four tiles' column sums and sentinels
-  double fS[G];
+  double* csw = lds + 4 * 520;         // [4][520]: row-weighted column sums (moments)
+  double fS[G], fR[G], fT[G];
 #pragma unroll
-  for (int g = 0; g < G; ++g) fS[g] = 0.0;
+  for (int g = 0; g < G; ++g) {
+    fS[g] = 0.0;
+    fR[g] = 0.0;
+    fT[g] = 0.0;
+  }
   for (int tq = t0; tq < t1; tq += 4) {
     const int t = tq + w;
     const bool tok = t < t1;
@@ -1019,9 +1025,12 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
     const u32x4 tv = tok ? *reinterpret_cast<const u32x4*>(s.ctab + static_cast<int64_t>(t) * 512 +
                                                            lane * 8)
                          : u32x4{0u, 0u, 0u, 0u};
-    double acc[8];
+    double acc[8], accw[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) acc[k] = 0.0;
+    for (int k = 0; k < 8; ++k) {
+      acc[k] = 0.0;
+      accw[k] = 0.0;
+    }
     if (tok) {
       for (int base = 0; base < s.cap; base += 64) {
         const int32_t pe = base + lane < s.cap ? prow[base + lane] : -1;
@@ -1029,7 +1038,7 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
         if (nr == 0) break;
         for (int r0 = 0; r0 < nr; r0 += U) {
           f32x4 v0[U], v1[U];
-          double sg[U];
+          double sg[U], sw[U];
           int64_t rows[U];
 #pragma unroll
           for (int q = 0; q < U; ++q) {
@@ -1038,6 +1047,7 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
             const int64_t row = e & 0x7fffffff;
             rows[q] = row;
             sg[q] = ok ? (e < 0 ? -1.0 : 1.0) : 0.0;
+            sw[q] = MOM ? sg[q] * static_cast<double>(row + 1) * s.inv_l1 : 0.0;
             if (VEC) {
               load8f_sel(s.C + row * s.n3 + col, ok && lane_ok, s.zero, v0[q], v1[q]);
             } else if (ok && lane_ok) {
@@ -1059,14 +1069,21 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
             for (int e = 0; e < 8; ++e) {
               const double x = static_cast<double>(e < 4 ? v0[q][e] : v1[q][e - 4]);
               acc[e] = fma(x, sg[q], acc[e]);
+              if (MOM) accw[e] = fma(x, sw[q], accw[e]);
             }
           }
         }
       }
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) cs[w * 520 + lane * 8 + e] = acc[e];
-    if (lane == 0) cs[w * 520 + kColTile] = 0.0;
+    for (int e = 0; e < 8; ++e) {
+      cs[w * 520 + lane * 8 + e] = acc[e];
+      if (MOM) csw[w * 520 + lane * 8 + e] = accw[e];
+    }
+    if (lane == 0) {
+      cs[w * 520 + kColTile] = 0.0;
+      if (MOM) csw[w * 520 + kColTile] = 0.0;
+    }
     *reinterpret_cast<u32x4*>(tabL + w * 512 + lane * 8) = tv;
     // segment starts of this thread's buckets in the four tiles, all loads issued at once
     int qb[G][4], qe[G][4];
@@ -1091,7 +1108,14 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
           const uint32_t ez = tabL[ti * 512 + q];
           const int cc = ez & 0x7fff;
           const double sgd = (ez & 0x8000u) ? -1.0 : 1.0;
-          fS[g] += sgd * cs[ti * 520 + cc];
+          const double x = sgd * cs[ti * 520 + cc];
+          fS[g] += x;
+          if (MOM) {
+            const double wj =
+                static_cast<double>(static_cast<int64_t>(tq + ti) * kColTile + cc + 1) * s.inv_l3;
+            fT[g] = fma(x, wj, fT[g]);
+            fR[g] += sgd * csw[ti * 520 + cc];
+          }
         }
       }
     }
@@ -1100,7 +1124,14 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     const int b = threadIdx.x + kThreads * g;
-    if (b < m) s.partS[(static_cast<int64_t>(gi) * m + a) * m + b] = fS[g];
+    if (b < m) {
+      const int64_t o = (static_cast<int64_t>(gi) * m + a) * m + b;
+      s.partS[o] = fS[g];
+      if (MOM) {
+        s.partR[o] = fR[g];
+        s.partT[o] = fT[g];
+      }
+    }
   }
 }
 
@@ -1124,9 +1155,9 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
   int u = blockIdx.x;
   if (u < s.nC) {
     FPSK_WG_STAMP(0);
-    if constexpr (!MOM && G >= 2 && G <= 4) {
+    if constexpr (G >= 2 && G <= 4) {
       if (s.wt_c) {
-        c_unit_wt<G, VEC>(s, u, lds_dyn, tabL);
+        c_unit_wt<MOM, G, VEC>(s, u, lds_dyn, tabL);
         return;
       }
     }
