@@ -469,6 +469,18 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   // m = 400: 82.5 -> 59.2 us).  The 512-entry tile lists of m > 256 let one 16-byte load per
   // thread stage all four; m <= 1024 keeps the fold's segment starts (8 G) in registers.
   d.wt_c = m > 256 && m <= 1024 && n1 <= 32 * static_cast<int64_t>(m) && d.tg >= 4;
+  // The same at 48 < m <= 192 for the probe with B as stored and whole 16-byte rows (the
+  // instance with 4-row B work-groups; its unaligned form would spill): column groups of 4 tiles
+  // instead of about 1024 / m groups, the padded 8-entry lists staged after the column sums
+  // (2048 x 4096 x 12288 at m = 80: stream pass 43.3 -> 41.5 us; 2048 x 8192 x 8192 at m = 64:
+  // 45.3 -> 43.8 us).
+  if (!mom && !transb && m > 48 && m <= 192 && n1 <= 32 * static_cast<int64_t>(m) &&
+      d.TC >= 4 && n2 % 8 == 0 && n3 % 8 == 0) {
+    d.wt_c = true;
+    d.npc = (d.TC + 3) / 4;
+    d.tg = (d.TC + d.npc - 1) / d.npc;
+    d.nC = m * d.npc;
+  }
   // Bucket-space product on the matrix cores, tiles of ts x ts outputs over NS k-slices.
   // Without moments: 16 x 16 tiles whose k-range the 4 waves split, while there are fewer than
   // 256 of them (slices for about 2048 waves); else 64 x 64 tiles of four 32 x 32 wave quadrants.
@@ -505,7 +517,12 @@ Decomp decompose(int64_t n1, int64_t n2, int64_t n3, int m, bool mom, bool trans
   const size_t comb = (mom ? 4096 : 2048) * sizeof(double);
   const size_t cs = (mom ? 1040 : 520) * sizeof(double);
   const size_t bdata = (static_cast<size_t>(d.cwb) * d.rb + d.rb) * sizeof(uint16_t);
-  const size_t wtc = d.wt_c ? (mom ? 8 : 4) * 520 * sizeof(double) : 0;   // 4 tiles' column sums
+  // one-tile-per-wave C work-groups: four tiles' column sums (and weighted sums), and at
+  // m <= 256 the four padded tile lists
+  const size_t wtc =
+      d.wt_c ? (mom ? 8 : 4) * 520 * sizeof(double) +
+                   (m <= 256 ? 4 * static_cast<size_t>(d.ctab_stride) * sizeof(uint16_t) : 0)
+             : 0;
   const size_t data = (std::max({comb + cs, bdata, wtc}) + 15) / 16 * 16;
   d.tab_off = static_cast<int>(data);
   // (the probe's B group fold, 8-row work-groups up to m = 256, stages the m + 1 segment

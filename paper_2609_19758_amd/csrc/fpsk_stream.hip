@@ -990,16 +990,20 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
   }
 }
 
-// C work-group with one column tile per wave (256 < m <= 1024, whose tile lists hold 512
-// entries): wave w sums all of bucket a's rows over tile tq + w (and, with moments, the
-// row-weighted sums), four tiles at a time, so no partial sums cross waves.  The four tiles'
-// column sums and lists go to LDS; thread b then folds bucket b over the four tiles in tile
-// order (the same order as the one-tile form; the column sums add each tile's rows in one wave's
-// order instead of four waves' interleaved order).  Two barriers per four tiles instead of three
-// per tile.
+// C work-group with one column tile per wave (small buckets at 256 < m <= 1024, and at
+// 48 < m <= 192 for the probe): wave w sums all of bucket a's rows over tile tq + w (and, with
+// moments, the row-weighted sums), four tiles at a time, so no partial sums cross waves.  The four
+// tiles' column sums and lists go to LDS (the 512-entry lists of m > 256 in the list area, one
+// 16-byte load per thread, loaded with the first rows; the padded lists of m <= 256 after the
+// column sums, loaded once the rows are summed); thread b then folds bucket b over the four tiles
+// in tile order (the same order as the one-tile form; the column sums add each tile's rows in one
+// wave's order instead of four waves' interleaved order).  Two barriers per four tiles instead of
+// three per tile.
 template <bool MOM, int G, bool VEC>
 __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tabL) {
   constexpr int U = 8;
+  constexpr int PADG = G == 1 ? 8 : 1;         // padded 8-entry segments at m <= 256
+  static_assert(!(MOM && G == 1), "the padded lists and weighted sums exceed the data area");
   const int m = s.m;
   const int a = u / s.npc, gi = u - a * s.npc;
   const int t0 = gi * s.tg;
@@ -1009,6 +1013,9 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
   const bool patched = s.patch_rowptr != nullptr;
   double* cs = lds;                    // [4][520]: the four tiles' column sums and sentinels
   double* csw = lds + 4 * 520;         // [4][520]: row-weighted column sums (moments)
+  // the four tiles' lists: 512-entry lists in the list area; padded lists after the column sums
+  const int stride = s.ctab_stride;
+  uint16_t* lists = PADG == 8 ? reinterpret_cast<uint16_t*>(lds + 4 * 520) : tabL;
   double fS[G], fR[G], fT[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
@@ -1022,9 +1029,10 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
     const int64_t col = static_cast<int64_t>(t) * kColTile + lane * 8;
     const bool lane_ok = tok && col < s.n3;
     // this wave's tile list (512 entries, 8 per lane), loaded with the first rows
-    const u32x4 tv = tok ? *reinterpret_cast<const u32x4*>(s.ctab + static_cast<int64_t>(t) * 512 +
-                                                           lane * 8)
-                         : u32x4{0u, 0u, 0u, 0u};
+    u32x4 tv = {0u, 0u, 0u, 0u};
+    if (PADG == 1 && tok) {
+      tv = *reinterpret_cast<const u32x4*>(s.ctab + static_cast<int64_t>(t) * 512 + lane * 8);
+    }
     double acc[8], accw[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -1084,7 +1092,20 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
       cs[w * 520 + kColTile] = 0.0;
       if (MOM) csw[w * 520 + kColTile] = 0.0;
     }
-    *reinterpret_cast<u32x4*>(tabL + w * 512 + lane * 8) = tv;
+    if (PADG == 1) {
+      *reinterpret_cast<u32x4*>(lists + w * 512 + lane * 8) = tv;
+    } else {
+      // the four padded lists, 8 entries per thread and pass
+      for (int e = threadIdx.x * 8; e < 4 * stride; e += kThreads * 8) {
+        const int ti = e / stride, off = e - ti * stride;
+        const u32x4 x =
+            tq + ti < t1
+                ? *reinterpret_cast<const u32x4*>(s.ctab + static_cast<int64_t>(tq + ti) * stride +
+                                                  off)
+                : u32x4{0u, 0u, 0u, 0u};
+        *reinterpret_cast<u32x4*>(lists + e) = x;
+      }
+    }
     // segment starts of this thread's buckets in the four tiles, all loads issued at once
     int qb[G][4], qe[G][4];
 #pragma unroll
@@ -1104,17 +1125,27 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
     for (int g = 0; g < G; ++g) {
 #pragma unroll
       for (int ti = 0; ti < 4; ++ti) {
-        for (int q = qb[g][ti]; q < qe[g][ti]; ++q) {
-          const uint32_t ez = tabL[ti * 512 + q];
-          const int cc = ez & 0x7fff;
-          const double sgd = (ez & 0x8000u) ? -1.0 : 1.0;
-          const double x = sgd * cs[ti * 520 + cc];
-          fS[g] += x;
-          if (MOM) {
-            const double wj =
-                static_cast<double>(static_cast<int64_t>(tq + ti) * kColTile + cc + 1) * s.inv_l3;
-            fT[g] = fma(x, wj, fT[g]);
-            fR[g] += sgd * csw[ti * 520 + cc];
+        for (int q = qb[g][ti]; q < qe[g][ti]; q += PADG) {
+          uint32_t ez[PADG];
+          if constexpr (PADG == 8) {
+            const u32x4 tw = *reinterpret_cast<const u32x4*>(lists + ti * stride + q);
+#pragma unroll
+            for (int z = 0; z < 8; ++z) ez[z] = (tw[z >> 1] >> (16 * (z & 1))) & 0xffffu;
+          } else {
+            ez[0] = lists[ti * 512 + q];
+          }
+#pragma unroll
+          for (int z = 0; z < PADG; ++z) {
+            const int cc = ez[z] & 0x7fff;
+            const double sgd = (ez[z] & 0x8000u) ? -1.0 : 1.0;
+            const double x = sgd * cs[ti * 520 + cc];
+            fS[g] += x;
+            if (MOM) {
+              const double wj =
+                  static_cast<double>(static_cast<int64_t>(tq + ti) * kColTile + cc + 1) * s.inv_l3;
+              fT[g] = fma(x, wj, fT[g]);
+              fR[g] += sgd * csw[ti * 520 + cc];
+            }
           }
         }
       }
@@ -1139,7 +1170,9 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
 // then the sorted column list of the current B chunk or C tile.  The longer lists of B chunks
 // with fewer rows hold the probe to 3 (2 or 4 rows) or 2 (1 row) work-groups per CU, so those
 // instances may use the registers of that occupancy instead of spilling at 4's 128.
-template <int DT, bool MOM, int RB, int G, int NG, bool VEC>
+// WTC: C work-groups of one tile per wave (c_unit_wt) in place of the one-tile form, as its own
+// instance so that the others keep their code and registers.
+template <int DT, bool MOM, int RB, int G, int NG, bool VEC, bool WTC>
 __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1)) ? 4 : (RB >= 2 ? 3 : 2))) void stream_kernel(
     StreamArgs s) {
   extern __shared__ double lds_dyn[];
@@ -1155,13 +1188,11 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
   int u = blockIdx.x;
   if (u < s.nC) {
     FPSK_WG_STAMP(0);
-    if constexpr (G >= 2 && G <= 4) {
-      if (s.wt_c) {
-        c_unit_wt<MOM, G, VEC>(s, u, lds_dyn, tabL);
-        return;
-      }
+    if constexpr (WTC) {
+      c_unit_wt<MOM, G, VEC>(s, u, lds_dyn, tabL);
+    } else {
+      c_unit<MOM, G, VEC>(s, u, lds_dyn, tabL);
     }
-    c_unit<MOM, G, VEC>(s, u, lds_dyn, tabL);
     return;
   }
   u -= s.nC;
@@ -1192,7 +1223,7 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
 // products start at a multiple of 8 so that their XCD-local slots hold, and come last so that
 // they fill the stream pass's tail.  The decision uses the kernel's 256 threads over
 // kDecideThreads virtual threads: the same bits as the stand-alone decision.
-template <int DT, bool VEC, int XB>
+template <int DT, bool VEC, int XB, bool WTC>
 __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, ProductArgs prod,
                                                                  ProductArgs dec, int nprod,
                                                                  int has_dec) {
@@ -1212,7 +1243,11 @@ __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, P
   if (u >= s.nC + s.nB + s.nA) return;
   uint16_t* tabL = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(lds_dyn) + s.tab_off);
   if (u < s.nC) {
-    c_unit<false, 1, VEC>(s, u, lds_dyn, tabL);
+    if constexpr (WTC) {
+      c_unit_wt<false, 1, VEC>(s, u, lds_dyn, tabL);
+    } else {
+      c_unit<false, 1, VEC>(s, u, lds_dyn, tabL);
+    }
     return;
   }
   u -= s.nC;
@@ -1236,23 +1271,23 @@ size_t probe_pipe_lds(int xb) {
   return (prod > dec ? prod : dec) * sizeof(double);
 }
 
-template <int DT, bool VEC, int XB>
+template <int DT, bool VEC, int XB, bool WTC>
 static void pipe_launch(const StreamArgs& s, const ProductArgs& prod, const ProductArgs& dec,
                         int nprod, int has_dec, size_t lds, hipStream_t st, hipEvent_t e0,
                         hipEvent_t e1) {
   const dim3 grid(8 + (s.nC + s.nB + s.nA + 7) / 8 * 8 + nprod);
-  launch_k(probe_pipe_kernel<DT, VEC, XB>, grid, dim3(kThreads), lds, st, e0, e1, s, prod, dec,
-           nprod, has_dec);
+  launch_k(probe_pipe_kernel<DT, VEC, XB, WTC>, grid, dim3(kThreads), lds, st, e0, e1, s, prod,
+           dec, nprod, has_dec);
 }
 
-template <int DT, bool VEC>
+template <int DT, bool VEC, bool WTC>
 static hipError_t pipe_dispatch(const StreamArgs& s, const ProductArgs& prod,
                                 const ProductArgs& dec, int nprod, int has_dec, int xb,
                                 size_t lds, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   switch (xb) {
-    case 1: pipe_launch<DT, VEC, 1>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
-    case 2: pipe_launch<DT, VEC, 2>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
-    case 3: pipe_launch<DT, VEC, 3>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
+    case 1: pipe_launch<DT, VEC, 1, WTC>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
+    case 2: pipe_launch<DT, VEC, 2, WTC>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
+    case 3: pipe_launch<DT, VEC, 3, WTC>(s, prod, dec, nprod, has_dec, lds, st, e0, e1); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1262,12 +1297,22 @@ hipError_t launch_probe_pipe(const StreamArgs& s, const ProductArgs& prod, const
                              int nprod, int has_dec, int dt, int xb, size_t lds_bytes,
                              hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   const bool vec = s.vec_a && s.vec_b && s.vec_c;
-  if (dt == 1) {
-    return vec ? pipe_dispatch<1, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1)
-               : pipe_dispatch<1, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1);
+  // (one-tile-per-wave C work-groups only with whole 16-byte rows, as in the stream kernel)
+  if (vec && s.wt_c) {
+    return dt == 1
+               ? pipe_dispatch<1, true, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1)
+               : pipe_dispatch<0, true, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1);
   }
-  return vec ? pipe_dispatch<0, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1)
-             : pipe_dispatch<0, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1);
+  if (dt == 1) {
+    return vec ? pipe_dispatch<1, true, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0,
+                                               e1)
+               : pipe_dispatch<1, false, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st,
+                                                e0, e1);
+  }
+  return vec ? pipe_dispatch<0, true, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0,
+                                             e1)
+             : pipe_dispatch<0, false, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0,
+                                              e1);
 }
 
 // ----------------------------------------------------------------------------------------
@@ -1279,17 +1324,38 @@ static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, int ng, si
   const int grid = s.nA + s.nB + s.nC;
   if (grid <= 0) return hipSuccess;
   const bool vec = s.vec_a && s.vec_b && s.vec_c;
+  // one-tile-per-wave C work-groups: their own instances (at G = 1 only the probe's aligned one)
+  const bool wtc = s.wt_c && !(g == 1 && (MOM || !vec));
+#define FPSK_STREAM_LAUNCH(RB_, G_, NG_, VEC_, WTC_)                                          \
+  launch_k(stream_kernel<DT, MOM, RB_, G_, NG_, VEC_, WTC_>, dim3(grid), dim3(kThreads), lds, st, \
+           e0, e1, s)
 #define FPSK_STREAM_CASE(RB_, G_, NG_)                                                        \
   if (rb == RB_ && g == G_ && ng == NG_) {                                                    \
     if (vec) {                                                                                \
-      launch_k(stream_kernel<DT, MOM, RB_, G_, NG_, true>, dim3(grid), dim3(kThreads), lds,   \
-               st, e0, e1, s);                                                                \
+      FPSK_STREAM_LAUNCH(RB_, G_, NG_, true, false);                                          \
     } else {                                                                                  \
-      launch_k(stream_kernel<DT, MOM, RB_, G_, NG_, false>, dim3(grid), dim3(kThreads), lds,  \
-               st, e0, e1, s);                                                                \
+      FPSK_STREAM_LAUNCH(RB_, G_, NG_, false, false);                                         \
     }                                                                                         \
     return hipGetLastError();                                                                 \
   }
+#define FPSK_STREAM_WTC_CASE(RB_, G_, NG_)                                                    \
+  if (wtc && rb == RB_ && g == G_ && ng == NG_) {                                             \
+    if (vec) {                                                                                \
+      FPSK_STREAM_LAUNCH(RB_, G_, NG_, true, true);                                           \
+    } else {                                                                                  \
+      FPSK_STREAM_LAUNCH(RB_, G_, NG_, false, true);                                          \
+    }                                                                                         \
+    return hipGetLastError();                                                                 \
+  }
+  if constexpr (!MOM) {
+    if (wtc && rb == 4 && g == 1 && ng == 1) {
+      FPSK_STREAM_LAUNCH(4, 1, 1, true, true);
+      return hipGetLastError();
+    }
+  }
+  FPSK_STREAM_WTC_CASE(4, 2, 1)
+  FPSK_STREAM_WTC_CASE(8, 2, 1)
+  FPSK_STREAM_WTC_CASE(4, 4, 1)
   FPSK_STREAM_CASE(8, 1, 4)
   FPSK_STREAM_CASE(8, 1, 2)
   FPSK_STREAM_CASE(8, 1, 1)
@@ -1300,6 +1366,8 @@ static hipError_t stream_dispatch(const StreamArgs& s, int rb, int g, int ng, si
   FPSK_STREAM_CASE(2, 8, 1)
   FPSK_STREAM_CASE(1, 16, 1)
 #undef FPSK_STREAM_CASE
+#undef FPSK_STREAM_WTC_CASE
+#undef FPSK_STREAM_LAUNCH
   return hipErrorInvalidValue;
 }
 
