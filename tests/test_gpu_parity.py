@@ -48,6 +48,8 @@ EXACT_CASES = [
     (300, 1030, 700, 600, "fp16"),      # RB = 4 over 258 row blocks: XCD-grouped order, ragged
     (300, 24, 6145, 300, "bf16"),       # C tiles one per wave, element loads, last group 1 tile
     (2000, 8, 7000, 1000, "fp16"),      # C tiles one per wave, G = 4, 7 tiles per group
+    (1000, 64, 2560, 100, "bf16"),      # C tiles one per wave at m <= 192: padded lists, 3 tiles
+    (600, 40, 4104, 160, "fp16"),       # the same over 9 tiles (groups of 3, the last partial)
     (400, 16, 3000, 1500, "bf16"),      # RB = 2, G = 8
     (700, 8, 5000, 4096, "fp16"),       # RB = 1, G = 16, m at the limit
     (2100, 520, 1030, 48, "bf16"),      # several A/C tiles and a ragged tail
