@@ -1095,15 +1095,22 @@ __device__ void c_unit_wt(const StreamArgs& s, int u, double* lds, uint16_t* tab
     if (PADG == 1) {
       *reinterpret_cast<u32x4*>(lists + w * 512 + lane * 8) = tv;
     } else {
-      // the four padded lists, 8 entries per thread and pass
-      for (int e = threadIdx.x * 8; e < 4 * stride; e += kThreads * 8) {
+      // the four padded lists (at most 4 x 1856 entries at m <= 192): 8 entries per thread and
+      // pass, every pass's load issued before the first store
+      u32x4 x[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = (threadIdx.x + kThreads * k) * 8;
         const int ti = e / stride, off = e - ti * stride;
-        const u32x4 x =
-            tq + ti < t1
-                ? *reinterpret_cast<const u32x4*>(s.ctab + static_cast<int64_t>(tq + ti) * stride +
-                                                  off)
-                : u32x4{0u, 0u, 0u, 0u};
-        *reinterpret_cast<u32x4*>(lists + e) = x;
+        const bool ok = e < 4 * stride && tq + ti < t1;
+        const uint16_t* src =
+            s.ctab + static_cast<int64_t>(ok ? tq + ti : 0) * stride + (ok ? off : 0);
+        x[k] = ok ? *reinterpret_cast<const u32x4*>(src) : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int e = (threadIdx.x + kThreads * k) * 8;
+        if (e < 4 * stride) *reinterpret_cast<u32x4*>(lists + e) = x[k];
       }
     }
     // segment starts of this thread's buckets in the four tiles, all loads issued at once
@@ -1299,9 +1306,10 @@ hipError_t launch_probe_pipe(const StreamArgs& s, const ProductArgs& prod, const
   const bool vec = s.vec_a && s.vec_b && s.vec_c;
   // (one-tile-per-wave C work-groups only with whole 16-byte rows, as in the stream kernel)
   if (vec && s.wt_c) {
-    return dt == 1
-               ? pipe_dispatch<1, true, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1)
-               : pipe_dispatch<0, true, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0, e1);
+    return dt == 1 ? pipe_dispatch<1, true, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st,
+                                                  e0, e1)
+                   : pipe_dispatch<0, true, true>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st,
+                                                  e0, e1);
   }
   if (dt == 1) {
     return vec ? pipe_dispatch<1, true, false>(s, prod, dec, nprod, has_dec, xb, lds_bytes, st, e0,
