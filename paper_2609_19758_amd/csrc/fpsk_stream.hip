@@ -864,10 +864,15 @@ __device__ void c_unit(const StreamArgs& s, int u, double* lds, uint16_t* tabL) 
       tv[it] = o < stride ? *reinterpret_cast<const u32x4*>(ctab + o) : u32x4{0u, 0u, 0u, 0u};
     }
     const int32_t* coff = s.coff + static_cast<int64_t>(t) * (m + 1);
+    // (the thread index is opaque here, so the compiler does not hoist the per-thread address
+    // out of the tile loop: that 64-bit pointer was the instance's only spill, and its reload
+    // waited on the tile's list load before the segment starts and rows could be issued)
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
     int qb[G], qe[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const int b = threadIdx.x + kThreads * g;
+      const int b = tid + kThreads * g;
       qb[g] = b < m ? coff[b] : 0;
       qe[g] = b < m ? coff[b + 1] : 0;
     }
