@@ -91,7 +91,13 @@ def site_recompute(a_bits, b_bits, fmt: str, sites):
 # the sources the probe's stream kernel is built from (its counters stay valid while these do)
 KERNEL_SRC = [os.path.join(ROOT, "paper_2609_19758_amd", "csrc", f)
               for f in ("fpsk_stream.hip", "fpsk_device.h", "fpsk_internal.h", "fpsk_block.h")]
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "stream_kernel_square4096_bf16_pmc.txt")
+DEFAULT_WORKLOAD = "square4096_bf16"
+DEFAULT_SETS = 4
+
+
+def pmc_summary_path(workload: str) -> str:
+    """The committed HBM-traffic summary of the probe's stream kernel on this workload."""
+    return os.path.join(ROOT, "profiles", f"stream_kernel_{workload}_pmc.txt")
 
 
 def kernel_source_hash() -> str:
@@ -107,7 +113,7 @@ def traffic_from_summary(workload: str):
     """HBM bytes per stream-kernel launch from the committed counter summary, or None when the
     summary is missing, covers another workload or was taken on other kernel sources."""
     try:
-        with open(PMC_SUMMARY) as f:
+        with open(pmc_summary_path(workload)) as f:
             kv = dict(line.split("=", 1) for line in f.read().splitlines()
                       if "=" in line and not line.startswith("#"))
     except OSError:
@@ -168,35 +174,40 @@ def _counter_means(db_path: str, counter: str) -> dict:
     return {n: (statistics.mean(dv.values()), len(dv)) for n, dv in per.items()}
 
 
-def write_pmc_summary(workload: str, fetch_db: str, write_db: str) -> int:
+def write_pmc_summary(workload: str, sets: int, fetch_db: str, write_db: str) -> int:
     """HBM bytes per launch of the probe's stream kernel: FETCH_SIZE and WRITE_SIZE (KiB per
-    dispatch) scaled by what they read for the plain copy kernel of known size."""
+    dispatch) scaled by what they read for the plain copy kernel of known size.  workload and
+    sets are those of the two counter runs (named in the summary's commands)."""
     from paper_2609_19758_amd import workloads as wl
     w = wl.workload(workload)
     fetch, write = _counter_means(fetch_db, "FETCH_SIZE"), _counter_means(write_db, "WRITE_SIZE")
-    stream = [n for n in fetch if "stream_kernel<" in n and ", false," in n]
+    # the probe's stream kernel instances (no moments); a run-time calibration probe at another
+    # m can add a second instance with a few dispatches: the timed calls' instance has the most
+    stream = [n for n in fetch if "stream_kernel<" in n and ", false," in n and n in write]
     copy = [n for n in fetch if "copy_kernel" in n]
-    if len(stream) != 1 or len(copy) != 1:
-        print(f"expected one probe stream kernel and one copy kernel, got {stream} {copy}",
+    if not stream or len(copy) != 1:
+        print(f"expected a probe stream kernel and one copy kernel, got {stream} {copy}",
               file=sys.stderr)
         return 1
-    sk, ck = stream[0], copy[0]
+    sk, ck = max(stream, key=lambda n: fetch[n][1]), copy[0]
     copy_kib = 256 * 1024                  # --copy-calibration 256: 256 MiB read and written
     fs, ws = copy_kib / fetch[ck][0], copy_kib / write[ck][0]
     traffic = (fetch[sk][0] * fs + write[sk][0] * ws) * 1024.0
     # the run directories as given, relative to the repository root
     fdir = os.path.relpath(os.path.dirname(os.path.abspath(fetch_db)), ROOT)
     wdir = os.path.relpath(os.path.dirname(os.path.abspath(write_db)), ROOT)
+    wargs = "" if workload == DEFAULT_WORKLOAD else f" --workload {workload}"
+    wargs += "" if sets == DEFAULT_SETS else f" --sets {sets}"
     lines = [
         f"# HBM traffic of the FP-Sketch probe's stream kernel, {workload}",
         "# commands (from /tmp, repo at $R), one counter per run:",
-        f"#   rocprofv3 --pmc FETCH_SIZE -d $R/{fdir} -o run -- python3 $R/bench.py "
+        f"#   rocprofv3 --pmc FETCH_SIZE -d $R/{fdir} -o run -- python3 $R/bench.py{wargs} "
         "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --probe-only "
         "--copy-calibration 256",
-        f"#   rocprofv3 --pmc WRITE_SIZE -d $R/{wdir} -o run -- python3 $R/bench.py "
+        f"#   rocprofv3 --pmc WRITE_SIZE -d $R/{wdir} -o run -- python3 $R/bench.py{wargs} "
         "--steps 20 --warmup 5 --no-cpu-baseline --recovery-calls 0 --probe-only "
         "--copy-calibration 256",
-        f"#   python3 bench.py --write-pmc-summary {fdir}/run_results.db "
+        f"#   python3 bench.py{wargs} --write-pmc-summary {fdir}/run_results.db "
         f"{wdir}/run_results.db",
         "# scale: the copy kernel moves 262144 KiB in and 262144 KiB out per dispatch",
         f"workload={workload}",
@@ -215,8 +226,9 @@ def write_pmc_summary(workload: str, fetch_db: str, write_db: str) -> int:
         f"algorithmic_bytes_per_launch={w.bytes_abc}",
         f"traffic_over_algorithmic={traffic / w.bytes_abc:.4f}",
     ]
-    os.makedirs(os.path.dirname(PMC_SUMMARY), exist_ok=True)
-    with open(PMC_SUMMARY, "w") as f:
+    out = pmc_summary_path(workload)
+    os.makedirs(os.path.dirname(out), exist_ok=True)
+    with open(out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
     return 0
@@ -467,8 +479,8 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="square4096_bf16")
-    ap.add_argument("--sets", type=int, default=4)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--sets", type=int, default=DEFAULT_SETS)
     ap.add_argument("--recovery-calls", type=int, default=4)
     ap.add_argument("--probe-only", action="store_true",
                     help="time and profile the ordinary probe only (no graph, deferred, "
@@ -492,7 +504,7 @@ def main() -> int:
     if args.summarize:
         return summarize_db(args.summarize)
     if args.write_pmc_summary:
-        return write_pmc_summary(args.workload, *args.write_pmc_summary)
+        return write_pmc_summary(args.workload, args.sets, *args.write_pmc_summary)
     if args.gpus != 1:
         print(f"bench.py: this verifier runs on one GPU; --gpus {args.gpus} is not supported "
               "(no sharded path is built)", file=sys.stderr)
