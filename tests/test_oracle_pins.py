@@ -425,9 +425,9 @@ def test_window_order():
 # --- additional pins (each targets a specific plausible slip) ------------------------------
 
 def test_hash_word_reduction_on_published_outputs():
-    """The hash spec reduces each splitmix64 output word x to bucket (x >> 32) * m >> 32 and
-    sign -1 iff bit 0 of x is set; the words here are the published outputs for state 1234567,
-    which the spec takes as the words of indices 0..4 of a stream keyed with 1234567."""
+    """The hash reduces each splitmix64 output word x to bucket (x >> 32) * m >> 32 and sign -1
+    iff bit 0 of x is set; the words here are the published outputs for state 1234567, which are
+    the words of indices 0..4 of the stream keyed with 1234567."""
     rows = [r for r in load_golden("splitmix64_vectors.csv") if r["seed"] == "1234567"]
     words = [int(r["output"]) for r in rows]
     got_x = o.splitmix64_stream(1234567, np.arange(5, dtype=np.uint64))
