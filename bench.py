@@ -493,7 +493,8 @@ def main() -> int:
     ap.add_argument("--write-pmc-summary", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
                     help="write the HBM traffic summary of the probe's stream kernel from two "
                          "rocprofv3 --pmc databases (FETCH_SIZE, WRITE_SIZE) of a run with "
-                         "--copy-calibration, and exit")
+                         "--copy-calibration (and the same --workload and --sets) to "
+                         "profiles/stream_kernel_<workload>_pmc.txt, and exit")
     ap.add_argument("--wg-timeline", action="store_true",
                     help="print the per-work-group timeline of the probe's stream kernel from "
                          "the diagnostic build (libfpsketch_timeline.so) and exit; --steps "
