@@ -82,6 +82,9 @@ struct StreamArgs {
   // C work-groups with one column tile per wave, four tiles at a time (256 < m <= 1024,
   // buckets of at most 32 rows, at least 4 tiles per work-group)
   int wt_c;
+  // the 4-row probe B work-groups of the one-tile-per-wave instances start at chunk
+  // (row block mod TB) and wrap (n3 a whole number of chunks, TB > 1)
+  int rot_b;
   double inv_l1, inv_l3;      // 1 / 2^ceil(log2 n1), 1 / 2^ceil(log2 n3)
   int vec_a, vec_b, vec_c;    // 16-byte vector loads allowed
   const void* zero;           // >= 64 bytes of zeros (read in place of invalid rows or lanes)

@@ -683,7 +683,12 @@ __device__ void b_unit(const StreamArgs& s, int u, uint16_t* L, uint16_t* tabL, 
 // small; thread t sums the 8 columns of its groups t, t + 256, ... in FP32, the group partials
 // replace the staged data, and thread t then adds the partials of buckets t, t + 256, ... (G of
 // them) in FP64.  At the end each bucket's Q[b, k0 .. k0 + 3] is one 16-byte store.
-template <int DT, bool VEC, int G>
+// ROT (the instances with one-tile-per-wave C work-groups): with rot_b the chunks are taken
+// from (row block mod TB) on, wrapping around, so that the work-groups in flight read
+// different column ranges of their rows (2048 x 8192 x 8192 at m = 64: stream pass 43.8 ->
+// 42.2 us).  The other instance, the 4096^3 one among them, is compiled without it: the index
+// arithmetic cost it 0.1 us per pass with a single chunk.
+template <int DT, bool VEC, int G, bool ROT>
 __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t* ldsu) {
   constexpr int RB = 4;
   constexpr int CW = kBChunkHalfs / RB;          // 4096 columns per chunk
@@ -696,7 +701,8 @@ __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t*
   const int m = s.m;
   const int stride = s.btab_stride;              // multiple of 8, at most 8 NGT kThreads
   const int t = threadIdx.x;
-  const int64_t k0 = static_cast<int64_t>(b_block<RB>(u, s.nB)) * RB;
+  const int rbk = b_block<RB>(u, s.nB);
+  const int64_t k0 = static_cast<int64_t>(rbk) * RB;
   int32_t* boffL = reinterpret_cast<int32_t*>(L + CW * RB + 8);   // after the zero column
   float* PL = reinterpret_cast<float*>(L);       // group partials, over the staged data
   if (t < RB) L[CW * RB + t] = 0;                // zero sentinel column (slot CW)
@@ -707,7 +713,9 @@ __device__ void b_unit_probe4(const StreamArgs& s, int u, uint16_t* L, uint32_t*
     for (int r = 0; r < RB; ++r) q[g][r] = 0.0;
   uint32_t mx = 0;
   const u32x4 sent = {0x10001000u, 0x10001000u, 0x10001000u, 0x10001000u};   // 8 x slot CW
-  for (int c = 0; c < s.TB; ++c) {
+  const int rot = (ROT && s.rot_b) ? rbk % s.TB : 0;
+  for (int i = 0; i < s.TB; ++i) {
+    const int c = i + rot < s.TB ? i + rot : i + rot - s.TB;   // chunk (rot + i) mod TB
     const int64_t cbase = static_cast<int64_t>(c) * CW;
     u32x4 v[NI][RB];
     uint32_t sb[NI];
@@ -1218,7 +1226,7 @@ __global__ __launch_bounds__(kThreads, MOM ? 2 : ((RB == 8 || (RB == 4 && G == 1
   if (s.transb) {
     row_unit<DT, MOM, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
   } else if constexpr (RB == 4 && G <= 2 && !MOM) {
-    b_unit_probe4<DT, VEC, G>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
+    b_unit_probe4<DT, VEC, G, WTC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
   } else {
     b_unit<DT, MOM, RB, G, NG, VEC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), tabL, ldsu);
   }
@@ -1271,7 +1279,7 @@ __global__ __launch_bounds__(kThreads, 4) void probe_pipe_kernel(StreamArgs s, P
   if (s.transb) {
     row_unit<DT, false, VEC>(s, w_side(s), s.wt_w != 0, u, lds_dyn, ldsu);
   } else {
-    b_unit_probe4<DT, VEC, 1>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
+    b_unit_probe4<DT, VEC, 1, WTC>(s, u, reinterpret_cast<uint16_t*>(lds_dyn), ldsu);
   }
 }
 
