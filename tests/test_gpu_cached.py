@@ -25,6 +25,7 @@ def fk():
     (512, 256, 384, 48, "bf16"),      # block path
     (640, 320, 512, 96, "fp16"),      # tile path
     (130, 37, 131, 7, "bf16"),        # element loads (rows not multiples of 8)
+    (600, 64, 8192, 64, "bf16"),      # B chunks in rotated order (two whole chunks)
 ])
 def test_cached_probe_equals_streamed_probe(fk, n1, n2, n3, m, fmt):
     import torch

@@ -51,6 +51,7 @@ def _sequence(n1, n2, n3, fmt, calls, seed, bits=None):
     (300, 512, 260, 64, "fp16"),     # m > 48: 3 x 3 blocks in the pipelined launch
     (640, 4100, 520, 49, "bf16"),    # m = 49, two slices
     (600, 512, 2048, 64, "bf16"),    # C tiles one per wave in both launches
+    (600, 64, 8192, 64, "bf16"),     # B chunks in rotated order (two whole chunks)
 ])
 def test_deferred_equals_ordinary(fk, n1, n2, n3, m, fmt):
     import torch

@@ -55,6 +55,8 @@ EXACT_CASES = [
     (2100, 520, 1030, 48, "bf16"),      # several A/C tiles and a ragged tail
     (100, 37, 90, 13, "fp16"),          # small buckets (one wave per tile), element loads
     (300, 2100, 200, 64, "bf16"),       # small buckets over 5 tiles: waves past the last idle
+    (600, 64, 8192, 64, "bf16"),        # B chunks from (row block mod 2) on: two whole chunks
+    (300, 40, 12288, 100, "fp16"),      # the same over three whole chunks (every rotation)
 ]
 
 
